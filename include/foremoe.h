@@ -1,0 +1,281 @@
+/*
+ * foremoe.h - C ABI of the per-micro-step MoE expert layer on one MI355X.
+ *
+ * ForeMoE (arXiv 2606.11867) balances MoE load per micro-step by placing
+ * experts and expert replicas in "slots" (Sec. 7, Terminology) according to
+ * the routing recorded during rollout (Sec. 5, Routing Collector). This
+ * library runs what one GPU does with such a placement, in five steps:
+ *
+ *   1. foremoe_histogram        tokens per expert from the recorded top-K ids
+ *   2. foremoe_assign_replicas  contiguous split of each expert's token list
+ *                               over its replicas (token assignment r_{s,e,j},
+ *                               Sec. 7.2 and Sec. 8 Stage 4)
+ *   3. foremoe_permute          gather tokens into slot-contiguous order
+ *   4. foremoe_grouped_ffn_*    SwiGLU expert FFN over the local slots
+ *                               (App. A): forward, dgrad and wgrad; replica
+ *                               weight gradients are summed into the main
+ *                               expert (Sec. 6.2, Copy-in)
+ *   5. foremoe_combine          gate-weighted sum back to token order (Sec. 2.1)
+ *   plus foremoe_combine_bwd / foremoe_permute_bwd for the policy-update
+ *   backward (Sec. 7.1: the backward repeats dispatch and combine).
+ *
+ * Conventions (all entry points):
+ *  - Every pointer argument is a DEVICE pointer unless stated otherwise; the
+ *    caller owns every buffer. The library never allocates device memory and
+ *    keeps no state besides a per-thread error message.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream) and never synchronises the host. Sizes that depend on the
+ *    routing (N = local pairs, slot offsets) stay on the device.
+ *  - Return value: FOREMOE_OK, or a negative status. Arguments are checked
+ *    on the host before any launch; on error nothing is launched and
+ *    foremoe_last_error() describes the problem. No exception crosses the ABI.
+ *  - Layouts are row-major. Index types are int32. "bf16" is bfloat16.
+ *  - Results are deterministic: no floating-point atomics are used, so two
+ *    calls with the same inputs give bitwise identical outputs.
+ *  - Thread-safe; calls on the same buffers must be ordered by the caller.
+ */
+#ifndef FOREMOE_H
+#define FOREMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FOREMOE_OK 0
+#define FOREMOE_EINVAL (-1)       /* bad argument (null pointer, bad size)          */
+#define FOREMOE_EUNSUPPORTED (-2) /* valid but unsupported shape or dtype            */
+#define FOREMOE_EHIP (-3)         /* a HIP launch failed                             */
+
+/* Limits checked on the host. */
+#define FOREMOE_MAX_EXPERTS 1024
+#define FOREMOE_MAX_SLOTS 1024
+#define FOREMOE_MAX_REPLICAS 16
+#define FOREMOE_MAX_TOPK 64
+
+typedef enum foremoe_dtype {
+  FOREMOE_F32 = 0,
+  FOREMOE_BF16 = 1
+} foremoe_dtype;
+
+/*
+ * One micro-step's placement on this GPU (Sec. 7, Terminology; Table 1:
+ * x_{e,j} and r_{s,e,j}). A host struct whose arrays are DEVICE arrays.
+ *
+ *  E                  experts in the model, 1..FOREMOE_MAX_EXPERTS
+ *  S                  local slots, 0..FOREMOE_MAX_SLOTS
+ *  R_max              row length of expert_rep_weight, 1..FOREMOE_MAX_REPLICAS
+ *  slot_expert[S]     expert held by slot j
+ *  slot_replica[S]    which replica of that expert slot j holds (0-based)
+ *  expert_nrep[E]     replicas R_e of expert e in the whole EP group, local
+ *                     or not (1..R_max)
+ *  expert_rep_weight  [E * R_max] integer split weights (>= 0, positive sum
+ *                     over the first R_e entries), or NULL for equal split
+ *  slot_widx[S]       weight index (0..W-1) slot j computes with; a replica
+ *                     may alias its source expert's weights
+ *  slot_gidx[S]       gradient index (0..G-1) slot j accumulates into: the
+ *                     main expert of slot j's expert (Sec. 6.2)
+ *
+ * Errors in the device arrays (a slot naming an expert or replica out of
+ * range, two slots holding the same replica, a zero weight sum) cannot be
+ * seen by the host check; the device counts them in the workspace status
+ * word FOREMOE_WS_PLAN_ERRORS and treats the entry as absent/equal-split.
+ */
+typedef struct foremoe_plan {
+  int32_t E;
+  int32_t S;
+  int32_t R_max;
+  int32_t reserved;
+  const int32_t* slot_expert;
+  const int32_t* slot_replica;
+  const int32_t* expert_nrep;
+  const int32_t* expert_rep_weight;
+  const int32_t* slot_widx;
+  const int32_t* slot_gidx;
+} foremoe_plan;
+
+/*
+ * Workspace. foremoe_histogram, foremoe_assign_replicas and foremoe_permute
+ * of one micro-step share one caller-owned device workspace of at least
+ * foremoe_workspace_size(T, K, E) bytes (256-byte aligned; returns 0 for
+ * invalid sizes). Its first 256 bytes are int32 status words (read them
+ * after the stream completes):
+ */
+#define FOREMOE_WS_INVALID_IDS 0  /* ids outside [-1, E): skipped, written by histogram */
+#define FOREMOE_WS_DROPPED 1      /* local pairs beyond n_cap, written by permute       */
+#define FOREMOE_WS_PLAN_ERRORS 2  /* device-side plan errors, written by assign         */
+size_t foremoe_workspace_size(int64_t T, int32_t K, int32_t E);
+
+/*
+ * Step 1 (Sec. 5 Routing Collector; load w_e of Table 1).
+ * ids     [T, K] int32, row-major, pair p = t*K + k. -1 = padding (skipped);
+ *         any other id outside [0, E) is invalid: skipped and counted in
+ *         FOREMOE_WS_INVALID_IDS.
+ * counts  [E] int32 out: counts[e] = #pairs with ids[p] == e over all T tokens.
+ * Also fills the workspace with per-block partial counts used by permute.
+ * T >= 0, 1 <= K <= FOREMOE_MAX_TOPK, T*K < 2^31.
+ */
+int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E,
+                      int32_t* counts, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 2 (Sec. 7.2 token conservation; Sec. 8 Stage 4; App. E Stage 4).
+ * For expert e with R_e replicas and weights w (equal if NULL), replica r
+ * takes the contiguous block [B_r, B_{r+1}) of e's token list (ascending
+ * pair index), B_r = floor(n_e * (w_0 + .. + w_{r-1}) / (w_0 + .. + w_{R_e-1})).
+ * rep_begin   [E, R_max+1] int32 out: B_0..B_{R_e}, then n_e up to R_max.
+ * slot_count  [S] int32 out: tokens of slot j = B_{r+1} - B_r of its replica.
+ * slot_offset [S+1] int32 out: exclusive prefix sum of slot_count in slot
+ *             order; slot_offset[S] = N, the local pairs of this GPU.
+ * ws          the workspace foremoe_histogram filled for the same ids.
+ */
+int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan,
+                            int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 3 (Sec. 9, replica-aware token dispatch; one GPU's half of it).
+ * Pair p with expert e is the q-th entry of e's token list and belongs to
+ * replica r with B_r <= q < B_{r+1}. If slot j holds (e, r) here, its row is
+ * row = slot_offset[j] + q - B_r and
+ *   x_perm[row, :] = x[p / K, :]   (bitwise copy)
+ *   row_to_pair[row] = p,  pair_to_row[p] = row;
+ * otherwise pair_to_row[p] = -1. Rows >= N are not written. Pairs whose row
+ * would be >= n_cap are dropped (pair_to_row = -1) and counted in
+ * FOREMOE_WS_DROPPED.
+ * x        [T, d] of `dtype`; d % 8 == 0 (bf16) or d % 4 == 0 (f32).
+ * x_perm   [n_cap, d] of `dtype`; row_to_pair [n_cap]; pair_to_row [T*K].
+ * ws       the workspace filled by foremoe_histogram and
+ *          foremoe_assign_replicas for the same ids and plan.
+ */
+int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
+                    const int32_t* ids, int32_t K, const foremoe_plan* plan,
+                    const int32_t* rep_begin, const int32_t* slot_offset, int64_t n_cap,
+                    void* x_perm, int32_t* row_to_pair, int32_t* pair_to_row,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 4, forward (App. A: SwiGLU expert with gate, up and down matrices).
+ * For each slot j, rows [slot_offset[j], slot_offset[j+1]) (clamped to
+ * n_cap), with w = slot_widx[j]:
+ *   A = X Wg[w]^T, U = X Wu[w]^T      (fp32 accumulate)
+ *   H = silu(A) * U,  silu(a) = a / (1 + exp(-a))
+ *   Y = H Wd[w]^T
+ * x_perm     [n_cap, d]
+ * w_gate_up  [W, 2F, d]: rows [0, F) are Wg[w], rows [F, 2F) are Wu[w]
+ * w_down     [W, d, F]
+ * h          [n_cap, F] out (kept for the weight gradient)
+ * y_perm     [n_cap, d] out
+ * save_au    [n_cap, 2F] out or NULL: A in columns [0, F), U in [F, 2F)
+ *            (needed by foremoe_grouped_ffn_dgrad)
+ * All tensors are `dtype`. bf16 runs on bf16 MFMA with fp32 accumulation
+ * and needs d % 128 == 0 and F % 128 == 0 (else FOREMOE_EUNSUPPORTED); f32
+ * accepts any d, F >= 1. 0 <= S <= FOREMOE_MAX_SLOTS.
+ * foremoe_grouped_ffn_fwd = foremoe_ffn_gate_up_fwd then foremoe_ffn_down_fwd;
+ * each of these two is a single kernel launch.
+ */
+int foremoe_grouped_ffn_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
+                            int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
+                            int32_t W, const void* w_gate_up, const void* w_down, int64_t n_cap,
+                            void* h, void* y_perm, void* save_au, void* stream);
+int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
+                            int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
+                            int32_t W, const void* w_gate_up, int64_t n_cap,
+                            void* h, void* save_au, void* stream);
+int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t F,
+                         int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
+                         int32_t W, const void* w_down, int64_t n_cap, void* y_perm, void* stream);
+
+/*
+ * Step 4, input gradient (chain rule of the forward above):
+ *   dH = dY Wd[w];  dA = dH * U * silu'(A);  dU = dH * silu(A)
+ *   dX = dA Wg[w] + dU Wu[w]
+ * with silu'(a) = s + a s (1 - s), s = 1 / (1 + exp(-a)).
+ * dy_perm [n_cap, d]; save_au [n_cap, 2F] from the forward;
+ * d_au    [n_cap, 2F] out: dA in columns [0, F), dU in [F, 2F);
+ * dx_perm [n_cap, d] out. Same dtype and shape rules as the forward.
+ * = foremoe_ffn_down_dgrad then foremoe_ffn_gate_up_dgrad (one launch each).
+ */
+int foremoe_grouped_ffn_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype,
+                              int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
+                              const int32_t* slot_widx, int32_t W, const void* w_gate_up,
+                              const void* w_down, int64_t n_cap, void* d_au, void* dx_perm,
+                              void* stream);
+int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype,
+                           int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
+                           const int32_t* slot_widx, int32_t W, const void* w_down,
+                           int64_t n_cap, void* d_au, void* stream);
+int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F,
+                              int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
+                              int32_t W, const void* w_gate_up, int64_t n_cap, void* dx_perm,
+                              void* stream);
+
+/*
+ * Step 4, weight gradient with main-expert accumulation (Sec. 6.2, Copy-in:
+ * the partial gradients of all replicas of an expert are summed into the
+ * main expert's gradient; App. A.4: fp32 gradient accumulation):
+ *   dW_gate_up[g] += [dA | dU]^T X,   dW_down[g] += dY^T H
+ * summed over the rows of every slot j with slot_gidx[j] == g, in slot
+ * order. ACCUMULATES (+=) into fp32 dw_gate_up [G, 2F, d] and
+ * dw_down [G, d, F], so gradients add up over micro-steps. Each output
+ * element is owned by one workgroup (no atomics). 1 <= G <= FOREMOE_MAX_SLOTS.
+ * = foremoe_ffn_gate_up_wgrad then foremoe_ffn_down_wgrad (one launch each).
+ */
+int foremoe_grouped_ffn_wgrad(const void* x_perm, const void* h, const void* dy_perm,
+                              const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F,
+                              int32_t S, const int32_t* slot_offset, const int32_t* slot_gidx,
+                              int32_t G, int64_t n_cap, float* dw_gate_up, float* dw_down,
+                              void* stream);
+int foremoe_ffn_gate_up_wgrad(const void* d_au, const void* x_perm, foremoe_dtype dtype,
+                              int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
+                              const int32_t* slot_gidx, int32_t G, int64_t n_cap,
+                              float* dw_gate_up, void* stream);
+int foremoe_ffn_down_wgrad(const void* dy_perm, const void* h, foremoe_dtype dtype,
+                           int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
+                           const int32_t* slot_gidx, int32_t G, int64_t n_cap,
+                           float* dw_down, void* stream);
+
+/*
+ * Step 5 (Sec. 2.1: the output is the router-probability weighted sum of
+ * the selected experts' outputs):
+ *   y[t, :] = sum_{k ascending, pair_to_row[tK+k] >= 0} gates[tK+k] * Y[row, :]
+ * fp32 accumulation; tokens with no local pair get a zero row (y is dense,
+ * this GPU's share of the sum).
+ * y_perm [n_cap, d] of in_dtype; gates [T, K] fp32; y [T, d] of out_dtype.
+ */
+int foremoe_combine(const void* y_perm, foremoe_dtype in_dtype, const int32_t* pair_to_row,
+                    const float* gates, int64_t T, int32_t K, int32_t d, int64_t n_cap,
+                    void* y, foremoe_dtype out_dtype, void* stream);
+
+/*
+ * Backward of step 5. For every pair p = tK+k with row = pair_to_row[p] >= 0:
+ *   dy_perm[row, :] = gates[p] * dy[t, :]
+ *   dgates[p] = <dy[t, :], y_perm[row, :]>        (fp32)
+ * and dgates[p] = 0 for pairs not computed here. dgates may be NULL (then
+ * y_perm is not read and may be NULL). dy [T, d], y_perm and dy_perm
+ * [n_cap, d], all of `dtype`.
+ */
+int foremoe_combine_bwd(const void* dy, const void* y_perm, foremoe_dtype dtype,
+                        const int32_t* pair_to_row, const float* gates, int64_t T, int32_t K,
+                        int32_t d, int64_t n_cap, void* dy_perm, float* dgates, void* stream);
+
+/*
+ * Backward of step 3: dx[t, :] = sum_{k ascending, row >= 0} dx_perm[row, :]
+ * (fp32 accumulation), zero rows for tokens with no local pair.
+ * dx_perm [n_cap, d] of in_dtype; dx [T, d] of out_dtype.
+ */
+int foremoe_permute_bwd(const void* dx_perm, foremoe_dtype in_dtype, const int32_t* pair_to_row,
+                        int64_t T, int32_t K, int32_t d, int64_t n_cap, void* dx,
+                        foremoe_dtype out_dtype, void* stream);
+
+/* Utilities (host only, no GPU work). */
+const char* foremoe_status_string(int status);
+const char* foremoe_last_error(void); /* message of this thread's last failed call */
+const char* foremoe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FOREMOE_H */

@@ -1,0 +1,212 @@
+"""Tensor-level binding of the C ABI: argument marshalling only.
+
+Every function allocates its outputs with torch (device memory), passes raw
+device pointers and the current HIP stream to libforemoe.so and raises if the
+library reports an error. No arithmetic of the expert layer happens here.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import check
+
+_DT = {torch.float32: _lib.F32, torch.bfloat16: _lib.BF16}
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return _DT[t.dtype]
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _i32(t: torch.Tensor, name: str) -> torch.Tensor:
+    if t.dtype != torch.int32:
+        raise TypeError(f"{name} must be int32")
+    return t
+
+
+@dataclass
+class DevicePlan:
+    """A slot table (see include/foremoe.h, foremoe_plan) resident on the device."""
+    E: int
+    S: int
+    R_max: int
+    W: int
+    G: int
+    slot_expert: torch.Tensor
+    slot_replica: torch.Tensor
+    expert_nrep: torch.Tensor
+    expert_rep_weight: Optional[torch.Tensor]
+    slot_widx: torch.Tensor
+    slot_gidx: torch.Tensor
+
+    @classmethod
+    def from_host(cls, plan, device) -> "DevicePlan":
+        dev = torch.device(device)
+
+        def t(a):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+        w = None if plan.expert_rep_weight is None else t(np.asarray(plan.expert_rep_weight).reshape(-1))
+        return cls(E=plan.E, S=plan.S, R_max=plan.R_max, W=plan.W, G=plan.G,
+                   slot_expert=t(plan.slot_expert), slot_replica=t(plan.slot_replica),
+                   expert_nrep=t(plan.expert_nrep), expert_rep_weight=w,
+                   slot_widx=t(plan.slot_widx), slot_gidx=t(plan.slot_gidx))
+
+    def c_struct(self) -> _lib.Plan:
+        return _lib.Plan(self.E, self.S, self.R_max, 0, self.slot_expert.data_ptr(),
+                         self.slot_replica.data_ptr(), self.expert_nrep.data_ptr(),
+                         None if self.expert_rep_weight is None else self.expert_rep_weight.data_ptr(),
+                         self.slot_widx.data_ptr(), self.slot_gidx.data_ptr())
+
+
+def workspace(T: int, K: int, E: int, device) -> torch.Tensor:
+    n = _lib.load().foremoe_workspace_size(T, K, E)
+    if n == 0:
+        raise ValueError("invalid workspace sizes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def ws_status(ws: torch.Tensor) -> np.ndarray:
+    """The int32 status words at the head of a workspace (synchronises)."""
+    return ws[:256].view(torch.int32).cpu().numpy()
+
+
+def histogram(ids: torch.Tensor, E: int, ws: torch.Tensor) -> torch.Tensor:
+    _i32(ids, "ids")
+    T, K = ids.shape
+    counts = torch.empty(E, dtype=torch.int32, device=ids.device)
+    check(_lib.load().foremoe_histogram(_ptr(ids), T, K, E, _ptr(counts), _ptr(ws), ws.numel(),
+                                        _stream(ids.device)), "foremoe_histogram")
+    return counts
+
+
+def assign_replicas(counts: torch.Tensor, plan: DevicePlan, ws: torch.Tensor):
+    dev = counts.device
+    rep_begin = torch.empty((plan.E, plan.R_max + 1), dtype=torch.int32, device=dev)
+    slot_count = torch.empty(max(plan.S, 1), dtype=torch.int32, device=dev)[: plan.S]
+    slot_offset = torch.empty(plan.S + 1, dtype=torch.int32, device=dev)
+    cp = plan.c_struct()
+    check(_lib.load().foremoe_assign_replicas(_ptr(counts), ctypes.byref(cp), _ptr(rep_begin),
+                                              slot_count.data_ptr(), _ptr(slot_offset), _ptr(ws), ws.numel(),
+                                              _stream(dev)), "foremoe_assign_replicas")
+    return rep_begin, slot_count, slot_offset
+
+
+def permute(x: torch.Tensor, ids: torch.Tensor, plan: DevicePlan, rep_begin: torch.Tensor,
+            slot_offset: torch.Tensor, n_cap: int, ws: torch.Tensor):
+    T, d = x.shape
+    K = ids.shape[1]
+    dev = x.device
+    x_perm = torch.empty((n_cap, d), dtype=x.dtype, device=dev)
+    row_to_pair = torch.empty(n_cap, dtype=torch.int32, device=dev)
+    pair_to_row = torch.empty(T * K, dtype=torch.int32, device=dev)
+    cp = plan.c_struct()
+    check(_lib.load().foremoe_permute(_ptr(x), _dt(x), T, d, _ptr(ids), K, ctypes.byref(cp), _ptr(rep_begin),
+                                      _ptr(slot_offset), n_cap, x_perm.data_ptr(), row_to_pair.data_ptr(),
+                                      pair_to_row.data_ptr(), _ptr(ws), ws.numel(), _stream(dev)),
+          "foremoe_permute")
+    return x_perm, row_to_pair, pair_to_row
+
+
+def grouped_ffn_fwd(x_perm: torch.Tensor, slot_offset: torch.Tensor, slot_widx: torch.Tensor,
+                    w_gate_up: torch.Tensor, w_down: torch.Tensor, save: bool = True):
+    n_cap, d = x_perm.shape
+    W, F2, _ = w_gate_up.shape
+    F = F2 // 2
+    S = slot_widx.shape[0]
+    dev = x_perm.device
+    h = torch.empty((n_cap, F), dtype=x_perm.dtype, device=dev)
+    y_perm = torch.empty((n_cap, d), dtype=x_perm.dtype, device=dev)
+    save_au = torch.empty((n_cap, 2 * F), dtype=x_perm.dtype, device=dev) if save else None
+    check(_lib.load().foremoe_grouped_ffn_fwd(_ptr(x_perm), _dt(x_perm), d, F, S, _ptr(slot_offset),
+                                              _ptr(slot_widx), W, _ptr(w_gate_up), _ptr(w_down), n_cap,
+                                              h.data_ptr(), y_perm.data_ptr(),
+                                              None if save_au is None else save_au.data_ptr(), _stream(dev)),
+          "foremoe_grouped_ffn_fwd")
+    return h, y_perm, save_au
+
+
+def grouped_ffn_dgrad(dy_perm: torch.Tensor, save_au: torch.Tensor, slot_offset: torch.Tensor,
+                      slot_widx: torch.Tensor, w_gate_up: torch.Tensor, w_down: torch.Tensor):
+    n_cap, d = dy_perm.shape
+    W, F2, _ = w_gate_up.shape
+    F = F2 // 2
+    S = slot_widx.shape[0]
+    dev = dy_perm.device
+    d_au = torch.empty((n_cap, 2 * F), dtype=dy_perm.dtype, device=dev)
+    dx_perm = torch.empty((n_cap, d), dtype=dy_perm.dtype, device=dev)
+    check(_lib.load().foremoe_grouped_ffn_dgrad(_ptr(dy_perm), _ptr(save_au), _dt(dy_perm), d, F, S,
+                                                _ptr(slot_offset), _ptr(slot_widx), W, _ptr(w_gate_up),
+                                                _ptr(w_down), n_cap, d_au.data_ptr(), dx_perm.data_ptr(),
+                                                _stream(dev)), "foremoe_grouped_ffn_dgrad")
+    return d_au, dx_perm
+
+
+def grouped_ffn_wgrad(x_perm: torch.Tensor, h: torch.Tensor, dy_perm: torch.Tensor, d_au: torch.Tensor,
+                      slot_offset: torch.Tensor, slot_gidx: torch.Tensor, dw_gate_up: torch.Tensor,
+                      dw_down: torch.Tensor) -> None:
+    """Accumulates (+=) into the fp32 gradients dw_gate_up [G, 2F, d], dw_down [G, d, F]."""
+    n_cap, d = x_perm.shape
+    G, F2, _ = dw_gate_up.shape
+    F = F2 // 2
+    S = slot_gidx.shape[0]
+    if dw_gate_up.dtype != torch.float32 or dw_down.dtype != torch.float32:
+        raise TypeError("weight gradients are fp32")
+    check(_lib.load().foremoe_grouped_ffn_wgrad(_ptr(x_perm), _ptr(h), _ptr(dy_perm), _ptr(d_au), _dt(x_perm),
+                                                d, F, S, _ptr(slot_offset), _ptr(slot_gidx), G, n_cap,
+                                                _ptr(dw_gate_up), _ptr(dw_down), _stream(x_perm.device)),
+          "foremoe_grouped_ffn_wgrad")
+
+
+def combine(y_perm: torch.Tensor, pair_to_row: torch.Tensor, gates: torch.Tensor,
+            out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    T, K = gates.shape
+    n_cap, d = y_perm.shape
+    y = torch.empty((T, d), dtype=out_dtype, device=y_perm.device)
+    check(_lib.load().foremoe_combine(_ptr(y_perm), _dt(y_perm), _ptr(pair_to_row), _ptr(gates), T, K, d, n_cap,
+                                      y.data_ptr(), _DT[out_dtype], _stream(y_perm.device)), "foremoe_combine")
+    return y
+
+
+def combine_bwd(dy: torch.Tensor, y_perm: torch.Tensor, pair_to_row: torch.Tensor, gates: torch.Tensor,
+                want_dgates: bool = True):
+    T, K = gates.shape
+    n_cap, d = y_perm.shape
+    dy_perm = torch.empty((n_cap, d), dtype=dy.dtype, device=dy.device)
+    dgates = torch.empty((T, K), dtype=torch.float32, device=dy.device) if want_dgates else None
+    check(_lib.load().foremoe_combine_bwd(_ptr(dy), _ptr(y_perm), _dt(dy), _ptr(pair_to_row), _ptr(gates), T, K,
+                                          d, n_cap, dy_perm.data_ptr(),
+                                          None if dgates is None else dgates.data_ptr(), _stream(dy.device)),
+          "foremoe_combine_bwd")
+    return dy_perm, dgates
+
+
+def permute_bwd(dx_perm: torch.Tensor, pair_to_row: torch.Tensor, T: int, K: int,
+                out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    n_cap, d = dx_perm.shape
+    dx = torch.empty((T, d), dtype=out_dtype, device=dx_perm.device)
+    check(_lib.load().foremoe_permute_bwd(_ptr(dx_perm), _dt(dx_perm), _ptr(pair_to_row), T, K, d, n_cap,
+                                          dx.data_ptr(), _DT[out_dtype], _stream(dx_perm.device)),
+          "foremoe_permute_bwd")
+    return dx

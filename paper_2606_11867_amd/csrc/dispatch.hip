@@ -1,0 +1,642 @@
+// Steps 1-3 and 5 of the per-micro-step expert layer: histogram, replica
+// split, permute, combine, and the backward gathers (combine_bwd,
+// permute_bwd). All integer work is exact and deterministic: per-expert
+// ranks come from wavefront ballots plus prefix sums, never from the order
+// in which atomics land.
+#include <climits>
+
+#include "common.h"
+
+namespace foremoe {
+namespace {
+
+constexpr int kWaves = kHistThreads / 64;
+constexpr int kPairsPerWave = kHistChunk / kWaves;
+
+int key_bits(int E) {
+  int b = 1;
+  while ((1 << b) < E + 1) ++b;
+  return b;
+}
+
+// Lanes of this wavefront holding the same key as this lane, restricted to
+// `active`. Keys are compared bit by bit with ballots (nbits ballots).
+__device__ __forceinline__ uint64_t match_key(int key, int nbits, uint64_t active) {
+  uint64_t m = active;
+  for (int b = 0; b < nbits; ++b) {
+    const int bit = (key >> b) & 1;
+    const uint64_t bal = __ballot(bit);
+    m &= bit ? bal : ~bal;
+  }
+  return m;
+}
+
+// Key of a recorded id: the expert, -1 for padding, E for invalid ids.
+__device__ __forceinline__ int id_key(int v, int E) { return v == -1 ? -1 : ((v >= 0 && v < E) ? v : E); }
+
+// ---------------------------------------------------------------------------
+// Step 1a: per-block counts of each expert (bucket E counts invalid ids).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kHistThreads) void hist_count_kernel(const int32_t* __restrict__ ids, int64_t npairs,
+                                                                  int E, int nbits, int32_t* __restrict__ partial) {
+  __shared__ int s_cnt[FOREMOE_MAX_EXPERTS + 1];
+  const int tid = threadIdx.x;
+  for (int e = tid; e <= E; e += kHistThreads) s_cnt[e] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kHistChunk;
+  const int lane = tid & 63;
+#pragma unroll 1
+  for (int i = 0; i < kHistChunk / kHistThreads; ++i) {
+    const int64_t p = base + (int64_t)i * kHistThreads + tid;
+    int key = -1;
+    if (p < npairs) key = id_key(ids[p], E);
+    const uint64_t active = __ballot(key >= 0);
+    const uint64_t m = match_key(key, nbits, active);
+    if (key >= 0 && lane == __builtin_ctzll(m)) atomicAdd(&s_cnt[key], __popcll(m));
+  }
+  __syncthreads();
+  int32_t* out = partial + (int64_t)blockIdx.x * (E + 1);
+  for (int e = tid; e <= E; e += kHistThreads) out[e] = s_cnt[e];
+}
+
+// Inclusive block-wide scan of one int per thread (256 threads).
+__device__ int block_inclusive_scan(int v, int* s_tmp /* [kWaves] */, int& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
+  if (lane == 63) s_tmp[w] = v;
+  __syncthreads();
+  int before = 0;
+  total = 0;
+  for (int i = 0; i < kWaves; ++i) {
+    const int t = s_tmp[i];
+    if (i < w) before += t;
+    total += t;
+  }
+  __syncthreads();
+  return v + before;
+}
+
+// ---------------------------------------------------------------------------
+// Step 1b: for each expert (one workgroup per expert column) turn the
+// per-block counts into exclusive block bases; the total is counts[e]
+// (bucket E: the invalid-id count status word).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kHistThreads) void hist_scan_kernel(int32_t* __restrict__ partial, int64_t nblocks, int E,
+                                                                 int32_t* __restrict__ counts, int32_t* __restrict__ status) {
+  __shared__ int s_tmp[kWaves];
+  const int e = blockIdx.x;
+  int carry = 0;
+  for (int64_t b0 = 0; b0 < nblocks; b0 += kHistThreads) {
+    const int64_t b = b0 + threadIdx.x;
+    const int v = b < nblocks ? partial[b * (E + 1) + e] : 0;
+    int total;
+    const int incl = block_inclusive_scan(v, s_tmp, total);
+    if (b < nblocks) partial[b * (E + 1) + e] = carry + incl - v;
+    carry += total;
+  }
+  if (threadIdx.x == 0) {
+    if (e < E) counts[e] = carry;
+    else status[FOREMOE_WS_INVALID_IDS] = carry;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Step 2: replica boundaries, slot counts and slot offsets (one workgroup).
+// ---------------------------------------------------------------------------
+struct PlanDev {
+  int E, S, R_max;
+  const int32_t* slot_expert;
+  const int32_t* slot_replica;
+  const int32_t* expert_nrep;
+  const int32_t* expert_rep_weight;
+};
+
+__device__ __forceinline__ int clamp_nrep(const PlanDev& P, int e, int& err) {
+  int R = P.expert_nrep[e];
+  if (R < 1 || R > P.R_max) {
+    ++err;
+    R = 1;
+  }
+  return R;
+}
+
+__global__ __launch_bounds__(kHistThreads) void assign_kernel(const int32_t* __restrict__ counts, PlanDev P,
+                                                              int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count,
+                                                              int32_t* __restrict__ slot_offset, int32_t* __restrict__ rep_slot,
+                                                              int32_t* __restrict__ status) {
+  __shared__ int s_err;
+  __shared__ int s_cnt[FOREMOE_MAX_SLOTS];
+  __shared__ int s_tmp[kWaves];
+  const int tid = threadIdx.x;
+  if (tid == 0) s_err = 0;
+  const int RS = P.R_max + 1;
+  for (int i = tid; i < P.E * P.R_max; i += kHistThreads) rep_slot[i] = INT_MAX;
+  __syncthreads();
+  int err = 0;
+  for (int e = tid; e < P.E; e += kHistThreads) {
+    const int n = counts[e];
+    const int R = clamp_nrep(P, e, err);
+    long long total = 0;
+    bool bad = false;
+    for (int r = 0; r < R; ++r) {
+      const int w = P.expert_rep_weight ? P.expert_rep_weight[e * P.R_max + r] : 1;
+      if (w < 0) bad = true;
+      total += w;
+    }
+    if (total <= 0) bad = true;
+    if (bad) ++err;
+    long long pref = 0;
+    int32_t* rb = rep_begin + (int64_t)e * RS;
+    rb[0] = 0;
+    for (int r = 0; r < R; ++r) {
+      const long long w = bad ? 1 : (P.expert_rep_weight ? P.expert_rep_weight[e * P.R_max + r] : 1);
+      pref += w;
+      rb[r + 1] = (int)(((long long)n * pref) / (bad ? (long long)R : total));
+    }
+    for (int r = R + 1; r < RS; ++r) rb[r] = n;
+  }
+  // Slot j claims replica (e, r); with duplicates the lowest j wins.
+  for (int j = tid; j < P.S; j += kHistThreads) {
+    const int e = P.slot_expert[j], r = P.slot_replica[j];
+    if (e >= 0 && e < P.E && r >= 0 && r < P.R_max) atomicMin(&rep_slot[e * P.R_max + r], j);
+  }
+  __syncthreads();
+  for (int j = tid; j < P.S; j += kHistThreads) {
+    const int e = P.slot_expert[j], r = P.slot_replica[j];
+    int c = 0;
+    if (e >= 0 && e < P.E && r >= 0) {
+      int dummy = 0;
+      const int R = clamp_nrep(P, e, dummy);
+      if (r < R && rep_slot[e * P.R_max + r] == j) {
+        const int32_t* rb = rep_begin + (int64_t)e * RS;
+        c = rb[r + 1] - rb[r];
+      } else {
+        ++err;
+      }
+    } else {
+      ++err;
+    }
+    slot_count[j] = c;
+    s_cnt[j] = c;
+  }
+  if (err) atomicAdd(&s_err, err);
+  __syncthreads();
+  for (int i = tid; i < P.E * P.R_max; i += kHistThreads) {
+    // replicas beyond R_e, and replicas held by no (valid) slot, are remote
+    const int e = i / P.R_max, r = i % P.R_max;
+    int dummy = 0;
+    const int R = clamp_nrep(P, e, dummy);
+    if (rep_slot[i] == INT_MAX || r >= R) rep_slot[i] = -1;
+  }
+  int carry = 0;
+  for (int j0 = 0; j0 < P.S; j0 += kHistThreads) {
+    const int j = j0 + tid;
+    const int v = j < P.S ? s_cnt[j] : 0;
+    int total;
+    const int incl = block_inclusive_scan(v, s_tmp, total);
+    if (j < P.S) slot_offset[j] = carry + incl - v;
+    carry += total;
+  }
+  if (tid == 0) {
+    slot_offset[P.S] = carry;
+    status[FOREMOE_WS_PLAN_ERRORS] = s_err;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Step 3a: stable rank of every pair in its expert's list, replica, slot,
+// row; writes both index maps. Each wave ranks a contiguous quarter of the
+// block's pairs in ascending order.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kHistThreads) void permute_rank_kernel(
+    const int32_t* __restrict__ ids, int64_t npairs, int E, int nbits, int R_max,
+    const int32_t* __restrict__ block_base, const int32_t* __restrict__ rep_begin,
+    const int32_t* __restrict__ rep_slot, const int32_t* __restrict__ slot_offset, int S, int64_t n_cap,
+    int32_t* __restrict__ pair_to_row, int32_t* __restrict__ row_to_pair, int32_t* __restrict__ status) {
+  __shared__ int s_w[kWaves][FOREMOE_MAX_EXPERTS + 1];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int e = lane; e <= E; e += 64) s_w[w][e] = 0;
+  __syncthreads();
+  const int64_t wbase = (int64_t)blockIdx.x * kHistChunk + (int64_t)w * kPairsPerWave;
+  // pass 1: per-wave counts
+  for (int i = 0; i < kPairsPerWave / 64; ++i) {
+    const int64_t p = wbase + i * 64 + lane;
+    int key = -1;
+    if (p < npairs) key = id_key(ids[p], E);
+    if (key == E) key = -1;
+    const uint64_t active = __ballot(key >= 0);
+    const uint64_t m = match_key(key, nbits, active);
+    if (key >= 0 && lane == __builtin_ctzll(m)) s_w[w][key] += __popcll(m);
+  }
+  __syncthreads();
+  // pass 2: exclusive bases of each wave, starting from the block's base
+  for (int e = tid; e < E; e += kHistThreads) {
+    int run = block_base[(int64_t)blockIdx.x * (E + 1) + e];
+    for (int ww = 0; ww < kWaves; ++ww) {
+      const int c = s_w[ww][e];
+      s_w[ww][e] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  // pass 3: rank, replica, slot, row
+  const int RS = R_max + 1;
+  for (int i = 0; i < kPairsPerWave / 64; ++i) {
+    const int64_t p = wbase + i * 64 + lane;
+    int key = -1;
+    if (p < npairs) key = id_key(ids[p], E);
+    if (key == E) key = -1;
+    const uint64_t active = __ballot(key >= 0);
+    const uint64_t m = match_key(key, nbits, active);
+    int q = 0;
+    if (key >= 0) q = s_w[w][key] + lanes_below(m);
+    __builtin_amdgcn_wave_barrier();
+    if (key >= 0 && lane == __builtin_ctzll(m)) s_w[w][key] = q + __popcll(m);
+    __builtin_amdgcn_wave_barrier();
+    if (p < npairs) {
+      int row = -1;
+      if (key >= 0) {
+        const int32_t* rb = rep_begin + (int64_t)key * RS;
+        int r = 0;
+        while (r + 1 < R_max && rb[r + 1] <= q) ++r;
+        const int j = rep_slot[key * R_max + r];
+        if (j >= 0 && j < S) {
+          const int64_t rr = (int64_t)slot_offset[j] + q - rb[r];
+          if (rr >= 0 && rr < n_cap) {
+            row = (int)rr;
+            row_to_pair[row] = (int32_t)p;
+          }
+        }
+      }
+      pair_to_row[p] = row;
+    }
+  }
+  if (blockIdx.x == 0 && tid == 0) {
+    const int64_t N = slot_offset[S];
+    status[FOREMOE_WS_DROPPED] = N > n_cap ? (int)(N - n_cap) : 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Step 3b: gather token rows into slot order, 16-byte vectors, one row per
+// wavefront iteration, four vectors in flight per lane.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restrict__ x, int64_t vec_per_row, int K,
+                                                          int64_t npairs, const int32_t* __restrict__ row_to_pair,
+                                                          const int32_t* __restrict__ n_rows_dev, int64_t n_cap,
+                                                          uint4* __restrict__ x_perm) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  int64_t N = *n_rows_dev;
+  if (N > n_cap) N = n_cap;
+  for (int64_t row = wave; row < N; row += nwaves) {
+    const int64_t p = row_to_pair[row];
+    if (p < 0 || p >= npairs) continue;  // never taken when the maps are consistent
+    const int64_t t = p / K;
+    const uint4* src = x + t * vec_per_row;
+    uint4* dst = x_perm + row * vec_per_row;
+    for (int64_t v0 = lane; v0 < vec_per_row; v0 += 256) {
+      uint4 a[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v0 + u * 64 < vec_per_row) a[u] = src[v0 + u * 64];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v0 + u * 64 < vec_per_row) dst[v0 + u * 64] = a[u];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Vector helpers for the gathers: one "vector" is 16 bytes of input
+// (8 bf16 or 4 fp32), widened to floats.
+// ---------------------------------------------------------------------------
+template <typename T>
+struct Vec;
+
+template <>
+struct Vec<uint16_t> {
+  static constexpr int N = 8;
+  __device__ static void load(const uint16_t* p, float* f) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = bf2f(w[i] & 0xFFFFu);
+      f[2 * i + 1] = bf2f(w[i] >> 16);
+    }
+  }
+  template <int M>
+  __device__ static void store(uint16_t* p, const float* f) {
+    static_assert(M % 2 == 0, "even element count");
+    uint32_t w[M / 2];
+#pragma unroll
+    for (int i = 0; i < M / 2; ++i) w[i] = pack_bf2(f[2 * i], f[2 * i + 1]);
+    if constexpr (M == 8) {
+      *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+      *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+    }
+  }
+};
+
+template <>
+struct Vec<float> {
+  static constexpr int N = 4;
+  __device__ static void load(const float* p, float* f) {
+    const float4 v = *reinterpret_cast<const float4*>(p);
+    f[0] = v.x;
+    f[1] = v.y;
+    f[2] = v.z;
+    f[3] = v.w;
+  }
+  template <int M>
+  __device__ static void store(float* p, const float* f) {
+#pragma unroll
+    for (int i = 0; i < M; i += 4) *reinterpret_cast<float4*>(p + i) = make_float4(f[i], f[i + 1], f[i + 2], f[i + 3]);
+  }
+};
+
+constexpr int kGatherChunk = 4;  // 16-byte vectors per lane per pass
+
+// ---------------------------------------------------------------------------
+// Step 5 (and the backward of step 3 with unit weights): one wavefront per
+// token, y[t] = sum_k g_k * Y[row_k] in ascending k, fp32 accumulation.
+// ---------------------------------------------------------------------------
+template <typename Tin, typename Tout>
+__global__ __launch_bounds__(256) void combine_kernel(const Tin* __restrict__ y_perm, const int32_t* __restrict__ pair_to_row,
+                                                      const float* __restrict__ gates, int64_t T, int K, int d,
+                                                      int64_t n_cap, Tout* __restrict__ y) {
+  constexpr int VE = Vec<Tin>::N;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  const int nvec = d / VE;
+  for (int64_t t = wave; t < T; t += nwaves) {
+    for (int v0 = 0; v0 < nvec; v0 += 64 * kGatherChunk) {
+      float acc[kGatherChunk][VE];
+#pragma unroll
+      for (int u = 0; u < kGatherChunk; ++u)
+#pragma unroll
+        for (int i = 0; i < VE; ++i) acc[u][i] = 0.f;
+      for (int k = 0; k < K; ++k) {
+        const int row = pair_to_row[t * K + k];
+        if (row < 0 || row >= n_cap) continue;
+        const float g = gates ? gates[t * K + k] : 1.0f;
+        const Tin* src = y_perm + (int64_t)row * d;
+        float v[kGatherChunk][VE];
+#pragma unroll
+        for (int u = 0; u < kGatherChunk; ++u) {
+          const int vi = v0 + u * 64 + lane;
+          if (vi < nvec) Vec<Tin>::load(src + (int64_t)vi * VE, v[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kGatherChunk; ++u)
+#pragma unroll
+          for (int i = 0; i < VE; ++i) acc[u][i] += g * v[u][i];
+      }
+      Tout* dst = y + t * d;
+#pragma unroll
+      for (int u = 0; u < kGatherChunk; ++u) {
+        const int vi = v0 + u * 64 + lane;
+        if (vi < nvec) Vec<Tout>::template store<VE>(dst + (int64_t)vi * VE, acc[u]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward of step 5: one wavefront per token; for each local pair write
+// dY[row] = g * dy[t] and dgates[p] = <dy[t], Y[row]> (deterministic
+// butterfly reduction); dgates of non-local pairs = 0.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(const T* __restrict__ dy, const T* __restrict__ y_perm,
+                                                          const int32_t* __restrict__ pair_to_row,
+                                                          const float* __restrict__ gates, int64_t Ttok, int K, int d,
+                                                          int64_t n_cap, T* __restrict__ dy_perm, float* __restrict__ dgates) {
+  constexpr int VE = Vec<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  const int nvec = d / VE;
+  for (int64_t t = wave; t < Ttok; t += nwaves) {
+    const T* dyt = dy + t * d;
+    for (int k = 0; k < K; ++k) {
+      const int64_t p = t * K + k;
+      const int row = pair_to_row[p];
+      if (row < 0 || row >= n_cap) {
+        if (dgates && lane == 0) dgates[p] = 0.f;
+        continue;
+      }
+      const float g = gates[p];
+      float part = 0.f;
+      for (int v0 = 0; v0 < nvec; v0 += 64 * kGatherChunk) {
+        float a[kGatherChunk][VE], b[kGatherChunk][VE];
+#pragma unroll
+        for (int u = 0; u < kGatherChunk; ++u) {
+          const int vi = v0 + u * 64 + lane;
+          if (vi < nvec) {
+            Vec<T>::load(dyt + (int64_t)vi * VE, a[u]);
+            if (dgates) Vec<T>::load(y_perm + (int64_t)row * d + (int64_t)vi * VE, b[u]);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kGatherChunk; ++u) {
+          const int vi = v0 + u * 64 + lane;
+          if (vi < nvec) {
+            float o[VE];
+#pragma unroll
+            for (int i = 0; i < VE; ++i) {
+              o[i] = g * a[u][i];
+              if (dgates) part += a[u][i] * b[u][i];
+            }
+            Vec<T>::template store<VE>(dy_perm + (int64_t)row * d + (int64_t)vi * VE, o);
+          }
+        }
+      }
+      if (dgates) {
+        part = wave_sum(part);
+        if (lane == 0) dgates[p] = part;
+      }
+    }
+  }
+}
+
+int gather_grid(int64_t items) {
+  // four wavefronts per workgroup; enough workgroups to fill the chip
+  int64_t blocks = (items + 3) / 4;
+  const int64_t cap = (int64_t)num_cus() * 16;
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  return (int)blocks;
+}
+
+}  // namespace
+}  // namespace foremoe
+
+using namespace foremoe;
+
+#define REQUIRE(cond, ...)                                      \
+  do {                                                          \
+    if (!(cond)) return set_error(FOREMOE_EINVAL, __VA_ARGS__); \
+  } while (0)
+
+extern "C" {
+
+int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t* counts, void* ws,
+                      size_t ws_bytes, void* stream) {
+  REQUIRE(T >= 0, "histogram: T < 0");
+  REQUIRE(K >= 1 && K <= FOREMOE_MAX_TOPK, "histogram: K=%d outside [1, %d]", K, FOREMOE_MAX_TOPK);
+  REQUIRE(E >= 1 && E <= FOREMOE_MAX_EXPERTS, "histogram: E=%d outside [1, %d]", E, FOREMOE_MAX_EXPERTS);
+  REQUIRE(T * (int64_t)K < (int64_t)INT_MAX, "histogram: T*K must be below 2^31");
+  REQUIRE(ids || T == 0, "histogram: ids is NULL");
+  REQUIRE(counts && ws, "histogram: counts or ws is NULL");
+  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, E), "histogram: workspace too small (%zu < %zu)", ws_bytes,
+          ws_bytes_needed(T, K, E));
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t npairs = T * (int64_t)K;
+  const int64_t nb = hist_blocks(npairs);
+  int32_t* status = (int32_t*)ws;
+  int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
+  hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, E, key_bits(E),
+                     partial);
+  hipLaunchKernelGGL(hist_scan_kernel, dim3(E + 1), dim3(kHistThreads), 0, st, partial, nb, E, counts, status);
+  return check_launch("foremoe_histogram");
+}
+
+int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
+                            int32_t* slot_offset, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(plan, "assign_replicas: plan is NULL");
+  REQUIRE(plan->E >= 1 && plan->E <= FOREMOE_MAX_EXPERTS, "assign_replicas: E=%d out of range", plan->E);
+  REQUIRE(plan->S >= 0 && plan->S <= FOREMOE_MAX_SLOTS, "assign_replicas: S=%d out of range", plan->S);
+  REQUIRE(plan->R_max >= 1 && plan->R_max <= FOREMOE_MAX_REPLICAS, "assign_replicas: R_max=%d out of range",
+          plan->R_max);
+  REQUIRE(counts && rep_begin && slot_offset && ws, "assign_replicas: NULL buffer");
+  REQUIRE(plan->expert_nrep, "assign_replicas: plan->expert_nrep is NULL");
+  REQUIRE(plan->S == 0 || (plan->slot_expert && plan->slot_replica && slot_count),
+          "assign_replicas: NULL slot arrays");
+  REQUIRE(ws_bytes >= kWsPartialOff, "assign_replicas: workspace too small");
+  PlanDev P{plan->E, plan->S, plan->R_max, plan->slot_expert, plan->slot_replica, plan->expert_nrep,
+            plan->expert_rep_weight};
+  int32_t* status = (int32_t*)ws;
+  int32_t* rep_slot = (int32_t*)((char*)ws + kWsRepSlotOff);
+  hipLaunchKernelGGL(assign_kernel, dim3(1), dim3(kHistThreads), 0, (hipStream_t)stream, counts, P, rep_begin,
+                     slot_count, slot_offset, rep_slot, status);
+  return check_launch("foremoe_assign_replicas");
+}
+
+int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, const int32_t* ids, int32_t K,
+                    const foremoe_plan* plan, const int32_t* rep_begin, const int32_t* slot_offset, int64_t n_cap,
+                    void* x_perm, int32_t* row_to_pair, int32_t* pair_to_row, void* ws, size_t ws_bytes,
+                    void* stream) {
+  REQUIRE(plan, "permute: plan is NULL");
+  REQUIRE(dtype == FOREMOE_F32 || dtype == FOREMOE_BF16, "permute: bad dtype");
+  REQUIRE(T >= 0 && n_cap >= 0 && d >= 1, "permute: bad sizes");
+  REQUIRE(K >= 1 && K <= FOREMOE_MAX_TOPK, "permute: K out of range");
+  REQUIRE(T * (int64_t)K < (int64_t)INT_MAX && n_cap < (int64_t)INT_MAX, "permute: sizes must be below 2^31");
+  REQUIRE(plan->E >= 1 && plan->E <= FOREMOE_MAX_EXPERTS, "permute: E out of range");
+  REQUIRE(plan->S >= 0 && plan->S <= FOREMOE_MAX_SLOTS, "permute: S out of range");
+  REQUIRE(plan->R_max >= 1 && plan->R_max <= FOREMOE_MAX_REPLICAS, "permute: R_max out of range");
+  REQUIRE(rep_begin && slot_offset && ws, "permute: NULL buffer");
+  REQUIRE(T == 0 || (x && ids && pair_to_row), "permute: NULL input");
+  REQUIRE(n_cap == 0 || (x_perm && row_to_pair), "permute: NULL output");
+  const int esz = dtype == FOREMOE_BF16 ? 2 : 4;
+  if ((int64_t)d * esz % 16 != 0)
+    return set_error(FOREMOE_EUNSUPPORTED, "permute: row of %d elements is not a multiple of 16 bytes", d);
+  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, plan->E), "permute: workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t npairs = T * (int64_t)K;
+  const int64_t nb = hist_blocks(npairs);
+  int32_t* status = (int32_t*)ws;
+  const int32_t* rep_slot = (const int32_t*)((char*)ws + kWsRepSlotOff);
+  const int32_t* base = (const int32_t*)((char*)ws + kWsPartialOff);
+  hipLaunchKernelGGL(permute_rank_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, plan->E,
+                     key_bits(plan->E), plan->R_max, base, rep_begin, rep_slot, slot_offset, plan->S, n_cap,
+                     pair_to_row, row_to_pair, status);
+  const int64_t vpr = (int64_t)d * esz / 16;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(gather_grid(n_cap)), dim3(256), 0, st, (const uint4*)x, vpr, K,
+                     npairs, row_to_pair, slot_offset + plan->S, n_cap, (uint4*)x_perm);
+  return check_launch("foremoe_permute");
+}
+
+static int launch_combine(const void* y_perm, foremoe_dtype in_dtype, const int32_t* pair_to_row, const float* gates,
+                          int64_t T, int32_t K, int32_t d, int64_t n_cap, void* y, foremoe_dtype out_dtype,
+                          hipStream_t st) {
+  const dim3 grid(gather_grid(T)), block(256);
+  if (in_dtype == FOREMOE_BF16 && out_dtype == FOREMOE_BF16)
+    hipLaunchKernelGGL((combine_kernel<uint16_t, uint16_t>), grid, block, 0, st, (const uint16_t*)y_perm, pair_to_row,
+                       gates, T, K, d, n_cap, (uint16_t*)y);
+  else if (in_dtype == FOREMOE_BF16 && out_dtype == FOREMOE_F32)
+    hipLaunchKernelGGL((combine_kernel<uint16_t, float>), grid, block, 0, st, (const uint16_t*)y_perm, pair_to_row,
+                       gates, T, K, d, n_cap, (float*)y);
+  else if (in_dtype == FOREMOE_F32 && out_dtype == FOREMOE_F32)
+    hipLaunchKernelGGL((combine_kernel<float, float>), grid, block, 0, st, (const float*)y_perm, pair_to_row, gates,
+                       T, K, d, n_cap, (float*)y);
+  else
+    return set_error(FOREMOE_EUNSUPPORTED, "combine: fp32 input with bf16 output is not supported");
+  return FOREMOE_OK;
+}
+
+static int check_gather_args(const char* who, foremoe_dtype in_dtype, foremoe_dtype out_dtype, int64_t T, int32_t K,
+                             int32_t d, int64_t n_cap) {
+  REQUIRE(in_dtype == FOREMOE_F32 || in_dtype == FOREMOE_BF16, "%s: bad input dtype", who);
+  REQUIRE(out_dtype == FOREMOE_F32 || out_dtype == FOREMOE_BF16, "%s: bad output dtype", who);
+  REQUIRE(T >= 0 && d >= 1 && n_cap >= 0, "%s: bad sizes", who);
+  REQUIRE(K >= 1 && K <= FOREMOE_MAX_TOPK, "%s: K out of range", who);
+  REQUIRE(T * (int64_t)K < (int64_t)INT_MAX && n_cap < (int64_t)INT_MAX, "%s: sizes must be below 2^31", who);
+  const int ve = in_dtype == FOREMOE_BF16 ? 8 : 4;
+  if (d % ve != 0) return set_error(FOREMOE_EUNSUPPORTED, "%s: d=%d must be a multiple of %d", who, d, ve);
+  return FOREMOE_OK;
+}
+
+int foremoe_combine(const void* y_perm, foremoe_dtype in_dtype, const int32_t* pair_to_row, const float* gates,
+                    int64_t T, int32_t K, int32_t d, int64_t n_cap, void* y, foremoe_dtype out_dtype, void* stream) {
+  int rc = check_gather_args("combine", in_dtype, out_dtype, T, K, d, n_cap);
+  if (rc) return rc;
+  REQUIRE(T == 0 || (pair_to_row && gates && y), "combine: NULL buffer");
+  REQUIRE(T == 0 || n_cap == 0 || y_perm, "combine: y_perm is NULL");
+  if (T == 0) return FOREMOE_OK;
+  rc = launch_combine(y_perm, in_dtype, pair_to_row, gates, T, K, d, n_cap, y, out_dtype, (hipStream_t)stream);
+  if (rc) return rc;
+  return check_launch("foremoe_combine");
+}
+
+int foremoe_permute_bwd(const void* dx_perm, foremoe_dtype in_dtype, const int32_t* pair_to_row, int64_t T, int32_t K,
+                        int32_t d, int64_t n_cap, void* dx, foremoe_dtype out_dtype, void* stream) {
+  int rc = check_gather_args("permute_bwd", in_dtype, out_dtype, T, K, d, n_cap);
+  if (rc) return rc;
+  REQUIRE(T == 0 || (pair_to_row && dx), "permute_bwd: NULL buffer");
+  REQUIRE(T == 0 || n_cap == 0 || dx_perm, "permute_bwd: dx_perm is NULL");
+  if (T == 0) return FOREMOE_OK;
+  rc = launch_combine(dx_perm, in_dtype, pair_to_row, nullptr, T, K, d, n_cap, dx, out_dtype, (hipStream_t)stream);
+  if (rc) return rc;
+  return check_launch("foremoe_permute_bwd");
+}
+
+int foremoe_combine_bwd(const void* dy, const void* y_perm, foremoe_dtype dtype, const int32_t* pair_to_row,
+                        const float* gates, int64_t T, int32_t K, int32_t d, int64_t n_cap, void* dy_perm,
+                        float* dgates, void* stream) {
+  int rc = check_gather_args("combine_bwd", dtype, dtype, T, K, d, n_cap);
+  if (rc) return rc;
+  REQUIRE(T == 0 || (dy && pair_to_row && gates), "combine_bwd: NULL input");
+  REQUIRE(T == 0 || n_cap == 0 || dy_perm, "combine_bwd: dy_perm is NULL");
+  REQUIRE(!dgates || T == 0 || n_cap == 0 || y_perm, "combine_bwd: dgates needs y_perm");
+  if (T == 0) return FOREMOE_OK;
+  hipStream_t st = (hipStream_t)stream;
+  const dim3 grid(gather_grid(T)), block(256);
+  if (dtype == FOREMOE_BF16)
+    hipLaunchKernelGGL(combine_bwd_kernel<uint16_t>, grid, block, 0, st, (const uint16_t*)dy, (const uint16_t*)y_perm,
+                       pair_to_row, gates, T, K, d, n_cap, (uint16_t*)dy_perm, dgates);
+  else
+    hipLaunchKernelGGL(combine_bwd_kernel<float>, grid, block, 0, st, (const float*)dy, (const float*)y_perm,
+                       pair_to_row, gates, T, K, d, n_cap, (float*)dy_perm, dgates);
+  return check_launch("foremoe_combine_bwd");
+}
+
+}  // extern "C"

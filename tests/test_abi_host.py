@@ -1,0 +1,118 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+declared in include/foremoe.h, and rejects bad arguments before touching the
+GPU (these calls return from host validation; no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "foremoe.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2606_11867_amd as fm
+    if not os.path.exists(fm.LIB_PATH):
+        from paper_2606_11867_amd import build
+        build.build()
+    return fm.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(foremoe_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_steps():
+    names = declared_functions()
+    for n in ["foremoe_histogram", "foremoe_assign_replicas", "foremoe_permute", "foremoe_grouped_ffn_fwd",
+              "foremoe_grouped_ffn_dgrad", "foremoe_grouped_ffn_wgrad", "foremoe_combine",
+              "foremoe_combine_bwd", "foremoe_permute_bwd"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_2606_11867_amd import _lib
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert name in _lib.SIGNATURES, f"{name} missing from the binding"
+
+
+def test_version_and_status_strings(lib):
+    assert b"gfx950" in lib.foremoe_version()
+    assert lib.foremoe_status_string(0) == b"ok"
+    assert lib.foremoe_status_string(-1) == b"invalid argument"
+    assert lib.foremoe_status_string(-2) == b"unsupported shape or dtype"
+
+
+def test_workspace_size(lib):
+    small = lib.foremoe_workspace_size(256, 2, 8)
+    assert small > 0 and small % 256 == 0
+    big = lib.foremoe_workspace_size(32768, 8, 256)
+    assert big > small
+    # status words, the replica->slot table, then [blocks][E+1] partial counts
+    assert big >= 256 + 4 * 1024 * 16 + 128 * 257 * 4
+    assert big - (256 + 4 * 1024 * 16 + 128 * 257 * 4) < 256
+    assert lib.foremoe_workspace_size(-1, 2, 8) == 0
+    assert lib.foremoe_workspace_size(10, 0, 8) == 0
+    assert lib.foremoe_workspace_size(10, 2, 2000) == 0
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+def test_histogram_rejects_bad_args(lib):
+    assert lib.foremoe_histogram(None, 10, 2, 8, FAKE, FAKE, 1 << 20, None) == -1
+    assert lib.foremoe_histogram(FAKE, 10, 0, 8, FAKE, FAKE, 1 << 20, None) == -1
+    assert lib.foremoe_histogram(FAKE, 10, 2, 0, FAKE, FAKE, 1 << 20, None) == -1
+    assert lib.foremoe_histogram(FAKE, 10, 2, 8, FAKE, FAKE, 16, None) == -1
+    assert b"workspace too small" in lib.foremoe_last_error()
+    assert lib.foremoe_histogram(FAKE, 1 << 29, 8, 8, FAKE, FAKE, 1 << 40, None) == -1
+
+
+def test_assign_rejects_bad_plan(lib):
+    from paper_2606_11867_amd._lib import Plan
+    p = Plan(8, 4, 0, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE)
+    assert lib.foremoe_assign_replicas(FAKE, ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    p = Plan(8, 5000, 2, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE)
+    assert lib.foremoe_assign_replicas(FAKE, ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert lib.foremoe_assign_replicas(FAKE, None, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+
+
+def test_permute_rejects_misaligned_rows(lib):
+    from paper_2606_11867_amd._lib import Plan
+    p = Plan(8, 4, 2, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE)
+    rc = lib.foremoe_permute(FAKE, 1, 16, 12, FAKE, 2, ctypes.byref(p), FAKE, FAKE, 32, FAKE, FAKE, FAKE, FAKE,
+                             1 << 20, None)
+    assert rc == -2  # 12 bf16 elements = 24 bytes, not a multiple of 16
+
+
+def test_ffn_rejects_unsupported_bf16_shapes(lib):
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 96, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None)
+    assert rc == -2
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 128, 200, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None)
+    assert rc == -2
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 7, 128, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None)
+    assert rc == -1
+    rc = lib.foremoe_grouped_ffn_wgrad(FAKE, FAKE, FAKE, FAKE, 1, 128, 128, 4, FAKE, FAKE, 0, 64, FAKE, FAKE, None)
+    assert rc == -1  # G < 1
+
+
+def test_gathers_reject_bad_args(lib):
+    assert lib.foremoe_combine(FAKE, 1, FAKE, FAKE, 16, 2, 12, 32, FAKE, 1, None) == -2   # d % 8
+    assert lib.foremoe_combine(FAKE, 0, FAKE, FAKE, 16, 2, 16, 32, FAKE, 1, None) == -2   # f32 -> bf16
+    assert lib.foremoe_combine(FAKE, 1, FAKE, FAKE, 16, 99, 16, 32, FAKE, 1, None) == -1  # K > 64
+    assert lib.foremoe_combine_bwd(FAKE, None, 1, FAKE, FAKE, 16, 2, 16, 32, FAKE, FAKE, None) == -1
+    assert lib.foremoe_permute_bwd(FAKE, 1, None, 16, 2, 16, 32, FAKE, 0, None) == -1
+
+
+def test_empty_calls_launch_nothing(lib):
+    # zero tokens: the gathers return before any launch
+    assert lib.foremoe_combine(None, 1, None, None, 0, 2, 16, 0, None, 1, None) == 0
+    assert lib.foremoe_permute_bwd(None, 1, None, 0, 2, 16, 0, None, 0, None) == 0
+    # zero slots: the FFN returns before any launch
+    assert lib.foremoe_grouped_ffn_fwd(None, 1, 128, 128, 0, FAKE, None, 1, None, None, 0, None, None, None,
+                                       None) == 0

@@ -1,0 +1,368 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Integer outputs (counts, replica boundaries, slot offsets, both index maps)
+and the permuted rows must be bit-exact. Floating-point outputs must satisfy
+max|err| <= 1e-2 * max|ref| + 1e-3 per tensor. Every input comes from the
+seeded generator; every expected value from the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle.foremoe_oracle as O
+from tests.gpu_helpers import (check_close, config_workload, custom_workload, gpu_dispatch, oracle_dispatch,
+                               rnd, tdtype, to_dev, to_np)
+
+pytestmark = pytest.mark.gpu
+
+SMALL = ["tinyf32", "small", "odd128", "share"]
+
+
+def _wl(name):
+    if name.startswith("cfg"):
+        return config_workload(int(name[3:]))
+    return custom_workload(name)
+
+
+def _ms(w, which="measured"):
+    return w.micro[w.measured] if which == "measured" else w.micro[which]
+
+
+def _print_case(name, w, m):
+    print(f"\n[case] {name}: {w.spec.name} micro-step {m.index} T={w.spec.T} d={w.spec.d} F={w.spec.F} "
+          f"E={w.spec.E} K={w.spec.K} S={m.plan.S}", flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Steps 1-3: bit-exact dispatch
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg2", "cfg3", "cfg4"])
+def test_dispatch_bit_exact(gpu, name):
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    ref = oracle_dispatch(w, m)
+    N = int(ref["slot_offset"][-1])
+    n_cap = N + 37
+    ref = oracle_dispatch(w, m, n_cap=n_cap)
+    got = gpu_dispatch(w, m, gpu, n_cap=n_cap)
+    torch.cuda.synchronize()
+    assert np.array_equal(got["counts"].cpu().numpy(), ref["counts"])
+    assert np.array_equal(got["rep_begin"].cpu().numpy(), ref["rep_begin"])
+    assert np.array_equal(got["slot_count"].cpu().numpy(), ref["slot_count"])
+    assert np.array_equal(got["slot_offset"].cpu().numpy(), ref["slot_offset"])
+    assert np.array_equal(got["pair_to_row"].cpu().numpy(), ref["pair_to_row"])
+    assert np.array_equal(got["row_to_pair"].cpu().numpy()[:N], ref["row_to_pair"][:N])
+    assert np.array_equal(to_np(got["x_perm"][:N]), ref["x_perm"][:N])  # bitwise: bf16/f32 -> f64 is exact
+    status = got["ws"][:256].view(torch.int32).cpu().numpy()
+    assert status[0] == ref["invalid"] and status[1] == 0 and status[2] == 0
+
+
+def test_dispatch_edge_cases(gpu):
+    """Padding and invalid ids, empty and duplicate slots, remote replicas,
+    unequal weights, and an n_cap overflow."""
+    from workload import plan_from_slots
+    rng = np.random.default_rng(5)
+    T, K, E, d = 333, 3, 10, 64
+    ids = rng.integers(0, E, size=(T, K)).astype(np.int32)
+    ids[rng.random((T, K)) < 0.1] = -1
+    ids[3, 0] = 57      # invalid
+    ids[200, 2] = -5    # invalid
+    x = rng.standard_normal((T, d)).astype(np.float32)
+    plan = plan_from_slots(E, [(1, 0), (4, 2), (0, 0), (4, 0), (9, 0), (1, 1), (7, 0)],
+                           nrep={4: 3, 1: 2, 0: 2}, rep_weights={4: [3, 0, 1], 1: [1, 4], 0: [2, 5]}, R_max=4)
+
+    class M:
+        pass
+    m = M()
+    m.ids, m.plan, m.index = ids, plan, 0
+
+    class Wl:
+        pass
+    wl = Wl()
+    wl.spec = type("s", (), {"dtype": "f32"})()
+    ref = oracle_dispatch(wl, m, x=x)
+    N = int(ref["slot_offset"][-1])
+    for n_cap in (N + 5, N - 11):
+        ref = oracle_dispatch(wl, m, n_cap=n_cap, x=x)
+        got = gpu_dispatch(wl, m, gpu, n_cap=n_cap, x=x)
+        torch.cuda.synchronize()
+        assert np.array_equal(got["counts"].cpu().numpy(), ref["counts"])
+        assert np.array_equal(got["rep_begin"].cpu().numpy(), ref["rep_begin"])
+        assert np.array_equal(got["slot_offset"].cpu().numpy(), ref["slot_offset"])
+        assert np.array_equal(got["pair_to_row"].cpu().numpy(), ref["pair_to_row"])
+        lim = min(N, n_cap)
+        assert np.array_equal(got["row_to_pair"].cpu().numpy()[:lim], ref["row_to_pair"][:lim])
+        assert np.array_equal(to_np(got["x_perm"][:lim]), ref["x_perm"][:lim])
+        status = got["ws"][:256].view(torch.int32).cpu().numpy()
+        assert status[0] == ref["invalid"] == 2
+        assert status[1] == max(0, N - n_cap) == ref["dropped"]
+        assert status[2] == 0
+
+
+def test_dispatch_plan_errors_are_flagged(gpu):
+    from workload import plan_from_slots
+    rng = np.random.default_rng(6)
+    T, K, E = 64, 2, 6
+    ids = rng.integers(0, E, size=(T, K)).astype(np.int32)
+    plan = plan_from_slots(E, [(0, 0), (1, 0), (0, 0), (2, 0)])  # slot 2 duplicates slot 0
+
+    class M:
+        pass
+    m = M()
+    m.ids, m.plan, m.index = ids, plan, 0
+
+    class Wl:
+        pass
+    wl = Wl()
+    wl.spec = type("s", (), {"dtype": "f32"})()
+    x = rng.standard_normal((T, 8)).astype(np.float32)
+    got = gpu_dispatch(wl, m, gpu, x=x)
+    torch.cuda.synchronize()
+    status = got["ws"][:256].view(torch.int32).cpu().numpy()
+    assert status[2] == 1                                  # one plan error
+    sc = got["slot_count"].cpu().numpy()
+    counts = got["counts"].cpu().numpy()
+    assert sc[2] == 0 and sc[0] == counts[0]                # lowest slot keeps the replica
+
+
+def test_dispatch_empty_and_all_padding(gpu):
+    from paper_2606_11867_amd import api
+    from workload import plan_from_slots
+    plan = plan_from_slots(4, [(0, 0), (1, 0)])
+    dp = api.DevicePlan.from_host(plan, gpu)
+    for T in (0, 40):
+        ids = torch.full((T, 2), -1, dtype=torch.int32, device=gpu)
+        ws = api.workspace(T, 2, 4, gpu)
+        counts = api.histogram(ids, 4, ws)
+        rb, sc, so = api.assign_replicas(counts, dp, ws)
+        x = torch.zeros((T, 16), dtype=torch.bfloat16, device=gpu)
+        xp, r2p, p2r = api.permute(x, ids, dp, rb, so, 8, ws)
+        torch.cuda.synchronize()
+        assert counts.cpu().tolist() == [0, 0, 0, 0]
+        assert so.cpu().tolist() == [0, 0, 0]
+        assert bool((p2r == -1).all())
+
+
+# ---------------------------------------------------------------------------
+# Step 4: grouped SwiGLU FFN, per call, inputs from the generator/oracle
+# ---------------------------------------------------------------------------
+def _ffn_inputs(w, m):
+    ref = oracle_dispatch(w, m)
+    N = int(ref["slot_offset"][-1])
+    gu, dn = w.weights(m.plan)
+    x_perm = ref["x_perm"][:N]
+    return ref, N, gu, dn, x_perm
+
+
+@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
+def test_ffn_forward(gpu, name):
+    from paper_2606_11867_amd import api
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    ref, N, gu, dn, x_perm = _ffn_inputs(w, m)
+    f = O.ffn_forward(x_perm, ref["slot_offset"], m.plan.slot_widx, gu, dn)
+    dt = tdtype(w)
+    so = torch.from_numpy(ref["slot_offset"]).to(gpu)
+    widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+    h, y, au = api.grouped_ffn_fwd(to_dev(x_perm, dt, gpu), so, widx, to_dev(gu, dt, gpu), to_dev(dn, dt, gpu))
+    torch.cuda.synchronize()
+    check_close("H", to_np(h), f["H"])
+    check_close("Y", to_np(y), f["Y"])
+    check_close("A", to_np(au[:, : w.spec.F]), f["A"])
+    check_close("U", to_np(au[:, w.spec.F:]), f["U"])
+
+
+def _sampled_rows(ref, m, rng, per_slot=6):
+    """A few rows of every non-empty slot, regrouped as a small slot table."""
+    off = ref["slot_offset"]
+    rows, sub_off, widx = [], [0], []
+    for j in range(m.plan.S):
+        lo, hi = int(off[j]), int(off[j + 1])
+        if hi <= lo:
+            continue
+        pick = np.unique(np.concatenate([[lo, hi - 1], rng.integers(lo, hi, size=per_slot)]))
+        rows.extend(pick.tolist())
+        sub_off.append(sub_off[-1] + len(pick))
+        widx.append(int(m.plan.slot_widx[j]))
+    return np.array(rows), np.array(sub_off), np.array(widx)
+
+
+@pytest.mark.parametrize("name", ["cfg2", "cfg4"])
+def test_ffn_forward_sampled_rows_full_size(gpu, name):
+    """Full-size forward; the oracle recomputes sampled rows of every slot."""
+    from paper_2606_11867_amd import api
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    got = gpu_dispatch(w, m, gpu)
+    gu, dn = w.weights(m.plan)
+    dt = tdtype(w)
+    widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+    h, y, au = api.grouped_ffn_fwd(got["x_perm"], got["slot_offset"], widx, to_dev(gu, dt, gpu),
+                                   to_dev(dn, dt, gpu))
+    torch.cuda.synchronize()
+    ref = oracle_dispatch(w, m)
+    rows, sub_off, sub_widx = _sampled_rows(ref, m, np.random.default_rng(0))
+    f = O.ffn_forward(ref["x_perm"][rows], sub_off, sub_widx, gu, dn)
+    check_close("H", to_np(h[torch.from_numpy(rows).to(gpu)]), f["H"])
+    check_close("Y", to_np(y[torch.from_numpy(rows).to(gpu)]), f["Y"])
+
+
+@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
+def test_ffn_backward(gpu, name):
+    from paper_2606_11867_amd import api
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    ref, N, gu, dn, x_perm = _ffn_inputs(w, m)
+    f = O.ffn_forward(x_perm, ref["slot_offset"], m.plan.slot_widx, gu, dn)
+    rng = np.random.default_rng(77)
+    dy_perm = rnd(w, rng.standard_normal((N, w.spec.d)))
+    au = rnd(w, np.concatenate([f["A"], f["U"]], axis=1))
+    hq = rnd(w, f["H"])
+    F = w.spec.F
+    g = O.ffn_dgrad(dy_perm, au[:, :F], au[:, F:], ref["slot_offset"], m.plan.slot_widx, gu, dn)
+    dt = tdtype(w)
+    so = torch.from_numpy(ref["slot_offset"]).to(gpu)
+    widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+    gidx = torch.from_numpy(m.plan.slot_gidx).to(gpu)
+    d_au, dx = api.grouped_ffn_dgrad(to_dev(dy_perm, dt, gpu), to_dev(au, dt, gpu), so, widx, to_dev(gu, dt, gpu),
+                                     to_dev(dn, dt, gpu))
+    torch.cuda.synchronize()
+    check_close("dA", to_np(d_au[:, :F]), g["dA"])
+    check_close("dU", to_np(d_au[:, F:]), g["dU"])
+    check_close("dX", to_np(dx), g["dX"])
+    # weight gradient from the same (rounded) operands, accumulated onto a non-zero start
+    dau_q = rnd(w, np.concatenate([g["dA"], g["dU"]], axis=1))
+    G = m.plan.G
+    start_gu = rng.standard_normal((G, 2 * F, w.spec.d)).astype(np.float32)
+    start_dn = rng.standard_normal((G, w.spec.d, F)).astype(np.float32)
+    dwgu = torch.from_numpy(start_gu.copy()).to(gpu)
+    dwdn = torch.from_numpy(start_dn.copy()).to(gpu)
+    api.grouped_ffn_wgrad(to_dev(x_perm, dt, gpu), to_dev(hq, dt, gpu), to_dev(dy_perm, dt, gpu),
+                          to_dev(dau_q, dt, gpu), so, gidx, dwgu, dwdn)
+    torch.cuda.synchronize()
+    rgu, rdn = O.ffn_wgrad(x_perm, hq, dy_perm, dau_q[:, :F], dau_q[:, F:], ref["slot_offset"], m.plan.slot_gidx, G,
+                           start_gu.astype(np.float64), start_dn.astype(np.float64))
+    check_close("dW_gate_up", to_np(dwgu), rgu)
+    check_close("dW_down", to_np(dwdn), rdn)
+
+
+# ---------------------------------------------------------------------------
+# Step 5 and the backward gathers
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3", "cfg4"])
+def test_gathers(gpu, name):
+    from paper_2606_11867_amd import api
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    ref = oracle_dispatch(w, m)
+    T, K = m.ids.shape
+    N = int(ref["slot_offset"][-1])
+    n_cap = max(N, 1)
+    rng = np.random.default_rng(3)
+    d = w.spec.d
+    y_perm = rnd(w, rng.standard_normal((n_cap, d)))
+    dy = rnd(w, rng.standard_normal((T, d)))
+    dt = tdtype(w)
+    p2r = torch.from_numpy(ref["pair_to_row"]).to(gpu)
+    gates = torch.from_numpy(m.gates).to(gpu)
+    yp = to_dev(y_perm, dt, gpu)
+    exp_y = O.combine(y_perm, ref["pair_to_row"], m.gates, T, K)
+    for out in ([torch.float32, torch.bfloat16] if dt == torch.bfloat16 else [torch.float32]):
+        y = api.combine(yp, p2r, gates, out_dtype=out)
+        torch.cuda.synchronize()
+        check_close(f"y[{out}]", to_np(y), exp_y)
+    exp_dyp, exp_dg = O.combine_bwd(dy, y_perm, ref["row_to_pair"], m.gates, N, T, K)
+    dyp, dg = api.combine_bwd(to_dev(dy, dt, gpu), yp, p2r, gates)
+    torch.cuda.synchronize()
+    check_close("dy_perm", to_np(dyp[:N]), exp_dyp[:N])
+    check_close("dgates", to_np(dg), exp_dg)
+    exp_dx = O.permute_bwd(y_perm, ref["pair_to_row"], T, K)
+    dx = api.permute_bwd(yp, p2r, T, K, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    check_close("dx", to_np(dx), exp_dx)
+
+
+# ---------------------------------------------------------------------------
+# The whole layer, forward + backward, each side with its own intermediates
+# ---------------------------------------------------------------------------
+def run_gpu_layer(w, m, gpu, dy, dw_gate_up=None, dw_down=None):
+    from paper_2606_11867_amd import api
+    T, K = m.ids.shape
+    d = w.spec.d
+    got = gpu_dispatch(w, m, gpu)
+    dt = tdtype(w)
+    gu, dn = w.weights(m.plan)
+    gud, dnd = to_dev(gu, dt, gpu), to_dev(dn, dt, gpu)
+    widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+    gidx = torch.from_numpy(m.plan.slot_gidx).to(gpu)
+    gates = torch.from_numpy(m.gates).to(gpu)
+    h, y_perm, au = api.grouped_ffn_fwd(got["x_perm"], got["slot_offset"], widx, gud, dnd)
+    y = api.combine(y_perm, got["pair_to_row"], gates, out_dtype=torch.float32)
+    dyp, dg = api.combine_bwd(to_dev(dy, dt, gpu), y_perm, got["pair_to_row"], gates)
+    d_au, dxp = api.grouped_ffn_dgrad(dyp, au, got["slot_offset"], widx, gud, dnd)
+    if dw_gate_up is None:
+        dw_gate_up = torch.zeros((m.plan.G, 2 * w.spec.F, d), dtype=torch.float32, device=gpu)
+        dw_down = torch.zeros((m.plan.G, d, w.spec.F), dtype=torch.float32, device=gpu)
+    api.grouped_ffn_wgrad(got["x_perm"], h, dyp, d_au, got["slot_offset"], gidx, dw_gate_up, dw_down)
+    dx = api.permute_bwd(dxp, got["pair_to_row"], T, K, out_dtype=torch.float32)
+    return dict(y=y, dgates=dg, dx=dx, dw_gate_up=dw_gate_up, dw_down=dw_down)
+
+
+@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
+def test_layer_chain(gpu, name):
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    T, K = m.ids.shape
+    dy = w.dy(m.index)
+    got = run_gpu_layer(w, m, gpu, dy)
+    torch.cuda.synchronize()
+    gu, dn = w.weights(m.plan)
+    N = int(oracle_dispatch(w, m)["slot_offset"][-1])
+    fwd = O.layer_forward(w.x(m.index), m.ids, m.gates, m.plan, gu, dn, n_cap=max(N, 1))
+    bwd = O.layer_backward(fwd, dy, m.gates, m.plan, gu, dn, T, K)
+    check_close("y", to_np(got["y"]), fwd["y"])
+    check_close("dgates", to_np(got["dgates"]), bwd["dgates"])
+    check_close("dx", to_np(got["dx"]), bwd["dx"])
+    check_close("dW_gate_up", to_np(got["dw_gate_up"]), bwd["dw_gate_up"])
+    check_close("dW_down", to_np(got["dw_down"]), bwd["dw_down"])
+
+
+def test_policy_update_accumulates_over_micro_steps(gpu):
+    """16 micro-steps with independently jittered routing and a replica
+    choice per micro-step; main-expert fp32 gradients accumulate over all."""
+    from workload import make_custom
+    w = make_custom(T=1024, d=256, F=128, E=32, K=4, P=4, n_rep=2, seed=41, micro_steps=16)
+    G = w.micro[0].plan.G
+    d, F = w.spec.d, w.spec.F
+    dwgu = torch.zeros((G, 2 * F, d), dtype=torch.float32, device=gpu)
+    dwdn = torch.zeros((G, d, F), dtype=torch.float32, device=gpu)
+    rgu = np.zeros((G, 2 * F, d))
+    rdn = np.zeros((G, d, F))
+    for m in w.micro:
+        assert np.array_equal(m.plan.local_experts, w.micro[0].plan.local_experts)
+        T, K = m.ids.shape
+        dy = w.dy(m.index)
+        run_gpu_layer(w, m, gpu, dy, dwgu, dwdn)
+        gu, dn = w.weights(m.plan)
+        fwd = O.layer_forward(w.x(m.index), m.ids, m.gates, m.plan, gu, dn)
+        O.layer_backward(fwd, dy, m.gates, m.plan, gu, dn, T, K, rgu, rdn)
+    torch.cuda.synchronize()
+    check_close("dW_gate_up(16)", to_np(dwgu), rgu)
+    check_close("dW_down(16)", to_np(dwdn), rdn)
+
+
+def test_determinism(gpu):
+    w = custom_workload("share")
+    m = _ms(w)
+    dy = w.dy(m.index)
+    a = run_gpu_layer(w, m, gpu, dy)
+    b = run_gpu_layer(w, m, gpu, dy)
+    torch.cuda.synchronize()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
