@@ -1,0 +1,313 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-micro-step MoE expert layer on one MI355X.
+
+Workload: the Qwen3-30B-A3B-shaped EP=8 rank share in the policy-update
+stage (T=16384 tokens, d=2048, F=768, E=128, top-8, 16 hosted experts + 4
+replica slots, 16 micro-steps with independently jittered routing). One
+step = one micro-step through every step of the path:
+
+  histogram -> assign_replicas -> permute -> gate/up (+SwiGLU) -> down
+  -> combine -> combine_bwd -> down dgrad (+SwiGLU') -> gate/up dgrad
+  -> gate/up wgrad -> down wgrad -> permute_bwd
+
+All inputs are resident in HBM before timing. Each ABI call is bracketed by
+HIP events on the stream it runs on; the dominant kernel's average duration
+gives the roofline line. The fp64 CPU oracle is timed on one micro-step as
+the CPU baseline.
+
+    python bench.py [--gpus 1] [--steps 32] [--warmup 16] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "grouped-FFN TFLOP/s & % bf16 MFMA peak; permute+combine GB/s; tokens/s per micro-step"
+
+PHASES = ["histogram", "assign_replicas", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
+          "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
+# phases that are exactly one kernel launch (candidates for the roofline line)
+SINGLE_LAUNCH = {"assign_replicas", "gate_up_fwd", "down_fwd", "combine", "combine_bwd", "down_dgrad",
+                 "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
+    return ap.parse_args()
+
+
+def main() -> int:
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU's share of the expert layer; --gpus {args.gpus} "
+              f"(WORLD_SIZE={world}) is not supported: the multi-GPU path (EP All-to-All over xGMI) "
+              "is not part of this build", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2606_11867_amd import _lib, api
+    from workload import CONFIGS, make_workload
+    from workload import accounting as acc
+
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    spec = CONFIGS[5]
+    t0 = time.time()
+    w = make_workload(5)
+    n_micro = min(args.micro_steps, len(w.micro))
+    T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
+    bf = torch.bfloat16
+
+    def dv(a, dt=bf):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev).to(dt)
+
+    # ---- resident inputs: routing, plans, activations, upstream grads, weights
+    local = w.micro[0].plan.local_experts
+    gu_h, dn_h = w.weights(w.micro[0].plan)
+    gu, dn = dv(gu_h), dv(dn_h)
+    G = int(len(local))
+    mss = []
+    for i in range(n_micro):
+        m = w.micro[i]
+        assert np.array_equal(m.plan.local_experts, local)
+        dp = api.DevicePlan.from_host(m.plan, dev)
+        mss.append(dict(ids=torch.from_numpy(m.ids).to(dev), gates=torch.from_numpy(m.gates).to(dev),
+                        x=dv(w.x(i)), dy=dv(w.dy(i)), plan=dp, cplan=dp.c_struct(), S=m.plan.S))
+    S_max = max(ms["S"] for ms in mss)
+    n_cap = T * K
+    z = lambda *s, dt=bf: torch.zeros(s, dtype=dt, device=dev)  # noqa: E731
+    buf = dict(
+        counts=z(E, dt=torch.int32), rep_begin=z(E, 3, dt=torch.int32), slot_count=z(S_max, dt=torch.int32),
+        slot_offset=z(S_max + 1, dt=torch.int32), ws=api.workspace(T, K, E, dev),
+        x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
+        y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d), dy_perm=z(n_cap, d), dgates=z(T, K, dt=torch.float32),
+        d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d), dx=z(T, d),
+        dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32))
+    P = {k: v.data_ptr() for k, v in buf.items()}
+    wsz = buf["ws"].numel()
+    stream = torch.cuda.current_stream(dev)
+    sp = stream.cuda_stream
+    BF16 = _lib.BF16
+    setup_s = time.time() - t0
+
+    def chk(rc, what):
+        if rc != 0:
+            raise _lib.ForeMoEError(rc, what)
+
+    def run_step(i, ev=None):
+        ms = mss[i % n_micro]
+        S = ms["S"]
+        so = P["slot_offset"]
+        widx, gidx = ms["plan"].slot_widx.data_ptr(), ms["plan"].slot_gidx.data_ptr()
+        cp = ctypes.byref(ms["cplan"])
+
+        def mark(k):
+            if ev is not None:
+                ev[k].record(stream)
+        mark(0)
+        chk(lib.foremoe_histogram(ms["ids"].data_ptr(), T, K, E, P["counts"], P["ws"], wsz, sp), "histogram")
+        mark(1)
+        chk(lib.foremoe_assign_replicas(P["counts"], cp, P["rep_begin"], P["slot_count"], so, P["ws"], wsz, sp),
+            "assign")
+        mark(2)
+        chk(lib.foremoe_permute(ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so,
+                                n_cap, P["x_perm"], P["r2p"], P["p2r"], P["ws"], wsz, sp), "permute")
+        mark(3)
+        chk(lib.foremoe_ffn_gate_up_fwd(P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"],
+                                        P["au"], sp), "gate_up_fwd")
+        mark(4)
+        chk(lib.foremoe_ffn_down_fwd(P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], sp),
+            "down_fwd")
+        mark(5)
+        chk(lib.foremoe_combine(P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap, P["y"], BF16,
+                                sp), "combine")
+        mark(6)
+        chk(lib.foremoe_combine_bwd(ms["dy"].data_ptr(), P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K,
+                                    d, n_cap, P["dy_perm"], P["dgates"], sp), "combine_bwd")
+        mark(7)
+        chk(lib.foremoe_ffn_down_dgrad(P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap,
+                                       P["d_au"], sp), "down_dgrad")
+        mark(8)
+        chk(lib.foremoe_ffn_gate_up_dgrad(P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap,
+                                          P["dx_perm"], sp), "gate_up_dgrad")
+        mark(9)
+        chk(lib.foremoe_ffn_gate_up_wgrad(P["d_au"], P["x_perm"], BF16, d, F, S, so, gidx, G, n_cap, P["dwgu"],
+                                          sp), "gate_up_wgrad")
+        mark(10)
+        chk(lib.foremoe_ffn_down_wgrad(P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"], sp),
+            "down_wgrad")
+        mark(11)
+        chk(lib.foremoe_permute_bwd(P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], BF16, sp),
+            "permute_bwd")
+        mark(12)
+
+    # ---- realised per-micro-step sizes (read back once, outside the timed region)
+    Ns, Gs = [], []
+    for i in range(n_micro):
+        run_step(i)
+        torch.cuda.synchronize()
+        S = mss[i]["S"]
+        sc = buf["slot_count"][:S].cpu().numpy()
+        Ns.append(int(buf["slot_offset"][S].item()))
+        gidx = mss[i]["plan"].slot_gidx.cpu().numpy()
+        Gs.append(int(len(set(gidx[sc > 0].tolist()))))
+
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(PHASES) + 1)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for s in range(args.steps):
+        run_step(s, evs[s])
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    phase_ms = {p: 0.0 for p in PHASES}
+    for s in range(args.steps):
+        for k, p in enumerate(PHASES):
+            phase_ms[p] += evs[s][k].elapsed_time(evs[s][k + 1])
+
+    # ---- algorithmic work of the timed steps
+    work = {p: {"flop": 0.0, "bytes": 0.0} for p in PHASES}
+    for s in range(args.steps):
+        N, g = Ns[s % n_micro], Gs[s % n_micro]
+        work["histogram"]["bytes"] += 4.0 * T * K
+        work["permute"]["bytes"] += acc.permute_bytes(N, T, K, d, 2)
+        work["gate_up_fwd"]["flop"] += acc.gate_up_flops(N, d, F)
+        work["gate_up_fwd"]["bytes"] += 2.0 * (N * d + g * 2 * F * d + N * F + N * 2 * F)
+        work["down_fwd"]["flop"] += acc.down_flops(N, d, F)
+        work["down_fwd"]["bytes"] += 2.0 * (N * F + g * d * F + N * d)
+        work["combine"]["bytes"] += acc.combine_bytes(N, T, K, d, 2, 2)
+        work["combine_bwd"]["bytes"] += acc.combine_bwd_bytes(N, T, K, d, 2)
+        work["down_dgrad"]["flop"] += acc.down_flops(N, d, F)
+        work["down_dgrad"]["bytes"] += 2.0 * (N * d + g * d * F + N * 2 * F + N * 2 * F)
+        work["gate_up_dgrad"]["flop"] += acc.gate_up_flops(N, d, F)
+        work["gate_up_dgrad"]["bytes"] += 2.0 * (N * 2 * F + g * 2 * F * d + N * d)
+        work["gate_up_wgrad"]["flop"] += acc.gate_up_flops(N, d, F)
+        work["gate_up_wgrad"]["bytes"] += 2.0 * (N * 2 * F + N * d) + 2.0 * g * 2 * F * d * 4
+        work["down_wgrad"]["flop"] += acc.down_flops(N, d, F)
+        work["down_wgrad"]["bytes"] += 2.0 * (N * d + N * F) + 2.0 * g * d * F * 4
+        work["permute_bwd"]["bytes"] += acc.permute_bwd_bytes(N, T, K, d, 2, 2)
+
+    kernels = {}
+    for p in PHASES:
+        t_s = phase_ms[p] / 1e3
+        fl, by = work[p]["flop"], work[p]["bytes"]
+        t_mfma = fl / acc.PEAK_BF16_DENSE_FLOPS
+        t_hbm = by / acc.PEAK_HBM_BYTES_PER_S
+        if fl > 0 and t_mfma >= t_hbm:
+            bound, ach, peak, unit = "mfma", fl / t_s / 1e12, acc.PEAK_BF16_DENSE_FLOPS / 1e12, "TFLOP/s"
+        else:
+            bound, ach, peak, unit = "hbm", by / t_s / 1e9, acc.PEAK_HBM_BYTES_PER_S / 1e9, "GB/s"
+        kernels[p] = {"us_per_step": round(phase_ms[p] * 1e3 / args.steps, 2), "bound": bound,
+                      "achieved": round(ach, 2), "unit": unit, "frac": round(ach / peak, 4),
+                      "tflops": round(fl / t_s / 1e12, 2) if fl else None,
+                      "gbs": round(by / t_s / 1e9, 1)}
+    dom = max((p for p in PHASES if p in SINGLE_LAUNCH), key=lambda p: phase_ms[p])
+    kd = kernels[dom]
+    per_launch_us = phase_ms[dom] * 1e3 / args.steps
+    roofline = {"bound": kd["bound"], "achieved": kd["achieved"],
+                "peak": round((acc.PEAK_BF16_DENSE_FLOPS / 1e12) if kd["bound"] == "mfma"
+                              else acc.PEAK_HBM_BYTES_PER_S / 1e9, 1),
+                "unit": kd["unit"], "frac": kd["frac"], "traffic": None, "kernel": dom,
+                "avg_launch_us": round(per_launch_us, 2)}
+
+    ffn = ["gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad"]
+    ffn_flop = sum(work[p]["flop"] for p in ffn)
+    ffn_s = sum(phase_ms[p] for p in ffn) / 1e3
+    fwd_ph = ["histogram", "assign_replicas", "permute", "gate_up_fwd", "down_fwd", "combine"]
+    fwd_s = sum(phase_ms[p] for p in fwd_ph) / 1e3
+    ffn_fwd_s = (phase_ms["gate_up_fwd"] + phase_ms["down_fwd"]) / 1e3
+    ffn_fwd_flop = work["gate_up_fwd"]["flop"] + work["down_fwd"]["flop"]
+    value = T * args.steps / (total_ms / 1e3)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Zipf s=1.1 + Dirichlet a=0.3 routing; N(0,1) tokens and upstream grads; "
+                "N(0,1/fan_in) weights)",
+        "config": {"workload": "qwen3-30b-a3b EP=8 rank share, policy-update micro-step (fwd+bwd)",
+                   "T": T, "d": d, "F": F, "E": E, "K": K, "local_experts": G, "slots": S_max,
+                   "micro_steps": n_micro, "n_pairs_mean": round(float(np.mean(Ns)), 1),
+                   "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns))},
+        "roofline": roofline,
+        "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),
+        "grouped_ffn_frac_bf16_peak": round(ffn_flop / ffn_s / acc.PEAK_BF16_DENSE_FLOPS, 4),
+        "grouped_ffn_fwd_tflops": round(ffn_fwd_flop / ffn_fwd_s / 1e12, 2),
+        "permute_gbs": kernels["permute"]["gbs"],
+        "combine_gbs": kernels["combine"]["gbs"],
+        "forward_tokens_per_s": round(T * args.steps / fwd_s, 1),
+        "kernels": kernels,
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def cpu_baseline(w, budget_s: float = 10.0) -> dict:
+    """The fp64 oracle on whole micro-steps (forward + backward, gradients
+    accumulated over micro-steps), run until about `budget_s` of CPU time."""
+    import numpy as np
+
+    import oracle.foremoe_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = 1
+    T, K = w.micro[0].ids.shape
+    gu, dn = w.weights(w.micro[0].plan)
+    G = w.micro[0].plan.G
+    dwgu = np.zeros((G, gu.shape[1], gu.shape[2]))
+    dwdn = np.zeros((G, dn.shape[1], dn.shape[2]))
+    done, pairs, dt = 0, 0, 0.0
+    while done < len(w.micro) and (done == 0 or dt < budget_s):
+        m = w.micro[done]
+        x, dy = w.x(done), w.dy(done)
+        t0 = time.perf_counter()
+        fwd = O.layer_forward(x, m.ids, m.gates, m.plan, gu, dn, n_cap=T * K)
+        O.layer_backward(fwd, dy, m.gates, m.plan, gu, dn, T, K, dwgu, dwdn)
+        dt += time.perf_counter() - t0
+        pairs += int(fwd["slot_offset"][-1])
+        done += 1
+    return {"value": round(T * done / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"micro-steps 0..{done - 1} of the same workload ({done} x {T} tokens, {pairs} local "
+                      f"pairs), forward + backward in fp64 numpy, gradients accumulated; "
+                      f"{dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -10,15 +10,22 @@ import numpy as np
 
 
 def f32_to_bf16_bits(a) -> np.ndarray:
-    """Round float32 values to bfloat16 (RNE); return the uint16 bit patterns."""
+    """Round float32 values to bfloat16 (RNE); return the uint16 bit patterns.
+
+    For finite inputs the 32-bit sum below cannot wrap (the largest finite
+    pattern 0xFF7FFFFF plus 0x8000 stays below 2^32).
+    """
     a = np.ascontiguousarray(a, dtype=np.float32)
-    if not np.all(np.isfinite(a)):
+    bits = a.view(np.uint32)
+    if np.any((bits & np.uint32(0x7F800000)) == np.uint32(0x7F800000)):
         raise ValueError("bf16 rounding expects finite inputs")
-    bits = a.view(np.uint32).astype(np.uint64)
-    lsb = (bits >> np.uint64(16)) & np.uint64(1)
-    rounded = (bits + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
-    out = rounded.astype(np.uint16)
-    if np.any((out & 0x7F80) == 0x7F80):
+    r = bits >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += bits
+    r >>= np.uint32(16)
+    out = r.astype(np.uint16)
+    if np.any((out & np.uint16(0x7F80)) == np.uint16(0x7F80)):
         raise ValueError("value overflows bfloat16")
     return out
 
