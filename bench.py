@@ -36,7 +36,7 @@ PHASES = ["histogram", "assign_replicas", "permute", "gate_up_fwd", "down_fwd", 
           "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
 # phases that are exactly one kernel launch (candidates for the roofline line)
 SINGLE_LAUNCH = {"assign_replicas", "gate_up_fwd", "down_fwd", "combine", "combine_bwd", "down_dgrad",
-                 "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"}
+                 "gate_up_dgrad", "permute_bwd"}
 
 
 def parse():
@@ -99,9 +99,11 @@ def main() -> int:
         x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
         y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d), dy_perm=z(n_cap, d), dgates=z(T, K, dt=torch.float32),
         d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d), dx=z(T, d),
-        dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32))
+        dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32),
+        wws=api.wgrad_workspace(d, F, dev))
     P = {k: v.data_ptr() for k, v in buf.items()}
     wsz = buf["ws"].numel()
+    wwsz = buf["wws"].numel()
     stream = torch.cuda.current_stream(dev)
     sp = stream.cuda_stream
     BF16 = _lib.BF16
@@ -149,10 +151,10 @@ def main() -> int:
                                           P["dx_perm"], sp), "gate_up_dgrad")
         mark(9)
         chk(lib.foremoe_ffn_gate_up_wgrad(P["d_au"], P["x_perm"], BF16, d, F, S, so, gidx, G, n_cap, P["dwgu"],
-                                          sp), "gate_up_wgrad")
+                                          P["wws"], wwsz, sp), "gate_up_wgrad")
         mark(10)
-        chk(lib.foremoe_ffn_down_wgrad(P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"], sp),
-            "down_wgrad")
+        chk(lib.foremoe_ffn_down_wgrad(P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"],
+                                       P["wws"], wwsz, sp), "down_wgrad")
         mark(11)
         chk(lib.foremoe_permute_bwd(P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], BF16, sp),
             "permute_bwd")

@@ -171,8 +171,9 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
  * save_au    [n_cap, 2F] out or NULL: A in columns [0, F), U in [F, 2F)
  *            (needed by foremoe_grouped_ffn_dgrad)
  * All tensors are `dtype`. bf16 runs on bf16 MFMA with fp32 accumulation
- * and needs d % 128 == 0 and F % 128 == 0 (else FOREMOE_EUNSUPPORTED); f32
- * accepts any d, F >= 1. 0 <= S <= FOREMOE_MAX_SLOTS.
+ * and needs d % 128 == 0, F % 128 == 0 and (n_cap + 256) * max(d, 2F) * 2
+ * below 2^31 (else FOREMOE_EUNSUPPORTED); f32 accepts any d, F >= 1.
+ * 0 <= S <= FOREMOE_MAX_SLOTS.
  * foremoe_grouped_ffn_fwd = foremoe_ffn_gate_up_fwd then foremoe_ffn_down_fwd;
  * each of these two is a single kernel launch.
  */
@@ -219,23 +220,31 @@ int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, 
  *   dW_gate_up[g] += [dA | dU]^T X,   dW_down[g] += dY^T H
  * summed over the rows of every slot j with slot_gidx[j] == g, in slot
  * order. ACCUMULATES (+=) into fp32 dw_gate_up [G, 2F, d] and
- * dw_down [G, d, F], so gradients add up over micro-steps. Each output
- * element is owned by one workgroup (no atomics). 1 <= G <= FOREMOE_MAX_SLOTS.
- * = foremoe_ffn_gate_up_wgrad then foremoe_ffn_down_wgrad (one launch each).
+ * dw_down [G, d, F], so gradients add up over micro-steps.
+ * ws, ws_bytes: optional device scratch for splitting one expert's rows over
+ *   many workgroups (fp32 partial tiles, summed in a fixed order by a second
+ *   kernel of the same call). foremoe_wgrad_workspace_size(d, F) bytes give
+ *   the full split; NULL/0 runs without splitting (slower for skewed loads,
+ *   same result). Calls sharing one ws must be ordered on one stream.
+ * No float atomics: each output element's summation order is fixed, so the
+ * result is deterministic. 1 <= G <= FOREMOE_MAX_SLOTS.
+ * = foremoe_ffn_gate_up_wgrad then foremoe_ffn_down_wgrad (each one main
+ *   kernel, plus one reduction kernel when ws is given).
  */
+size_t foremoe_wgrad_workspace_size(int32_t d, int32_t F);
 int foremoe_grouped_ffn_wgrad(const void* x_perm, const void* h, const void* dy_perm,
                               const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F,
                               int32_t S, const int32_t* slot_offset, const int32_t* slot_gidx,
                               int32_t G, int64_t n_cap, float* dw_gate_up, float* dw_down,
-                              void* stream);
+                              void* ws, size_t ws_bytes, void* stream);
 int foremoe_ffn_gate_up_wgrad(const void* d_au, const void* x_perm, foremoe_dtype dtype,
                               int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
                               const int32_t* slot_gidx, int32_t G, int64_t n_cap,
-                              float* dw_gate_up, void* stream);
+                              float* dw_gate_up, void* ws, size_t ws_bytes, void* stream);
 int foremoe_ffn_down_wgrad(const void* dy_perm, const void* h, foremoe_dtype dtype,
                            int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
                            const int32_t* slot_gidx, int32_t G, int64_t n_cap,
-                           float* dw_down, void* stream);
+                           float* dw_down, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Step 5 (Sec. 2.1: the output is the router-probability weighted sum of

@@ -52,12 +52,13 @@ SIGNATURES = {
                                               c_i64, c_p, c_p]),
     "foremoe_ffn_gate_up_dgrad": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
                                                  c_i64, c_p, c_p]),
+    "foremoe_wgrad_workspace_size": (c_sz, [c_i32, c_i32]),
     "foremoe_grouped_ffn_wgrad": (ctypes.c_int, [c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p,
-                                                 c_i32, c_i64, c_p, c_p, c_p]),
+                                                 c_i32, c_i64, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_gate_up_wgrad": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32,
-                                                 c_i64, c_p, c_p]),
+                                                 c_i64, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_down_wgrad": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32,
-                                              c_i64, c_p, c_p]),
+                                              c_i64, c_p, c_p, c_sz, c_p]),
     "foremoe_combine": (ctypes.c_int, [c_p, c_i32, c_p, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_i32, c_p]),
     "foremoe_combine_bwd": (ctypes.c_int, [c_p, c_p, c_i32, c_p, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_p,
                                            c_p]),

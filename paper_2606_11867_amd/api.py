@@ -163,19 +163,29 @@ def grouped_ffn_dgrad(dy_perm: torch.Tensor, save_au: torch.Tensor, slot_offset:
     return d_au, dx_perm
 
 
+def wgrad_workspace(d: int, F: int, device) -> torch.Tensor:
+    """Scratch for splitting hot experts' weight gradients over many CUs."""
+    n = _lib.load().foremoe_wgrad_workspace_size(d, F)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
 def grouped_ffn_wgrad(x_perm: torch.Tensor, h: torch.Tensor, dy_perm: torch.Tensor, d_au: torch.Tensor,
                       slot_offset: torch.Tensor, slot_gidx: torch.Tensor, dw_gate_up: torch.Tensor,
-                      dw_down: torch.Tensor) -> None:
-    """Accumulates (+=) into the fp32 gradients dw_gate_up [G, 2F, d], dw_down [G, d, F]."""
+                      dw_down: torch.Tensor, ws: Optional[torch.Tensor] = None) -> None:
+    """Accumulates (+=) into the fp32 gradients dw_gate_up [G, 2F, d], dw_down [G, d, F].
+
+    ``ws`` (from ``wgrad_workspace``) lets the kernels split skewed experts
+    over many CUs; without it the result is the same, only slower."""
     n_cap, d = x_perm.shape
     G, F2, _ = dw_gate_up.shape
     F = F2 // 2
     S = slot_gidx.shape[0]
     if dw_gate_up.dtype != torch.float32 or dw_down.dtype != torch.float32:
         raise TypeError("weight gradients are fp32")
+    wsp, wsn = (None, 0) if ws is None else (_ptr(ws), ws.numel())
     check(_lib.load().foremoe_grouped_ffn_wgrad(_ptr(x_perm), _ptr(h), _ptr(dy_perm), _ptr(d_au), _dt(x_perm),
                                                 d, F, S, _ptr(slot_offset), _ptr(slot_gidx), G, n_cap,
-                                                _ptr(dw_gate_up), _ptr(dw_down), _stream(x_perm.device)),
+                                                _ptr(dw_gate_up), _ptr(dw_down), wsp, wsn, _stream(x_perm.device)),
           "foremoe_grouped_ffn_wgrad")
 
 

@@ -2,16 +2,20 @@
 // input gradient and weight gradient.
 //
 // bf16 path: persistent workgroups of 4 wavefronts walk a tile list built on
-// the device from the slot offsets (no host sync), stage 64-deep K slices of
-// both operands through double-buffered LDS, and multiply with
-// v_mfma_f32_32x32x16_bf16 (fp32 accumulation). The SwiGLU activation and
-// its derivative are fused into the epilogues. Operands that are contiguous
-// along M/N (the weight-gradient operands and the transposed weights of the
-// input gradient) are transposed 8x8 in registers on their way to LDS, so
-// LDS always holds K-contiguous rows for the MFMA reads.
+// the device from the slot offsets (no host sync). Operand tiles stream from
+// HBM straight into LDS with range-checked buffer loads (buffer_load ... lds:
+// no staging registers; rows outside the current slot read as zero and no
+// load can leave its operand) through a ring of LDS stages, and are
+// multiplied with v_mfma_f32_32x32x16_bf16 (fp32 accumulation). Operands
+// that are contiguous along K are read with ds_read_b128; operands contiguous
+// along M/N (the weights in dgrad, both operands of wgrad) stay in their
+// memory layout in LDS and are read with the gfx950 transpose read
+// ds_read_b64_tr_b16. The SwiGLU activation and its derivative are fused into
+// the epilogues.
 //
 // f32 path: plain per-element kernels (small shapes only; no MFMA).
 #include <climits>
+#include <type_traits>
 
 #include "common.h"
 
@@ -20,14 +24,19 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int kThreads = 256;
-constexpr int kBK = 64;
-constexpr int kStr = kBK + 8;  // LDS row stride in elements (144 bytes: conflict-free MFMA reads)
 
-enum Epi { kEpiStore = 0, kEpiSwigluFwd = 1, kEpiSwigluBwd = 2, kEpiAccF32 = 3 };
+enum Epi { kEpiStore = 0, kEpiSwigluFwd = 1, kEpiSwigluBwd = 2 };
 
 __device__ __forceinline__ float silu_f(float a) { return a / (1.0f + __expf(-a)); }
+
+__device__ __forceinline__ int lane64() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 // Virtual workgroup id: workgroups are dispatched round-robin over the 8 XCDs,
 // so give the workgroups of one XCD consecutive ids (they then share tiles
@@ -61,77 +70,127 @@ __device__ int scan256(int v, int* s_tmp, int& total) {
 }
 
 // ---------------------------------------------------------------------------
-// Tile loaders (global -> registers -> LDS)
+// Range-checked buffer loads straight into LDS
 // ---------------------------------------------------------------------------
-// ROWS x 64 tile whose rows are K-contiguous in global memory. Thread t moves
-// 16 bytes of row (t / 8 + 32 p), column (t % 8) * 8, for p < ROWS / 32.
-template <int ROWS>
-struct KcLoader {
-  static constexpr int NP = ROWS / 32;
-  const uint16_t* ptr[NP];
-  uint4 v[NP];
-  __device__ __forceinline__ int row(int p) const { return p * 32 + (threadIdx.x >> 3); }
-  __device__ __forceinline__ int col() const { return (threadIdx.x & 7) * 8; }
-  __device__ __forceinline__ void load(int k0) {
-#pragma unroll
-    for (int p = 0; p < NP; ++p) v[p] = *reinterpret_cast<const uint4*>(ptr[p] + k0 + col());
+// A buffer resource over [base, base + bytes): a load at an offset >= bytes
+// returns zeros, so ragged tile edges read as zero and no load can leave the
+// operand.
+__device__ __forceinline__ i32x4 buf_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  i32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xFFFFu));
+  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+  r.w = 0x00020000;
+  return r;
+}
+
+// One wavefront moves 64 x 16 bytes: lane l's bytes land at LDS address
+// lds_wave_base + 16 l. The load is issued asynchronously; completion is
+// awaited with wait_vm() before the workgroup barrier that publishes it.
+__device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_wave_base, uint32_t voff) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_wave_base);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m0v), "v"(voff), "s"(rs)
+               : "memory");
+}
+
+// Wait until at most N vector-memory operations of this wavefront are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+
+// ---------------------------------------------------------------------------
+// LDS operand tiles. A "K-major" tile keeps ROWS rows (m or n) of BK
+// contiguous k values; a "MN-major" tile keeps BK rows (k) of ROWS contiguous
+// m or n values. Both are filled by dma16 and XOR-swizzled in 16-byte chunks
+// so that the MFMA fragment reads hit 16 (or 32) different LDS bank groups of
+// gfx950's 64 banks.
+// ---------------------------------------------------------------------------
+template <int ROWS, int BK>
+struct KTile {
+  static constexpr int CPR = BK / 8;     // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;   // rows per wavefront load
+  static constexpr int NI = ROWS / RPI;  // wavefront loads per tile
+  static constexpr int PER_WAVE = NI / 4;
+  static constexpr int BYTES = ROWS * BK * 2;
+  static_assert(NI % 4 == 0, "tile must split over 4 wavefronts");
+  __device__ __forceinline__ static int swz(int r) {
+    if constexpr (CPR == 8) return (r >> 1) & 7;
+    else return (r >> 2) & 3;
   }
-  __device__ __forceinline__ void store(uint16_t* s) const {
+  // rowoff(r): byte offset (in the buffer) of tile row r at k = 0; k0: first k.
+  template <class RowOff>
+  __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, RowOff rowoff, int k0) {
+    const int l = lane64(), w = wave_id();
 #pragma unroll
-    for (int p = 0; p < NP; ++p) *reinterpret_cast<uint4*>(s + row(p) * kStr + col()) = v[p];
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int q = w + 4 * i;
+      const int r = q * RPI + l / CPR;
+      const int c = (l % CPR) ^ swz(r);
+      dma16(rs, lds + q * 1024, rowoff(r) + (uint32_t)(k0 + c * 8) * 2u);
+    }
+  }
+  // MFMA operand for rows mn0..mn0+31 of the tile, k-step kk (16 k values):
+  // lane l gets row mn0 + l % 32, k = 16 kk + 8 (l / 32) + 0..7. The swizzle
+  // only depends on l % 32 (mn0 is a multiple of 32), so the address splits
+  // into a per-block lane offset and a per-k-step lane offset.
+  __device__ __forceinline__ static uint32_t lane_off(int mn0) {
+    return (uint32_t)(mn0 + (lane64() & 31)) * (BK * 2);
+  }
+  __device__ __forceinline__ static uint32_t kstep_off(int kk) {
+    const int l = lane64();
+    return (uint32_t)(((2 * kk + (l >> 5)) ^ swz(l & 31)) * 16);
+  }
+  __device__ __forceinline__ static bf16x8 frag(const char* lds, uint32_t off, const uint32_t* koff, int kk) {
+    return *reinterpret_cast<const bf16x8*>(lds + off + koff[kk]);
   }
 };
 
-// ROWS x 64 tile stored K-major in global memory: element (r, k) at
-// base + k * ld + r. Each thread loads 8x8 blocks (8 K rows of 8 contiguous
-// elements), transposes them in registers and writes 8 K-contiguous LDS rows.
-// K rows outside [lo, hi) read as zero.
-template <int ROWS>
-struct McLoader {
-  static constexpr int KB = kBK / 8;
-  static constexpr int NBLK = KB * (ROWS / 8);
-  static constexpr int PER = (NBLK + kThreads - 1) / kThreads;
-  uint4 v[PER][8];
-  __device__ __forceinline__ int blk(int b) const { return b * kThreads + threadIdx.x; }
-  __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int k0, int lo, int hi) {
+template <int ROWS, int BK>
+struct MTile {
+  static constexpr int RB = ROWS * 2;    // bytes per k row
+  static constexpr int KPI = 1024 / RB;  // k rows per wavefront load
+  static constexpr int NI = BK / KPI;
+  static constexpr int PER_WAVE = NI / 4;
+  static constexpr int BYTES = ROWS * BK * 2;
+  static_assert(NI % 4 == 0 && KPI >= 1, "tile must split over 4 wavefronts");
+  __device__ __forceinline__ static int swz(int k) { return 4 * (k & 3); }
+  // koff(k): byte offset of tile k-row k at the tile's first m/n.
+  template <class KOff>
+  __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, KOff koff) {
+    const int l = lane64(), w = wave_id();
 #pragma unroll
-    for (int b = 0; b < PER; ++b) {
-      const int id = blk(b);
-      if (NBLK % kThreads != 0 && id >= NBLK) continue;
-      const int kb = id % KB, mb = id / KB;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int k = k0 + kb * 8 + r;
-        if (k >= lo && k < hi)
-          v[b][r] = *reinterpret_cast<const uint4*>(base + (int64_t)k * ld + mb * 8);
-        else
-          v[b][r] = make_uint4(0, 0, 0, 0);
-      }
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int q = w + 4 * i;
+      const int k = q * KPI + (l * 16) / RB;
+      const int c = ((l * 16) % RB) / 16 ^ swz(k);
+      dma16(rs, lds + q * 1024, koff(k) + (uint32_t)c * 16u);
     }
   }
-  __device__ __forceinline__ void store(uint16_t* s) const {
+  // Same operand layout as KTile::frag, assembled from two transpose reads:
+  // in each 16-lane group g, lane i addresses 4 consecutive m/n of one k row
+  // and lane j receives one m/n at 4 consecutive k. The k row's low two bits
+  // (which pick the swizzle) come from the lane alone, so the address is a
+  // per-block lane offset plus an immediate (16 kk + 4 h) * RB.
+  __device__ __forceinline__ static uint32_t lane_off(int mn0) {
+    const int l = lane64();
+    const int g = l >> 4, j = l & 15;
+    const int krow = 8 * (g >> 1) + (j >> 2);
+    const int mn = mn0 + 16 * (g & 1) + 4 * (j & 3);
+    return (uint32_t)(krow * RB + (((mn >> 3) ^ swz(krow)) << 4) + (mn & 7) * 2);
+  }
+  __device__ __forceinline__ static uint32_t kstep_off(int) { return 0; }
+  __device__ __forceinline__ static bf16x8 frag(const char* lds, uint32_t off, const uint32_t*, int kk) {
+    s16x4 v[2];
 #pragma unroll
-    for (int b = 0; b < PER; ++b) {
-      const int id = blk(b);
-      if (NBLK % kThreads != 0 && id >= NBLK) continue;
-      const int kb = id % KB, mb = id / KB;
-      uint32_t w[8][4];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        w[r][0] = v[b][r].x;
-        w[r][1] = v[b][r].y;
-        w[r][2] = v[b][r].z;
-        w[r][3] = v[b][r].w;
-      }
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
-        uint32_t o[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_perm(w[2 * i + 1][c >> 1], w[2 * i][c >> 1], sel);
-        *reinterpret_cast<uint4*>(s + (mb * 8 + c) * kStr + kb * 8) = make_uint4(o[0], o[1], o[2], o[3]);
-      }
-    }
+    for (int h = 0; h < 2; ++h)
+      v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds + off + (kk * 16 + 4 * h) * RB));
+    const s16x8 t = __builtin_shufflevector(v[0], v[1], 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, t);
   }
 };
 
@@ -140,7 +199,7 @@ struct McLoader {
 // output as 32x32 blocks. The MFMA is fed the B rows as its first operand,
 // so each lane ends up with 4 consecutive output columns of one output row:
 // block (i, j), register q of lane l holds row  wm*BM/2 + 32 i + l % 32  and
-// column  col(j) + 8 (q / 4) + 4 (l / 32) + q % 4.
+// column  bcol(j) + 8 (q / 4) + 4 (l / 32) + q % 4.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, bool SWIGLU_COLS>
 struct Core {
@@ -169,18 +228,33 @@ struct Core {
         for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
   }
 
-  __device__ __forceinline__ void compute(const uint16_t* As, const uint16_t* Bs, int wm, int wn) {
-    const int lane = threadIdx.x & 63;
-    const int l32 = lane & 31, hi8 = (lane >> 5) * 8;
+  // Per-lane LDS offsets of every 32-row block this wave reads (fixed for
+  // the whole kernel) and of every k-step.
+  template <class AT, class BT, int BK>
+  struct Offsets {
+    uint32_t a[MB], b[NB], ka[BK / 16], kb[BK / 16];
+    __device__ __forceinline__ Offsets(int wm, int wn) {
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
+      for (int i = 0; i < MB; ++i) a[i] = AT::lane_off(wm * WM + i * 32);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) b[j] = BT::lane_off(bcol(wn, j));
+#pragma unroll
+      for (int kk = 0; kk < BK / 16; ++kk) {
+        ka[kk] = AT::kstep_off(kk);
+        kb[kk] = BT::kstep_off(kk);
+      }
+    }
+  };
+
+  template <class AT, class BT, int BK>
+  __device__ __forceinline__ void compute(const char* As, const char* Bs, const Offsets<AT, BT, BK>& o) {
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
       bf16x8 af[MB], bfr[NB];
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * WM + i * 32 + l32) * kStr + kk * 16 + hi8);
+      for (int i = 0; i < MB; ++i) af[i] = AT::frag(As, o.a[i], o.ka, kk);
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(Bs + (bcol(wn, j) + l32) * kStr + kk * 16 + hi8);
+      for (int j = 0; j < NB; ++j) bfr[j] = BT::frag(Bs, o.b[j], o.kb, kk);
 #pragma unroll
       for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -189,6 +263,26 @@ struct Core {
     }
   }
 };
+
+// Wait for the loads of the stage about to be computed: `ahead` younger
+// stages (of `per` loads each) may stay in flight.
+template <int NS, int PER>
+__device__ __forceinline__ void wait_stage(int ahead) {
+  static_assert(NS >= 2 && NS <= 4, "stages");
+  if constexpr (NS >= 4) {
+    if (ahead >= 2) {
+      wait_vm<2 * PER>();
+      return;
+    }
+  }
+  if constexpr (NS >= 3) {
+    if (ahead >= 1) {
+      wait_vm<PER>();
+      return;
+    }
+  }
+  wait_vm<0>();
+}
 
 // ---------------------------------------------------------------------------
 // Row-grouped GEMM: for each slot j, rows [off_j, off_{j+1}) (clamped to
@@ -238,24 +332,27 @@ __device__ void build_slot_tiles(const int32_t* __restrict__ off, int S, int64_t
   __syncthreads();
 }
 
-template <int BM, int BN, bool B_KCONTIG, int EPI>
+template <int BM, int BN, int BK, int NS, bool B_KMAJ, int EPI>
 __global__ __launch_bounds__(kThreads) void gemm_rows_kernel(RowsArgs a) {
   constexpr bool SW = (EPI == kEpiSwigluFwd);
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][(BM + BN) * kStr];
+  using AT = KTile<BM, BK>;
+  using BT = typename std::conditional<B_KMAJ, KTile<BN, BK>, MTile<BN, BK>>::type;
+  constexpr int STAGE = AT::BYTES + BT::BYTES;
+  constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
+  __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
   __shared__ int s_mt[FOREMOE_MAX_SLOTS + 1];
   __shared__ int s_tmp[4];
 
   build_slot_tiles<BM>(a.slot_offset, a.S, a.n_cap, s_mt, s_tmp);
   const int n_tiles = a.N / BN;
   const int total = s_mt[a.S] * n_tiles;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = lane64(), wave = wave_id();
   const int wm = wave >> 1, wn = wave & 1;
-  const int KT = a.K / kBK;
+  const int KT = a.K / BK;
+  const uint32_t lds0 = lds_addr(lds);
 
   Core<BM, BN, SW> core;
-  KcLoader<BM> la;
-  KcLoader<BN> lbk;
-  McLoader<BN> lbm;
+  const typename Core<BM, BN, SW>::template Offsets<AT, BT, BK> offs(wm, wn);
 
   for (int t = xcd_virtual_id(); t < total; t += gridDim.x) {
     const int mtg = t / n_tiles, nt = t % n_tiles;
@@ -265,59 +362,55 @@ __global__ __launch_bounds__(kThreads) void gemm_rows_kernel(RowsArgs a) {
       if (s_mt[mid] <= mtg) lo = mid;
       else hi = mid - 1;
     }
-    const int j = lo;
+    const int j = __builtin_amdgcn_readfirstlane(lo);
     int64_t rbeg = a.slot_offset[j], rend = a.slot_offset[j + 1];
     rbeg = rbeg < 0 ? 0 : (rbeg > a.n_cap ? a.n_cap : rbeg);
     rend = rend < 0 ? 0 : (rend > a.n_cap ? a.n_cap : rend);
-    const int64_t m0 = rbeg + (int64_t)(mtg - s_mt[j]) * BM;
+    const int mrel = (mtg - s_mt[j]) * BM;  // first tile row relative to the slot
+    const int64_t m0 = rbeg + mrel;
     const int w = a.slot_widx[j];
     if (w < 0 || w >= a.W) continue;  // invalid weight index: rows left unwritten
-    const uint16_t* Bw = a.B + (int64_t)w * a.wstride;
     const int n0 = nt * BN;           // first output column of the tile grid
     const int f0 = nt * (BN / 2);     // SwiGLU: first H column
 
-#pragma unroll
-    for (int p = 0; p < KcLoader<BM>::NP; ++p) {
-      int64_t r = m0 + la.row(p);
-      if (r >= rend) r = rend - 1;  // clamp the ragged tail to a valid row
-      la.ptr[p] = a.A + r * a.lda;
-    }
-    if constexpr (B_KCONTIG) {
-#pragma unroll
-      for (int p = 0; p < KcLoader<BN>::NP; ++p) {
-        const int r = lbk.row(p);
-        int64_t wr;
-        if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
-        else wr = n0 + r;
-        lbk.ptr[p] = Bw + wr * a.ldb;
+    // operand A: the slot's rows only (rows past the slot read as zero)
+    const i32x4 rsa = buf_rsrc(a.A + rbeg * a.lda, (uint32_t)((rend - rbeg) * a.lda * 2));
+    const uint32_t lda2 = (uint32_t)(a.lda * 2);
+    auto arow = [&](int r) -> uint32_t { return (uint32_t)(mrel + r) * lda2; };
+    // operand B: weight matrix w
+    const i32x4 rsb = buf_rsrc(a.B + (int64_t)w * a.wstride, (uint32_t)(a.wstride * 2));
+    const uint32_t ldb2 = (uint32_t)(a.ldb * 2);
+    auto brow = [&](int r) -> uint32_t {
+      int wr;
+      if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
+      else wr = n0 + r;
+      return (uint32_t)wr * ldb2;
+    };
+    auto issue = [&](int kt) {
+      const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
+      AT::issue(rsa, sa, arow, kt * BK);
+      if constexpr (B_KMAJ) {
+        BT::issue(rsb, sa + AT::BYTES, brow, kt * BK);
+      } else {
+        // K-major weights: element (n, k) at (k * ldb + n) * 2
+        BT::issue(rsb, sa + AT::BYTES,
+                  [&](int k) -> uint32_t { return (uint32_t)(kt * BK + k) * ldb2 + (uint32_t)n0 * 2u; });
       }
-    }
-    const uint16_t* Bkn = Bw + n0;  // K-major weights: element (n, k) at Bkn + k * ldb + n
+    };
 
     core.zero();
-    la.load(0);
-    if constexpr (B_KCONTIG) lbk.load(0);
-    else lbm.load(Bkn, a.ldb, 0, 0, a.K);
-    la.store(lds[0]);
-    if constexpr (B_KCONTIG) lbk.store(lds[0] + BM * kStr);
-    else lbm.store(lds[0] + BM * kStr);
-    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < KT) issue(s);
     for (int kt = 0; kt < KT; ++kt) {
-      const int cur = kt & 1;
-      const bool more = kt + 1 < KT;
-      if (more) {
-        la.load((kt + 1) * kBK);
-        if constexpr (B_KCONTIG) lbk.load((kt + 1) * kBK);
-        else lbm.load(Bkn, a.ldb, (kt + 1) * kBK, 0, a.K);
-      }
-      core.compute(lds[cur], lds[cur] + BM * kStr, wm, wn);
-      if (more) {
-        la.store(lds[cur ^ 1]);
-        if constexpr (B_KCONTIG) lbk.store(lds[cur ^ 1] + BM * kStr);
-        else lbm.store(lds[cur ^ 1] + BM * kStr);
-      }
+      const int ahead = (kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1) - kt;
+      wait_stage<NS, PER>(ahead);
       __syncthreads();
+      if (kt + NS - 1 < KT) issue(kt + NS - 1);
+      const char* st = lds + (kt % NS) * STAGE;
+      core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
     }
+    __syncthreads();  // all reads of this tile's stages done before the next tile's loads
 
     // ---------------- epilogue ----------------
     const int l32 = lane & 31, c4 = (lane >> 5) * 4;
@@ -385,8 +478,15 @@ __global__ __launch_bounds__(kThreads) void gemm_rows_kernel(RowsArgs a) {
 
 // ---------------------------------------------------------------------------
 // Weight gradient: dW[g] (M x N, fp32) += sum over the rows of every slot
-// with gradient index g of A[row, :]^T B[row, :]. Groups are visited in
-// descending row count so that the long reductions start first.
+// with gradient index g of A[row, :]^T B[row, :].
+//
+// Work split: the row sequence of a group (the concatenated row ranges of
+// its slots, in slot order) is cut into chunks of CH rows when the caller's
+// workspace allows, so that one hot expert spreads over many CUs. Chunk 0 of
+// a group adds its result straight into dW; chunks 1.. write fp32 partial
+// tiles to the workspace, and wgrad_reduce_kernel (launched next on the same
+// stream) adds them in chunk order. Every output element therefore has one
+// fixed summation order: deterministic, no atomics on floats.
 // ---------------------------------------------------------------------------
 struct WgradArgs {
   const uint16_t* A;  // [n_cap, M]
@@ -401,117 +501,278 @@ struct WgradArgs {
   float* C;  // dW[g] at C + g * gstride, row-major [M, N]
   int64_t ldc;
   int64_t gstride;
+  float* part;  // partial tiles [p_max][BM * BN]
+  int p_max;
 };
 
-template <int BM, int BN>
-__global__ __launch_bounds__(kThreads) void gemm_wgrad_kernel(WgradArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][(BM + BN) * kStr];
-  __shared__ int s_off[FOREMOE_MAX_SLOTS + 1];
-  __shared__ int s_gidx[FOREMOE_MAX_SLOTS];
-  __shared__ int s_rows[FOREMOE_MAX_SLOTS];
-  __shared__ int s_order[FOREMOE_MAX_SLOTS];
-  __shared__ int s_nne;
+struct WgradPlan {
+  int off[FOREMOE_MAX_SLOTS + 1];   // clamped slot offsets
+  int gidx[FOREMOE_MAX_SLOTS];      // gradient index, -1 for empty/invalid slots
+  int rows[FOREMOE_MAX_SLOTS];      // rows per group
+  int order[FOREMOE_MAX_SLOTS];     // groups by descending rows
+  int ibase[FOREMOE_MAX_SLOTS + 1]; // work-item prefix over ordered groups
+  int pbase[FOREMOE_MAX_SLOTS + 1]; // partial-tile prefix over ordered groups
+  int nne;                          // non-empty groups
+  int ch;                           // chunk rows (INT_MAX: no split)
+};
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+template <int BM, int BN, int BK>
+__device__ void build_wgrad_plan(const WgradArgs& a, WgradPlan& P) {
+  const int tid = threadIdx.x;
   const int S = a.S, G = a.G;
-  if (tid == 0) s_nne = 0;
-  for (int g = tid; g < G; g += kThreads) s_rows[g] = 0;
+  const int tpg = (a.M / BM) * (a.N / BN);
+  if (tid == 0) P.nne = 0;
+  for (int g = tid; g < G; g += kThreads) P.rows[g] = 0;
   for (int j = tid; j <= S; j += kThreads) {
-    int64_t o = a.slot_offset[j];
-    s_off[j] = (int)(o < 0 ? 0 : (o > a.n_cap ? a.n_cap : o));
-    if (j < S) {
-      const int g = a.slot_gidx[j];
-      s_gidx[j] = (g >= 0 && g < G) ? g : -1;
-    }
+    const int64_t o = a.slot_offset[j];
+    P.off[j] = (int)(o < 0 ? 0 : (o > a.n_cap ? a.n_cap : o));
   }
   __syncthreads();
   for (int j = tid; j < S; j += kThreads) {
-    const int n = s_off[j + 1] - s_off[j];
-    if (n <= 0) s_gidx[j] = -1;  // empty (or inverted) ranges contribute nothing
-    else if (s_gidx[j] >= 0) atomicAdd(&s_rows[s_gidx[j]], n);
+    const int g = a.slot_gidx[j];
+    const int n = P.off[j + 1] - P.off[j];
+    P.gidx[j] = (g >= 0 && g < G && n > 0) ? g : -1;
+    if (P.gidx[j] >= 0) atomicAdd(&P.rows[g], n);
   }
   __syncthreads();
   for (int g = tid; g < G; g += kThreads) {
-    const int rg = s_rows[g];
+    const int rg = P.rows[g];
     if (rg <= 0) continue;
     int rank = 0;
     for (int h = 0; h < G; ++h) {
-      const int rh = s_rows[h];
+      const int rh = P.rows[h];
       rank += (rh > rg) || (rh == rg && h < g);
     }
-    s_order[rank] = g;
-    atomicAdd(&s_nne, 1);
+    P.order[rank] = g;
+    atomicAdd(&P.nne, 1);
   }
   __syncthreads();
+  if (tid == 0) {
+    long long total = 0;
+    for (int i = 0; i < P.nne; ++i) total += P.rows[P.order[i]];
+    int ch = INT_MAX;
+    if (a.p_max > 0 && total > 0) {
+      long long c = (total * tpg + a.p_max - 1) / a.p_max;
+      c = (c + BK - 1) / BK * BK;
+      if (c < BK) c = BK;
+      ch = c > INT_MAX ? INT_MAX : (int)c;
+    }
+    P.ch = ch;
+    int ib = 0, pb = 0;
+    for (int i = 0; i < P.nne; ++i) {
+      const int rg = P.rows[P.order[i]];
+      const int cg = ch == INT_MAX ? 1 : (rg + ch - 1) / ch;
+      P.ibase[i] = ib;
+      P.pbase[i] = pb;
+      ib += cg * tpg;
+      pb += (cg - 1) * tpg;
+    }
+    P.ibase[P.nne] = ib;
+    P.pbase[P.nne] = pb;
+  }
+  __syncthreads();
+}
 
+// Walks the k-tiles of one chunk [s0, s1) of a group's row sequence: each
+// k-tile lies inside one slot's row range [lo, hi).
+struct KCursor {
+  int j, pos, lo, hi, k;  // slot, sequence position of slot start, segment rows, tile start
+  bool done;
+};
+
+__device__ __forceinline__ void cursor_next_slot(const WgradPlan& P, int S, int g, int s1, KCursor& c) {
+  int j = c.j, pos = c.pos;
+  for (;;) {
+    if (j >= 0 && P.gidx[j] == g) pos += P.off[j + 1] - P.off[j];
+    ++j;
+    if (j >= S || pos >= s1) {
+      c.done = true;
+      return;
+    }
+    if (P.gidx[j] == g) break;
+  }
+  c.j = j;
+  c.pos = pos;
+  c.lo = P.off[j];
+  const int n = P.off[j + 1] - P.off[j];
+  c.hi = P.off[j] + (n < s1 - pos ? n : s1 - pos);
+  c.k = c.lo;
+}
+
+__device__ __forceinline__ KCursor cursor_begin(const WgradPlan& P, int S, int g, int s0, int s1) {
+  KCursor c;
+  c.done = false;
+  int pos = 0;
+  for (int j = 0; j < S; ++j) {
+    if (P.gidx[j] != g) continue;
+    const int n = P.off[j + 1] - P.off[j];
+    if (pos + n > s0) {
+      c.j = j;
+      c.pos = pos;
+      c.lo = P.off[j] + (s0 - pos);
+      c.hi = P.off[j] + (n < s1 - pos ? n : s1 - pos);
+      c.k = c.lo;
+      return c;
+    }
+    pos += n;
+  }
+  c.done = true;
+  return c;
+}
+
+template <int BK>
+__device__ __forceinline__ void cursor_advance(const WgradPlan& P, int S, int g, int s1, KCursor& c) {
+  c.k += BK;
+  if (c.k >= c.hi) cursor_next_slot(P, S, g, s1, c);
+}
+
+template <int BM, int BN, int BK, int NS>
+__global__ __launch_bounds__(kThreads) void gemm_wgrad_kernel(WgradArgs a) {
+  using AT = MTile<BM, BK>;
+  using BT = MTile<BN, BK>;
+  constexpr int STAGE = AT::BYTES + BT::BYTES;
+  constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
+  __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
+  __shared__ WgradPlan P;
+
+  build_wgrad_plan<BM, BN, BK>(a, P);
+  const int S = a.S;
   const int mt_n = a.M / BM, nt_n = a.N / BN, tpg = mt_n * nt_n;
-  const int total = s_nne * tpg;
+  const int total = P.ibase[P.nne];
+  const int lane = lane64(), wave = wave_id();
+  const int wm = wave >> 1, wn = wave & 1;
+  const uint32_t lds0 = lds_addr(lds);
+  const uint32_t lda2 = (uint32_t)(a.lda * 2), ldb2 = (uint32_t)(a.ldb * 2);
   Core<BM, BN, false> core;
-  McLoader<BM> la;
-  McLoader<BN> lb;
+  const typename Core<BM, BN, false>::template Offsets<AT, BT, BK> offs(wm, wn);
 
   for (int t = xcd_virtual_id(); t < total; t += gridDim.x) {
-    const int g = s_order[t / tpg];
-    const int tt = t % tpg;
-    const int m0 = (tt / nt_n) * BM, n0 = (tt % nt_n) * BN;
-    const uint16_t* Ab = a.A + m0;
-    const uint16_t* Bb = a.B + n0;
+    int lo = 0, hi = P.nne - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (P.ibase[mid] <= t) lo = mid;
+      else hi = mid - 1;
+    }
+    const int gi = __builtin_amdgcn_readfirstlane(lo);
+    const int g = P.order[gi];
+    const int local = t - P.ibase[gi];
+    const int c = local / tpg, tile = local % tpg;
+    const int m0 = (tile / nt_n) * BM, n0 = (tile % nt_n) * BN;
+    const int rg = P.rows[g];
+    const int s0 = P.ch == INT_MAX ? 0 : c * P.ch;
+    const int s1 = P.ch == INT_MAX ? rg : (s0 + P.ch < rg ? s0 + P.ch : rg);
 
-    int j = 0;
-    while (j < S && !(s_gidx[j] == g && s_off[j + 1] > s_off[j])) ++j;
-    int k0 = s_off[j];
+    KCursor ic = cursor_begin(P, S, g, s0, s1);
+    auto issue = [&](int slot_stage, const KCursor& cur) {
+      const uint32_t sa = lds0 + (uint32_t)(slot_stage * STAGE);
+      // the segment's rows [lo, hi): rows past hi read as zero
+      const i32x4 rsa = buf_rsrc(a.A + (int64_t)cur.lo * a.lda, (uint32_t)(cur.hi - cur.lo) * lda2);
+      const i32x4 rsb = buf_rsrc(a.B + (int64_t)cur.lo * a.ldb, (uint32_t)(cur.hi - cur.lo) * ldb2);
+      const int kr = cur.k - cur.lo;
+      AT::issue(rsa, sa, [&](int k) -> uint32_t { return (uint32_t)(kr + k) * lda2 + (uint32_t)m0 * 2u; });
+      BT::issue(rsb, sa + AT::BYTES,
+                [&](int k) -> uint32_t { return (uint32_t)(kr + k) * ldb2 + (uint32_t)n0 * 2u; });
+    };
 
     core.zero();
-    la.load(Ab, a.lda, k0, s_off[j], s_off[j + 1]);
-    lb.load(Bb, a.ldb, k0, s_off[j], s_off[j + 1]);
-    la.store(lds[0]);
-    lb.store(lds[0] + BM * kStr);
-    __syncthreads();
-    int cur = 0;
-    while (true) {
-      int j2 = j, k2 = k0 + kBK;
-      if (k2 >= s_off[j + 1]) {
-        ++j2;
-        while (j2 < S && !(s_gidx[j2] == g && s_off[j2 + 1] > s_off[j2])) ++j2;
-        k2 = j2 < S ? s_off[j2] : 0;
+    int issued = 0;
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) {
+      if (!ic.done) {
+        issue(issued % NS, ic);
+        cursor_advance<BK>(P, S, g, s1, ic);
+        ++issued;
       }
-      const bool more = j2 < S;
-      if (more) {
-        la.load(Ab, a.lda, k2, s_off[j2], s_off[j2 + 1]);
-        lb.load(Bb, a.ldb, k2, s_off[j2], s_off[j2 + 1]);
-      }
-      core.compute(lds[cur], lds[cur] + BM * kStr, wm, wn);
-      if (more) {
-        la.store(lds[cur ^ 1]);
-        lb.store(lds[cur ^ 1] + BM * kStr);
-      }
-      __syncthreads();
-      if (!more) break;
-      cur ^= 1;
-      j = j2;
-      k0 = k2;
     }
+    for (int kt = 0; kt < issued; ++kt) {
+      wait_stage<NS, PER>(issued - 1 - kt);
+      __syncthreads();
+      if (!ic.done) {
+        issue(issued % NS, ic);
+        cursor_advance<BK>(P, S, g, s1, ic);
+        ++issued;
+      }
+      const char* st = lds + (kt % NS) * STAGE;
+      core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
+    }
+    __syncthreads();
 
-    float* Cg = a.C + (int64_t)g * a.gstride;
     const int l32 = lane & 31, c4 = (lane >> 5) * 4;
+    if (c == 0) {
+      float* Cg = a.C + (int64_t)g * a.gstride;
 #pragma unroll
-    for (int i = 0; i < Core<BM, BN, false>::MB; ++i) {
-      const int64_t m = m0 + wm * (BM / 2) + i * 32 + l32;
+      for (int i = 0; i < Core<BM, BN, false>::MB; ++i) {
+        const int64_t m = m0 + wm * (BM / 2) + i * 32 + l32;
 #pragma unroll
-      for (int jj = 0; jj < Core<BM, BN, false>::NB; ++jj) {
+        for (int jj = 0; jj < Core<BM, BN, false>::NB; ++jj) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int n = n0 + wn * (BN / 2) + jj * 32 + q * 8 + c4;
-          float4* p = reinterpret_cast<float4*>(Cg + m * a.ldc + n);
-          float4 o = *p;
-          o.x += core.acc[i][jj][q * 4 + 0];
-          o.y += core.acc[i][jj][q * 4 + 1];
-          o.z += core.acc[i][jj][q * 4 + 2];
-          o.w += core.acc[i][jj][q * 4 + 3];
-          *p = o;
+          for (int q = 0; q < 4; ++q) {
+            const int n = n0 + wn * (BN / 2) + jj * 32 + q * 8 + c4;
+            float4* p = reinterpret_cast<float4*>(Cg + m * a.ldc + n);
+            float4 o = *p;
+            o.x += core.acc[i][jj][q * 4 + 0];
+            o.y += core.acc[i][jj][q * 4 + 1];
+            o.z += core.acc[i][jj][q * 4 + 2];
+            o.w += core.acc[i][jj][q * 4 + 3];
+            *p = o;
+          }
         }
       }
+    } else {
+      float* Pt = a.part + (int64_t)(P.pbase[gi] + (c - 1) * tpg + tile) * (BM * BN);
+#pragma unroll
+      for (int i = 0; i < Core<BM, BN, false>::MB; ++i) {
+        const int m = wm * (BM / 2) + i * 32 + l32;
+#pragma unroll
+        for (int jj = 0; jj < Core<BM, BN, false>::NB; ++jj) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int n = wn * (BN / 2) + jj * 32 + q * 8 + c4;
+            *reinterpret_cast<float4*>(Pt + m * BN + n) =
+                make_float4(core.acc[i][jj][q * 4 + 0], core.acc[i][jj][q * 4 + 1], core.acc[i][jj][q * 4 + 2],
+                            core.acc[i][jj][q * 4 + 3]);
+          }
+        }
+      }
+    }
+  }
+}
+
+// dW[g] tile += partials of chunks 1.. in chunk order (one workgroup per tile).
+template <int BM, int BN, int BK>
+__global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(WgradArgs a) {
+  __shared__ WgradPlan P;
+  build_wgrad_plan<BM, BN, BK>(a, P);
+  if (P.ch == INT_MAX) return;
+  const int mt_n = a.M / BM, nt_n = a.N / BN, tpg = mt_n * nt_n;
+  // split groups come first in the ordering (largest rows), so walk until C_g == 1
+  int nsplit = 0;
+  while (nsplit < P.nne && (P.rows[P.order[nsplit]] + P.ch - 1) / P.ch > 1) ++nsplit;
+  const int total = nsplit * tpg;
+  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+    const int gi = t / tpg, tile = t % tpg;
+    const int g = P.order[gi];
+    const int cg = (P.rows[g] + P.ch - 1) / P.ch;
+    const int m0 = (tile / nt_n) * BM, n0 = (tile % nt_n) * BN;
+    float* Cg = a.C + (int64_t)g * a.gstride;
+    const float* P0 = a.part + (int64_t)(P.pbase[gi] + tile) * (BM * BN);
+    for (int e = threadIdx.x * 4; e < BM * BN; e += kThreads * 4) {
+      float4 s = *reinterpret_cast<const float4*>(P0 + e);
+      for (int c = 2; c < cg; ++c) {
+        const float4 v = *reinterpret_cast<const float4*>(P0 + (int64_t)(c - 1) * tpg * (BM * BN) + e);
+        s.x += v.x;
+        s.y += v.y;
+        s.z += v.z;
+        s.w += v.w;
+      }
+      const int m = m0 + e / BN, n = n0 + e % BN;
+      float4* p = reinterpret_cast<float4*>(Cg + (int64_t)m * a.ldc + n);
+      float4 o = *p;
+      o.x += s.x;
+      o.y += s.y;
+      o.z += s.z;
+      o.w += s.w;
+      *p = o;
     }
   }
 }
@@ -612,10 +873,18 @@ __global__ __launch_bounds__(256) void f32_wgrad_kernel(const float* __restrict_
 // ---------------------------------------------------------------------------
 int persistent_grid() { return num_cus(); }
 
-template <int BN, bool KC, int EPI>
+// Row-grouped launches: 256-row tiles; 256-wide output tiles with 2 LDS
+// stages of 64-deep K slices (128 KiB), or 128-wide with 3 stages (144 KiB).
+template <int BN, bool KMAJ, int EPI>
 void launch_rows(const RowsArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_rows_kernel<256, BN, KC, EPI>), dim3(persistent_grid()), dim3(kThreads), 0, st, a);
+  constexpr int NS = BN == 256 ? 2 : 3;
+  hipLaunchKernelGGL((gemm_rows_kernel<256, BN, 64, NS, KMAJ, EPI>), dim3(persistent_grid()), dim3(kThreads), 0, st,
+                     a);
 }
+
+// Partial-tile budget of the weight-gradient split (tiles of 256 x 256 fp32).
+constexpr size_t kWgradPartialTiles = 256;
+constexpr size_t kWgradWorkspaceBytes = kWgradPartialTiles * 256 * 256 * 4;
 
 }  // namespace
 }  // namespace foremoe
@@ -636,6 +905,8 @@ static int check_ffn(const char* who, foremoe_dtype dtype, int32_t d, int32_t F,
   REQUIRE(slot_offset, "%s: slot_offset is NULL", who);
   if (dtype == FOREMOE_BF16 && (d % 128 != 0 || F % 128 != 0))
     return set_error(FOREMOE_EUNSUPPORTED, "%s: bf16 needs d %% 128 == 0 and F %% 128 == 0 (d=%d, F=%d)", who, d, F);
+  if (dtype == FOREMOE_BF16 && (n_cap + 256) * (int64_t)(d > 2 * F ? d : 2 * F) * 2 >= ((int64_t)1 << 31))
+    return set_error(FOREMOE_EUNSUPPORTED, "%s: n_cap * row bytes must stay below 2 GiB", who);
   return FOREMOE_OK;
 }
 
@@ -810,8 +1081,9 @@ int foremoe_grouped_ffn_dgrad(const void* dy_perm, const void* save_au, foremoe_
 
 static int wgrad_common(const char* who, const void* A, int lda, const void* B, int ldb, int M, int N,
                         foremoe_dtype dtype, int32_t S, const int32_t* slot_offset, const int32_t* slot_gidx, int32_t G,
-                        int64_t n_cap, float* dw, void* stream) {
+                        int64_t n_cap, float* dw, void* ws, size_t ws_bytes, void* stream) {
   REQUIRE(G >= 1 && G <= FOREMOE_MAX_SLOTS, "%s: G=%d out of range", who, G);
+  REQUIRE(ws || ws_bytes == 0, "%s: ws is NULL but ws_bytes > 0", who);
   if (S == 0 || n_cap == 0) return FOREMOE_OK;
   REQUIRE(A && B && slot_gidx && dw, "%s: NULL buffer", who);
   hipStream_t st = (hipStream_t)stream;
@@ -831,7 +1103,17 @@ static int wgrad_common(const char* who, const void* A, int lda, const void* B, 
     a.C = dw;
     a.ldc = N;
     a.gstride = (int64_t)M * N;
-    hipLaunchKernelGGL((gemm_wgrad_kernel<128, 128>), dim3(persistent_grid()), dim3(kThreads), 0, st, a);
+    a.part = (float*)ws;
+    const dim3 grid(persistent_grid()), block(kThreads);
+    if (M % 256 == 0 && N % 256 == 0) {
+      a.p_max = (int)(ws_bytes / (256 * 256 * 4));
+      hipLaunchKernelGGL((gemm_wgrad_kernel<256, 256, 64, 2>), grid, block, 0, st, a);
+      if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<256, 256, 64>), grid, block, 0, st, a);
+    } else {
+      a.p_max = (int)(ws_bytes / (128 * 128 * 4));
+      hipLaunchKernelGGL((gemm_wgrad_kernel<128, 128, 64, 3>), grid, block, 0, st, a);
+      if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<128, 128, 64>), grid, block, 0, st, a);
+    }
   } else {
     hipLaunchKernelGGL(f32_wgrad_kernel, dim3((N + 15) / 16, (M + 15) / 16, G), dim3(256), 0, st, (const float*)A, lda,
                        (const float*)B, ldb, M, N, slot_offset, slot_gidx, S, G, n_cap, dw);
@@ -839,32 +1121,38 @@ static int wgrad_common(const char* who, const void* A, int lda, const void* B, 
   return check_launch(who);
 }
 
+size_t foremoe_wgrad_workspace_size(int32_t d, int32_t F) {
+  if (d < 1 || F < 1) return 0;
+  return kWgradWorkspaceBytes;
+}
+
 int foremoe_ffn_gate_up_wgrad(const void* d_au, const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
                               int32_t S, const int32_t* slot_offset, const int32_t* slot_gidx, int32_t G,
-                              int64_t n_cap, float* dw_gate_up, void* stream) {
+                              int64_t n_cap, float* dw_gate_up, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_ffn("gate_up_wgrad", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
   return wgrad_common("foremoe_ffn_gate_up_wgrad", d_au, 2 * F, x_perm, d, 2 * F, d, dtype, S, slot_offset, slot_gidx,
-                      G, n_cap, dw_gate_up, stream);
+                      G, n_cap, dw_gate_up, ws, ws_bytes, stream);
 }
 
 int foremoe_ffn_down_wgrad(const void* dy_perm, const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                            const int32_t* slot_offset, const int32_t* slot_gidx, int32_t G, int64_t n_cap,
-                           float* dw_down, void* stream) {
+                           float* dw_down, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_ffn("down_wgrad", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
   return wgrad_common("foremoe_ffn_down_wgrad", dy_perm, d, h, F, d, F, dtype, S, slot_offset, slot_gidx, G, n_cap,
-                      dw_down, stream);
+                      dw_down, ws, ws_bytes, stream);
 }
 
 int foremoe_grouped_ffn_wgrad(const void* x_perm, const void* h, const void* dy_perm, const void* d_au,
                               foremoe_dtype dtype, int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
                               const int32_t* slot_gidx, int32_t G, int64_t n_cap, float* dw_gate_up, float* dw_down,
-                              void* stream) {
-  int rc = foremoe_ffn_gate_up_wgrad(d_au, x_perm, dtype, d, F, S, slot_offset, slot_gidx, G, n_cap, dw_gate_up,
-                                     stream);
+                              void* ws, size_t ws_bytes, void* stream) {
+  int rc = foremoe_ffn_gate_up_wgrad(d_au, x_perm, dtype, d, F, S, slot_offset, slot_gidx, G, n_cap, dw_gate_up, ws,
+                                     ws_bytes, stream);
   if (rc) return rc;
-  return foremoe_ffn_down_wgrad(dy_perm, h, dtype, d, F, S, slot_offset, slot_gidx, G, n_cap, dw_down, stream);
+  return foremoe_ffn_down_wgrad(dy_perm, h, dtype, d, F, S, slot_offset, slot_gidx, G, n_cap, dw_down, ws, ws_bytes,
+                                stream);
 }
 
 }  // extern "C"

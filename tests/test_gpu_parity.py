@@ -239,15 +239,18 @@ def test_ffn_backward(gpu, name):
     G = m.plan.G
     start_gu = rng.standard_normal((G, 2 * F, w.spec.d)).astype(np.float32)
     start_dn = rng.standard_normal((G, w.spec.d, F)).astype(np.float32)
-    dwgu = torch.from_numpy(start_gu.copy()).to(gpu)
-    dwdn = torch.from_numpy(start_dn.copy()).to(gpu)
-    api.grouped_ffn_wgrad(to_dev(x_perm, dt, gpu), to_dev(hq, dt, gpu), to_dev(dy_perm, dt, gpu),
-                          to_dev(dau_q, dt, gpu), so, gidx, dwgu, dwdn)
-    torch.cuda.synchronize()
     rgu, rdn = O.ffn_wgrad(x_perm, hq, dy_perm, dau_q[:, :F], dau_q[:, F:], ref["slot_offset"], m.plan.slot_gidx, G,
                            start_gu.astype(np.float64), start_dn.astype(np.float64))
-    check_close("dW_gate_up", to_np(dwgu), rgu)
-    check_close("dW_down", to_np(dwdn), rdn)
+    # without a workspace (one workgroup per output tile) and with the split over row chunks
+    for ws in (None, api.wgrad_workspace(w.spec.d, F, gpu)):
+        dwgu = torch.from_numpy(start_gu.copy()).to(gpu)
+        dwdn = torch.from_numpy(start_dn.copy()).to(gpu)
+        api.grouped_ffn_wgrad(to_dev(x_perm, dt, gpu), to_dev(hq, dt, gpu), to_dev(dy_perm, dt, gpu),
+                              to_dev(dau_q, dt, gpu), so, gidx, dwgu, dwdn, ws=ws)
+        torch.cuda.synchronize()
+        tag = "split" if ws is not None else "whole"
+        check_close(f"dW_gate_up[{tag}]", to_np(dwgu), rgu)
+        check_close(f"dW_down[{tag}]", to_np(dwdn), rdn)
 
 
 # ---------------------------------------------------------------------------
@@ -308,7 +311,8 @@ def run_gpu_layer(w, m, gpu, dy, dw_gate_up=None, dw_down=None):
     if dw_gate_up is None:
         dw_gate_up = torch.zeros((m.plan.G, 2 * w.spec.F, d), dtype=torch.float32, device=gpu)
         dw_down = torch.zeros((m.plan.G, d, w.spec.F), dtype=torch.float32, device=gpu)
-    api.grouped_ffn_wgrad(got["x_perm"], h, dyp, d_au, got["slot_offset"], gidx, dw_gate_up, dw_down)
+    api.grouped_ffn_wgrad(got["x_perm"], h, dyp, d_au, got["slot_offset"], gidx, dw_gate_up, dw_down,
+                          ws=api.wgrad_workspace(d, w.spec.F, gpu))
     dx = api.permute_bwd(dxp, got["pair_to_row"], T, K, out_dtype=torch.float32)
     return dict(y=y, dgates=dg, dx=dx, dw_gate_up=dw_gate_up, dw_down=dw_down)
 
