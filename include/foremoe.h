@@ -172,7 +172,7 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
  *            (needed by foremoe_grouped_ffn_dgrad)
  * All tensors are `dtype`. bf16 runs on bf16 MFMA with fp32 accumulation
  * and needs d % 128 == 0, F % 128 == 0 and (n_cap + 256) * max(d, 2F) * 2
- * below 2^31 (else FOREMOE_EUNSUPPORTED); f32 accepts any d, F >= 1.
+ * below 2^32 (else FOREMOE_EUNSUPPORTED); f32 accepts any d, F >= 1.
  * 0 <= S <= FOREMOE_MAX_SLOTS.
  * foremoe_grouped_ffn_fwd = foremoe_ffn_gate_up_fwd then foremoe_ffn_down_fwd;
  * each of these two is a single kernel launch.

@@ -29,7 +29,31 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kThreads = 256;
+// Tile configurations (overridable at build time for tuning sweeps).
+#ifndef FM_ROWS_BK
+#define FM_ROWS_BK 32
+#endif
+#ifndef FM_ROWS_NS
+#define FM_ROWS_NS 4
+#endif
+#ifndef FM_ROWS_WGM
+#define FM_ROWS_WGM 2
+#endif
+#ifndef FM_ROWS_WGN
+#define FM_ROWS_WGN 2
+#endif
+#ifndef FM_WG_BK
+#define FM_WG_BK 32
+#endif
+#ifndef FM_WG_NS
+#define FM_WG_NS 4
+#endif
+#ifndef FM_WG_WGM
+#define FM_WG_WGM 2
+#endif
+#ifndef FM_WG_WGN
+#define FM_WG_WGN 2
+#endif
 
 enum Epi { kEpiStore = 0, kEpiSwigluFwd = 1, kEpiSwigluBwd = 2 };
 
@@ -47,9 +71,9 @@ __device__ __forceinline__ int xcd_virtual_id() {
   return (b % 8) * (n / 8) + b / 8;
 }
 
-// Block-wide inclusive scan (256 threads).
-__device__ int scan256(int v, int* s_tmp, int& total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+// Block-wide inclusive scan (up to 16 wavefronts; s_tmp holds one int per wave).
+__device__ int block_scan(int v, int* s_tmp, int& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const int n = __shfl_up(v, o, 64);
@@ -59,8 +83,7 @@ __device__ int scan256(int v, int* s_tmp, int& total) {
   __syncthreads();
   int before = 0;
   total = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < nw; ++i) {
     const int t = s_tmp[i];
     if (i < w) before += t;
     total += t;
@@ -110,14 +133,14 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(
 // so that the MFMA fragment reads hit 16 (or 32) different LDS bank groups of
 // gfx950's 64 banks.
 // ---------------------------------------------------------------------------
-template <int ROWS, int BK>
+template <int ROWS, int BK, int NW>
 struct KTile {
   static constexpr int CPR = BK / 8;     // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;   // rows per wavefront load
   static constexpr int NI = ROWS / RPI;  // wavefront loads per tile
-  static constexpr int PER_WAVE = NI / 4;
+  static constexpr int PER_WAVE = NI / NW;
   static constexpr int BYTES = ROWS * BK * 2;
-  static_assert(NI % 4 == 0, "tile must split over 4 wavefronts");
+  static_assert(NI % NW == 0, "tile must split over the wavefronts");
   __device__ __forceinline__ static int swz(int r) {
     if constexpr (CPR == 8) return (r >> 1) & 7;
     else return (r >> 2) & 3;
@@ -128,7 +151,7 @@ struct KTile {
     const int l = lane64(), w = wave_id();
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i) {
-      const int q = w + 4 * i;
+      const int q = w + NW * i;
       const int r = q * RPI + l / CPR;
       const int c = (l % CPR) ^ swz(r);
       dma16(rs, lds + q * 1024, rowoff(r) + (uint32_t)(k0 + c * 8) * 2u);
@@ -150,14 +173,14 @@ struct KTile {
   }
 };
 
-template <int ROWS, int BK>
+template <int ROWS, int BK, int NW>
 struct MTile {
   static constexpr int RB = ROWS * 2;    // bytes per k row
   static constexpr int KPI = 1024 / RB;  // k rows per wavefront load
   static constexpr int NI = BK / KPI;
-  static constexpr int PER_WAVE = NI / 4;
+  static constexpr int PER_WAVE = NI / NW;
   static constexpr int BYTES = ROWS * BK * 2;
-  static_assert(NI % 4 == 0 && KPI >= 1, "tile must split over 4 wavefronts");
+  static_assert(NI % NW == 0 && KPI >= 1, "tile must split over the wavefronts");
   __device__ __forceinline__ static int swz(int k) { return 4 * (k & 3); }
   // koff(k): byte offset of tile k-row k at the tile's first m/n.
   template <class KOff>
@@ -165,7 +188,7 @@ struct MTile {
     const int l = lane64(), w = wave_id();
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i) {
-      const int q = w + 4 * i;
+      const int q = w + NW * i;
       const int k = q * KPI + (l * 16) / RB;
       const int c = ((l * 16) % RB) / 16 ^ swz(k);
       dma16(rs, lds + q * 1024, koff(k) + (uint32_t)c * 16u);
@@ -195,16 +218,18 @@ struct MTile {
 };
 
 // ---------------------------------------------------------------------------
-// MFMA tile core: 4 wavefronts as 2 x 2, each owning (BM/2) x (BN/2) of the
-// output as 32x32 blocks. The MFMA is fed the B rows as its first operand,
-// so each lane ends up with 4 consecutive output columns of one output row:
-// block (i, j), register q of lane l holds row  wm*BM/2 + 32 i + l % 32  and
-// column  bcol(j) + 8 (q / 4) + 4 (l / 32) + q % 4.
+// MFMA tile core: WGM x WGN wavefronts, each owning (BM/WGM) x (BN/WGN) of
+// the output as 32x32 blocks. The MFMA is fed the B rows as its first
+// operand, so each lane ends up with 4 consecutive output columns of one
+// output row: block (i, j), register q of lane l holds row
+// wm*WM + 32 i + l % 32 and column bcol(j) + 8 (q / 4) + 4 (l / 32) + q % 4.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, bool SWIGLU_COLS>
+template <int BM, int BN, int WGM, int WGN, bool SWIGLU_COLS>
 struct Core {
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int MB = WM / 32, NB = WN / 32;
+  static constexpr int GW = BN / 2 / WGN;  // SwiGLU: gate (or up) columns per wave
+  static_assert(MB >= 1 && NB >= 1 && (!SWIGLU_COLS || NB % 2 == 0), "wave tile");
   f32x16 acc[MB][NB];
 
   // LDS row of the B tile that wave column wn's block j starts at.
@@ -213,7 +238,7 @@ struct Core {
       // gate rows live in [0, BN/2), up rows in [BN/2, BN); the wave keeps the
       // gate block j and the up block j + NB/2 of the same output columns
       constexpr int H = NB / 2;
-      return j < H ? wn * (BN / 4) + j * 32 : BN / 2 + wn * (BN / 4) + (j - H) * 32;
+      return j < H ? wn * GW + j * 32 : BN / 2 + wn * GW + (j - H) * 32;
     } else {
       return wn * WN + j * 32;
     }
@@ -245,6 +270,42 @@ struct Core {
       }
     }
   };
+
+  // Operand fragments of one k-step, double-buffered in registers.
+  struct Frags {
+    bf16x8 a[2][MB], b[2][NB];
+  };
+
+  template <class AT, class BT, int BK>
+  __device__ __forceinline__ static void load_frags(Frags& f, int set, const char* As, const char* Bs,
+                                                    const Offsets<AT, BT, BK>& o, int kk) {
+#pragma unroll
+    for (int i = 0; i < MB; ++i) f.a[set][i] = AT::frag(As, o.a[i], o.ka, kk);
+#pragma unroll
+    for (int j = 0; j < NB; ++j) f.b[set][j] = BT::frag(Bs, o.b[j], o.kb, kk);
+  }
+
+  // The MFMAs of one k-step from register set `set`, with the LDS reads of
+  // the next k-step's fragments (if any) interleaved: one read after each of
+  // the first MB + NB MFMAs, so the reads complete under the matrix work.
+  template <class AT, class BT, int BK>
+  __device__ __forceinline__ void mfma_step(Frags& f, int set, bool prefetch, const char* nAs, const char* nBs,
+                                            const Offsets<AT, BT, BK>& o, int nkk) {
+#pragma unroll
+    for (int s = 0; s < MB * NB; ++s) {
+      const int i = s / NB, j = s % NB;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[set][j], f.a[set][i], acc[i][j], 0, 0, 0);
+      if (prefetch && s < MB + NB) {
+        if (s < MB) f.a[set ^ 1][s] = AT::frag(nAs, o.a[s], o.ka, nkk);
+        else f.b[set ^ 1][s - MB] = BT::frag(nBs, o.b[s - MB], o.kb, nkk);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < MB * NB; ++s) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      if (s < MB + NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    }
+  }
 
   template <class AT, class BT, int BK>
   __device__ __forceinline__ void compute(const char* As, const char* Bs, const Offsets<AT, BT, BK>& o) {
@@ -285,6 +346,53 @@ __device__ __forceinline__ void wait_stage(int ahead) {
 }
 
 // ---------------------------------------------------------------------------
+// Software-pipelined K loop over an LDS ring of NS >= 3 stages.
+//
+// Stage kt's first fragments are already in registers when iteration kt
+// starts. Before the last k-step of a stage, each wavefront waits for its own
+// loads of stage kt+1, the workgroup barrier publishes them (and retires all
+// reads of the stage kt-1 buffer), the loads of stage kt+NS-1 are issued into
+// that buffer, and the last k-step's MFMAs run while the next stage's first
+// fragments are read. issue(kt) issues the loads of stage kt; next() tells
+// whether more stages follow (stage count known up front: KT).
+// ---------------------------------------------------------------------------
+template <class CoreT, class AT, class BT, int BK, int NS, class Issue>
+__device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
+                                                 const typename CoreT::template Offsets<AT, BT, BK>& o,
+                                                 Issue&& issue) {
+  static_assert(NS >= 3, "the prefetch across the barrier needs three stages");
+  constexpr int KK = BK / 16;
+  constexpr int STAGE = AT::BYTES + BT::BYTES;
+  constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
+  typename CoreT::Frags f;
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < KT) issue(s);
+  wait_stage<NS, PER>((NS - 2 < KT - 1 ? NS - 2 : KT - 1));
+  __syncthreads();
+  CoreT::template load_frags<AT, BT, BK>(f, 0, lds, lds + AT::BYTES, o, 0);
+  for (int kt = 0; kt < KT; ++kt) {
+    const char* st = lds + (kt % NS) * STAGE;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int set = kk & 1;
+      if (kk < KK - 1) {
+        core.template mfma_step<AT, BT, BK>(f, set, true, st, st + AT::BYTES, o, kk + 1);
+      } else {
+        if (kt + 1 < KT) {
+          const int last = kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1;
+          wait_stage<NS, PER>(last - (kt + 1));
+        }
+        __syncthreads();
+        if (kt + NS - 1 < KT) issue(kt + NS - 1);
+        const char* nst = lds + ((kt + 1) % NS) * STAGE;
+        core.template mfma_step<AT, BT, BK>(f, set, kt + 1 < KT, nst, nst + AT::BYTES, o, 0);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Row-grouped GEMM: for each slot j, rows [off_j, off_{j+1}) (clamped to
 // n_cap) times the slot's weight matrix.
 // ---------------------------------------------------------------------------
@@ -314,7 +422,7 @@ struct RowsArgs {
 template <int BM>
 __device__ void build_slot_tiles(const int32_t* __restrict__ off, int S, int64_t n_cap, int* s_mt, int* s_tmp) {
   int carry = 0;
-  for (int j0 = 0; j0 < S; j0 += kThreads) {
+  for (int j0 = 0; j0 < S; j0 += (int)blockDim.x) {
     const int j = j0 + threadIdx.x;
     int n = 0;
     if (j < S) {
@@ -324,7 +432,7 @@ __device__ void build_slot_tiles(const int32_t* __restrict__ off, int S, int64_t
       n = hi > lo ? (int)((hi - lo + BM - 1) / BM) : 0;
     }
     int total;
-    const int incl = scan256(n, s_tmp, total);
+    const int incl = block_scan(n, s_tmp, total);
     if (j < S) s_mt[j] = carry + incl - n;
     carry += total;
   }
@@ -332,27 +440,29 @@ __device__ void build_slot_tiles(const int32_t* __restrict__ off, int S, int64_t
   __syncthreads();
 }
 
-template <int BM, int BN, int BK, int NS, bool B_KMAJ, int EPI>
-__global__ __launch_bounds__(kThreads) void gemm_rows_kernel(RowsArgs a) {
+template <int BM, int BN, int BK, int NS, int WGM, int WGN, bool B_KMAJ, int EPI>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   constexpr bool SW = (EPI == kEpiSwigluFwd);
-  using AT = KTile<BM, BK>;
-  using BT = typename std::conditional<B_KMAJ, KTile<BN, BK>, MTile<BN, BK>>::type;
+  constexpr int NW = WGM * WGN;
+  using CoreT = Core<BM, BN, WGM, WGN, SW>;
+  using AT = KTile<BM, BK, NW>;
+  using BT = typename std::conditional<B_KMAJ, KTile<BN, BK, NW>, MTile<BN, BK, NW>>::type;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
   constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
   __shared__ int s_mt[FOREMOE_MAX_SLOTS + 1];
-  __shared__ int s_tmp[4];
+  __shared__ int s_tmp[16];
 
   build_slot_tiles<BM>(a.slot_offset, a.S, a.n_cap, s_mt, s_tmp);
   const int n_tiles = a.N / BN;
   const int total = s_mt[a.S] * n_tiles;
   const int lane = lane64(), wave = wave_id();
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int KT = a.K / BK;
   const uint32_t lds0 = lds_addr(lds);
 
-  Core<BM, BN, SW> core;
-  const typename Core<BM, BN, SW>::template Offsets<AT, BT, BK> offs(wm, wn);
+  CoreT core;
+  const typename CoreT::template Offsets<AT, BT, BK> offs(wm, wn);
 
   for (int t = xcd_virtual_id(); t < total; t += gridDim.x) {
     const int mtg = t / n_tiles, nt = t % n_tiles;
@@ -399,32 +509,36 @@ __global__ __launch_bounds__(kThreads) void gemm_rows_kernel(RowsArgs a) {
     };
 
     core.zero();
+    if constexpr (NS >= 3 && BK % 32 == 0) {
+      pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
+    } else {
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < KT) issue(s);
-    for (int kt = 0; kt < KT; ++kt) {
-      const int ahead = (kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1) - kt;
-      wait_stage<NS, PER>(ahead);
-      __syncthreads();
-      if (kt + NS - 1 < KT) issue(kt + NS - 1);
-      const char* st = lds + (kt % NS) * STAGE;
-      core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
+      for (int s = 0; s < NS - 1; ++s)
+        if (s < KT) issue(s);
+      for (int kt = 0; kt < KT; ++kt) {
+        const int ahead = (kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1) - kt;
+        wait_stage<NS, PER>(ahead);
+        __syncthreads();
+        if (kt + NS - 1 < KT) issue(kt + NS - 1);
+        const char* st = lds + (kt % NS) * STAGE;
+        core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
+      }
     }
     __syncthreads();  // all reads of this tile's stages done before the next tile's loads
 
     // ---------------- epilogue ----------------
     const int l32 = lane & 31, c4 = (lane >> 5) * 4;
 #pragma unroll
-    for (int i = 0; i < Core<BM, BN, SW>::MB; ++i) {
-      const int64_t row = m0 + wm * (BM / 2) + i * 32 + l32;
+    for (int i = 0; i < CoreT::MB; ++i) {
+      const int64_t row = m0 + wm * CoreT::WM + i * 32 + l32;
       if (row >= rend) continue;
       if constexpr (EPI == kEpiSwigluFwd) {
-        constexpr int H = Core<BM, BN, SW>::NB / 2;
+        constexpr int H = CoreT::NB / 2;
 #pragma unroll
         for (int jj = 0; jj < H; ++jj) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
-            const int f = f0 + wn * (BN / 4) + jj * 32 + g * 8 + c4;
+            const int f = f0 + wn * CoreT::GW + jj * 32 + g * 8 + c4;
             float hv[4], av[4], uv[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -442,26 +556,37 @@ __global__ __launch_bounds__(kThreads) void gemm_rows_kernel(RowsArgs a) {
           }
         }
       } else {
+        [[maybe_unused]] uint2 ra[CoreT::NB][4], ru[CoreT::NB][4];
+        if constexpr (EPI == kEpiSwigluBwd) {
+          // all saved-activation loads of this row block first
 #pragma unroll
-        for (int jj = 0; jj < Core<BM, BN, SW>::NB; ++jj) {
+          for (int jj = 0; jj < CoreT::NB; ++jj)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int n = n0 + wn * CoreT::WN + jj * 32 + g * 8 + c4;
+              ra[jj][g] = *reinterpret_cast<const uint2*>(a.AU + row * a.ldau + n);
+              ru[jj][g] = *reinterpret_cast<const uint2*>(a.AU + row * a.ldau + a.F + n);
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < CoreT::NB; ++jj) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
-            const int n = n0 + wn * (BN / 2) + jj * 32 + g * 8 + c4;
+            const int n = n0 + wn * CoreT::WN + jj * 32 + g * 8 + c4;
             float v[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = core.acc[i][jj][g * 4 + e];
             if constexpr (EPI == kEpiSwigluBwd) {
               // v = dH at columns f = n..n+3; saved A in [0, F), U in [F, 2F)
-              const uint2 ra = *reinterpret_cast<const uint2*>(a.AU + row * a.ldau + n);
-              const uint2 ru = *reinterpret_cast<const uint2*>(a.AU + row * a.ldau + a.F + n);
-              const float A4[4] = {bf2f(ra.x & 0xFFFF), bf2f(ra.x >> 16), bf2f(ra.y & 0xFFFF), bf2f(ra.y >> 16)};
-              const float U4[4] = {bf2f(ru.x & 0xFFFF), bf2f(ru.x >> 16), bf2f(ru.y & 0xFFFF), bf2f(ru.y >> 16)};
+              const uint2 xa = ra[jj][g], xu = ru[jj][g];
+              const float A4[4] = {bf2f(xa.x & 0xFFFF), bf2f(xa.x >> 16), bf2f(xa.y & 0xFFFF), bf2f(xa.y >> 16)};
+              const float U4[4] = {bf2f(xu.x & 0xFFFF), bf2f(xu.x >> 16), bf2f(xu.y & 0xFFFF), bf2f(xu.y >> 16)};
               float da[4], du[4];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                const float s = 1.0f / (1.0f + __expf(-A4[e]));
-                da[e] = v[e] * U4[e] * (s + A4[e] * s * (1.0f - s));
-                du[e] = v[e] * A4[e] * s;
+                const float sg = 1.0f / (1.0f + __expf(-A4[e]));
+                da[e] = v[e] * U4[e] * (sg + A4[e] * sg * (1.0f - sg));
+                du[e] = v[e] * A4[e] * sg;
               }
               *reinterpret_cast<uint2*>(a.C + row * a.ldc + n) = make_uint2(pack_bf2(da[0], da[1]), pack_bf2(da[2], da[3]));
               *reinterpret_cast<uint2*>(a.C + row * a.ldc + a.F + n) =
@@ -521,21 +646,22 @@ __device__ void build_wgrad_plan(const WgradArgs& a, WgradPlan& P) {
   const int tid = threadIdx.x;
   const int S = a.S, G = a.G;
   const int tpg = (a.M / BM) * (a.N / BN);
+  const int nt = blockDim.x;
   if (tid == 0) P.nne = 0;
-  for (int g = tid; g < G; g += kThreads) P.rows[g] = 0;
-  for (int j = tid; j <= S; j += kThreads) {
+  for (int g = tid; g < G; g += nt) P.rows[g] = 0;
+  for (int j = tid; j <= S; j += nt) {
     const int64_t o = a.slot_offset[j];
     P.off[j] = (int)(o < 0 ? 0 : (o > a.n_cap ? a.n_cap : o));
   }
   __syncthreads();
-  for (int j = tid; j < S; j += kThreads) {
+  for (int j = tid; j < S; j += nt) {
     const int g = a.slot_gidx[j];
     const int n = P.off[j + 1] - P.off[j];
     P.gidx[j] = (g >= 0 && g < G && n > 0) ? g : -1;
     if (P.gidx[j] >= 0) atomicAdd(&P.rows[g], n);
   }
   __syncthreads();
-  for (int g = tid; g < G; g += kThreads) {
+  for (int g = tid; g < G; g += nt) {
     const int rg = P.rows[g];
     if (rg <= 0) continue;
     int rank = 0;
@@ -626,10 +752,12 @@ __device__ __forceinline__ void cursor_advance(const WgradPlan& P, int S, int g,
   if (c.k >= c.hi) cursor_next_slot(P, S, g, s1, c);
 }
 
-template <int BM, int BN, int BK, int NS>
-__global__ __launch_bounds__(kThreads) void gemm_wgrad_kernel(WgradArgs a) {
-  using AT = MTile<BM, BK>;
-  using BT = MTile<BN, BK>;
+template <int BM, int BN, int BK, int NS, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a) {
+  constexpr int NW = WGM * WGN;
+  using CoreT = Core<BM, BN, WGM, WGN, false>;
+  using AT = MTile<BM, BK, NW>;
+  using BT = MTile<BN, BK, NW>;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
   constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
@@ -640,11 +768,11 @@ __global__ __launch_bounds__(kThreads) void gemm_wgrad_kernel(WgradArgs a) {
   const int mt_n = a.M / BM, nt_n = a.N / BN, tpg = mt_n * nt_n;
   const int total = P.ibase[P.nne];
   const int lane = lane64(), wave = wave_id();
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const uint32_t lds0 = lds_addr(lds);
   const uint32_t lda2 = (uint32_t)(a.lda * 2), ldb2 = (uint32_t)(a.ldb * 2);
-  Core<BM, BN, false> core;
-  const typename Core<BM, BN, false>::template Offsets<AT, BT, BK> offs(wm, wn);
+  CoreT core;
+  const typename CoreT::template Offsets<AT, BT, BK> offs(wm, wn);
 
   for (int t = xcd_virtual_id(); t < total; t += gridDim.x) {
     int lo = 0, hi = P.nne - 1;
@@ -662,72 +790,105 @@ __global__ __launch_bounds__(kThreads) void gemm_wgrad_kernel(WgradArgs a) {
     const int s0 = P.ch == INT_MAX ? 0 : c * P.ch;
     const int s1 = P.ch == INT_MAX ? rg : (s0 + P.ch < rg ? s0 + P.ch : rg);
 
+    // number of k-tiles of this chunk (each k-tile stays inside one slot)
+    int KT = 0;
+    for (KCursor cc = cursor_begin(P, S, g, s0, s1); !cc.done; cursor_next_slot(P, S, g, s1, cc))
+      KT += (cc.hi - cc.lo + BK - 1) / BK;
     KCursor ic = cursor_begin(P, S, g, s0, s1);
-    auto issue = [&](int slot_stage, const KCursor& cur) {
-      const uint32_t sa = lds0 + (uint32_t)(slot_stage * STAGE);
+    auto issue = [&](int kt) {
+      // called once per k-tile, in order: load the cursor's tile, then advance
+      const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
       // the segment's rows [lo, hi): rows past hi read as zero
-      const i32x4 rsa = buf_rsrc(a.A + (int64_t)cur.lo * a.lda, (uint32_t)(cur.hi - cur.lo) * lda2);
-      const i32x4 rsb = buf_rsrc(a.B + (int64_t)cur.lo * a.ldb, (uint32_t)(cur.hi - cur.lo) * ldb2);
-      const int kr = cur.k - cur.lo;
+      const i32x4 rsa = buf_rsrc(a.A + (int64_t)ic.lo * a.lda, (uint32_t)(ic.hi - ic.lo) * lda2);
+      const i32x4 rsb = buf_rsrc(a.B + (int64_t)ic.lo * a.ldb, (uint32_t)(ic.hi - ic.lo) * ldb2);
+      const int kr = ic.k - ic.lo;
       AT::issue(rsa, sa, [&](int k) -> uint32_t { return (uint32_t)(kr + k) * lda2 + (uint32_t)m0 * 2u; });
       BT::issue(rsb, sa + AT::BYTES,
                 [&](int k) -> uint32_t { return (uint32_t)(kr + k) * ldb2 + (uint32_t)n0 * 2u; });
+      cursor_advance<BK>(P, S, g, s1, ic);
     };
 
     core.zero();
-    int issued = 0;
+    if constexpr (NS >= 3 && BK % 32 == 0) {
+      pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
+    } else {
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) {
-      if (!ic.done) {
-        issue(issued % NS, ic);
-        cursor_advance<BK>(P, S, g, s1, ic);
-        ++issued;
+      for (int s = 0; s < NS - 1; ++s)
+        if (s < KT) issue(s);
+      for (int kt = 0; kt < KT; ++kt) {
+        wait_stage<NS, PER>((kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1) - kt);
+        __syncthreads();
+        if (kt + NS - 1 < KT) issue(kt + NS - 1);
+        const char* st = lds + (kt % NS) * STAGE;
+        core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
       }
-    }
-    for (int kt = 0; kt < issued; ++kt) {
-      wait_stage<NS, PER>(issued - 1 - kt);
-      __syncthreads();
-      if (!ic.done) {
-        issue(issued % NS, ic);
-        cursor_advance<BK>(P, S, g, s1, ic);
-        ++issued;
-      }
-      const char* st = lds + (kt % NS) * STAGE;
-      core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
     }
     __syncthreads();
 
     const int l32 = lane & 31, c4 = (lane >> 5) * 4;
     if (c == 0) {
+      // dW += acc. The current dW values of this wave's output are brought
+      // into LDS with asynchronous buffer loads (two 32-row blocks at a time,
+      // all loads in flight together; each wave uses its own LDS region, so
+      // no barrier is needed), then added to the accumulators and stored.
       float* Cg = a.C + (int64_t)g * a.gstride;
+      constexpr int RB = CoreT::WN * 4;  // bytes of one output row of this wave
+      constexpr int CH = RB / 16;        // 16-byte chunks per row
+      constexpr int REGION = 2 * 32 * RB;
+      static_assert(NW * REGION <= NS * STAGE, "epilogue staging must fit the LDS stages");
+      static_assert(CH >= 16 && (CH & (CH - 1)) == 0, "row chunks");
+      const i32x4 rsc = buf_rsrc(Cg, (uint32_t)((int64_t)a.M * a.N * 4));
+      char* wl = lds + wave * REGION;
+      const int nb = n0 + wn * CoreT::WN;
 #pragma unroll
-      for (int i = 0; i < Core<BM, BN, false>::MB; ++i) {
-        const int64_t m = m0 + wm * (BM / 2) + i * 32 + l32;
+      for (int ph = 0; ph < (CoreT::MB + 1) / 2; ++ph) {
 #pragma unroll
-        for (int jj = 0; jj < Core<BM, BN, false>::NB; ++jj) {
+        for (int ii = 0; ii < 2; ++ii) {
+          const int i = ph * 2 + ii;
+          if (i >= CoreT::MB) break;
+          const int mb = m0 + wm * CoreT::WM + i * 32;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int n = n0 + wn * (BN / 2) + jj * 32 + q * 8 + c4;
-            float4* p = reinterpret_cast<float4*>(Cg + m * a.ldc + n);
-            float4 o = *p;
-            o.x += core.acc[i][jj][q * 4 + 0];
-            o.y += core.acc[i][jj][q * 4 + 1];
-            o.z += core.acc[i][jj][q * 4 + 2];
-            o.w += core.acc[i][jj][q * 4 + 3];
-            *p = o;
+          for (int q = 0; q < 32 * RB / 1024; ++q) {
+            const int r = q * (1024 / RB) + (lane * 16) / RB;
+            const int pc = ((lane * 16) % RB) / 16;
+            const int lc = pc ^ (r & (CH - 1));
+            dma16(rsc, lds_addr(wl + ii * (32 * RB) + q * 1024),
+                  (uint32_t)(((int64_t)(mb + r) * a.ldc + nb) * 4) + (uint32_t)lc * 16u);
           }
         }
+        wait_vm<0>();
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii) {
+          const int i = ph * 2 + ii;
+          if (i >= CoreT::MB) break;
+          const int64_t m = m0 + wm * CoreT::WM + i * 32 + l32;
+#pragma unroll
+          for (int jj = 0; jj < CoreT::NB; ++jj) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int nl = jj * 32 + q * 8 + c4;
+              const int pc = (nl / 4) ^ (l32 & (CH - 1));
+              float4 o = *reinterpret_cast<const float4*>(wl + ii * (32 * RB) + l32 * RB + pc * 16);
+              o.x += core.acc[i][jj][q * 4 + 0];
+              o.y += core.acc[i][jj][q * 4 + 1];
+              o.z += core.acc[i][jj][q * 4 + 2];
+              o.w += core.acc[i][jj][q * 4 + 3];
+              *reinterpret_cast<float4*>(Cg + m * a.ldc + nb + nl) = o;
+            }
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): LDS reads done before the region is refilled
       }
     } else {
       float* Pt = a.part + (int64_t)(P.pbase[gi] + (c - 1) * tpg + tile) * (BM * BN);
 #pragma unroll
-      for (int i = 0; i < Core<BM, BN, false>::MB; ++i) {
-        const int m = wm * (BM / 2) + i * 32 + l32;
+      for (int i = 0; i < CoreT::MB; ++i) {
+        const int m = wm * CoreT::WM + i * 32 + l32;
 #pragma unroll
-        for (int jj = 0; jj < Core<BM, BN, false>::NB; ++jj) {
+        for (int jj = 0; jj < CoreT::NB; ++jj) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int n = wn * (BN / 2) + jj * 32 + q * 8 + c4;
+            const int n = wn * CoreT::WN + jj * 32 + q * 8 + c4;
             *reinterpret_cast<float4*>(Pt + m * BN + n) =
                 make_float4(core.acc[i][jj][q * 4 + 0], core.acc[i][jj][q * 4 + 1], core.acc[i][jj][q * 4 + 2],
                             core.acc[i][jj][q * 4 + 3]);
@@ -735,12 +896,16 @@ __global__ __launch_bounds__(kThreads) void gemm_wgrad_kernel(WgradArgs a) {
         }
       }
     }
+    __syncthreads();  // the epilogue's LDS staging is done before the next item's loads
   }
 }
 
-// dW[g] tile += partials of chunks 1.. in chunk order (one workgroup per tile).
+// dW[g] tile += partials of chunks 1.. in chunk order. Each tile is cut into
+// kReduceParts row bands, one workgroup per band, so that all CUs stream.
+constexpr int kReduceParts = 16;
+
 template <int BM, int BN, int BK>
-__global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(WgradArgs a) {
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
   __shared__ WgradPlan P;
   build_wgrad_plan<BM, BN, BK>(a, P);
   if (P.ch == INT_MAX) return;
@@ -748,31 +913,50 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(WgradArgs a) {
   // split groups come first in the ordering (largest rows), so walk until C_g == 1
   int nsplit = 0;
   while (nsplit < P.nne && (P.rows[P.order[nsplit]] + P.ch - 1) / P.ch > 1) ++nsplit;
-  const int total = nsplit * tpg;
+  const int total = nsplit * tpg * kReduceParts;
+  constexpr int BAND = BM * BN / kReduceParts;  // elements per band
+  constexpr int V = BAND / 1024 < 4 ? BAND / 1024 : 4;  // float4 per thread per pass
+  static_assert(V >= 1 && BAND % (256 * 4 * V) == 0, "band split");
   for (int t = blockIdx.x; t < total; t += gridDim.x) {
-    const int gi = t / tpg, tile = t % tpg;
+    const int part = t % kReduceParts, tt = t / kReduceParts;
+    const int gi = tt / tpg, tile = tt % tpg;
     const int g = P.order[gi];
     const int cg = (P.rows[g] + P.ch - 1) / P.ch;
     const int m0 = (tile / nt_n) * BM, n0 = (tile % nt_n) * BN;
     float* Cg = a.C + (int64_t)g * a.gstride;
     const float* P0 = a.part + (int64_t)(P.pbase[gi] + tile) * (BM * BN);
-    for (int e = threadIdx.x * 4; e < BM * BN; e += kThreads * 4) {
-      float4 s = *reinterpret_cast<const float4*>(P0 + e);
+    const int64_t cstride = (int64_t)tpg * (BM * BN);
+    for (int e0 = part * BAND + threadIdx.x * 4; e0 < (part + 1) * BAND; e0 += 256 * 4 * V) {
+      float4 s[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) s[v] = *reinterpret_cast<const float4*>(P0 + e0 + v * 1024);
       for (int c = 2; c < cg; ++c) {
-        const float4 v = *reinterpret_cast<const float4*>(P0 + (int64_t)(c - 1) * tpg * (BM * BN) + e);
-        s.x += v.x;
-        s.y += v.y;
-        s.z += v.z;
-        s.w += v.w;
+        float4 x[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v) x[v] = *reinterpret_cast<const float4*>(P0 + (c - 1) * cstride + e0 + v * 1024);
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          s[v].x += x[v].x;
+          s[v].y += x[v].y;
+          s[v].z += x[v].z;
+          s[v].w += x[v].w;
+        }
       }
-      const int m = m0 + e / BN, n = n0 + e % BN;
-      float4* p = reinterpret_cast<float4*>(Cg + (int64_t)m * a.ldc + n);
-      float4 o = *p;
-      o.x += s.x;
-      o.y += s.y;
-      o.z += s.z;
-      o.w += s.w;
-      *p = o;
+      float4 o[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        const int e = e0 + v * 1024;
+        o[v] = *reinterpret_cast<const float4*>(Cg + (int64_t)(m0 + e / BN) * a.ldc + n0 + e % BN);
+      }
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        const int e = e0 + v * 1024;
+        o[v].x += s[v].x;
+        o[v].y += s[v].y;
+        o[v].z += s[v].z;
+        o[v].w += s[v].w;
+        *reinterpret_cast<float4*>(Cg + (int64_t)(m0 + e / BN) * a.ldc + n0 + e % BN) = o[v];
+      }
     }
   }
 }
@@ -877,9 +1061,14 @@ int persistent_grid() { return num_cus(); }
 // stages of 64-deep K slices (128 KiB), or 128-wide with 3 stages (144 KiB).
 template <int BN, bool KMAJ, int EPI>
 void launch_rows(const RowsArgs& a, hipStream_t st) {
-  constexpr int NS = BN == 256 ? 2 : 3;
-  hipLaunchKernelGGL((gemm_rows_kernel<256, BN, 64, NS, KMAJ, EPI>), dim3(persistent_grid()), dim3(kThreads), 0, st,
-                     a);
+  if constexpr (BN == 256) {
+    constexpr int WGM = FM_ROWS_WGM, WGN = FM_ROWS_WGN;
+    hipLaunchKernelGGL((gemm_rows_kernel<256, 256, FM_ROWS_BK, FM_ROWS_NS, WGM, WGN, KMAJ, EPI>),
+                       dim3(persistent_grid()), dim3(64 * WGM * WGN), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((gemm_rows_kernel<256, 128, 64, 3, 2, 2, KMAJ, EPI>), dim3(persistent_grid()), dim3(256), 0,
+                       st, a);
+  }
 }
 
 // Partial-tile budget of the weight-gradient split (tiles of 256 x 256 fp32).
@@ -905,8 +1094,9 @@ static int check_ffn(const char* who, foremoe_dtype dtype, int32_t d, int32_t F,
   REQUIRE(slot_offset, "%s: slot_offset is NULL", who);
   if (dtype == FOREMOE_BF16 && (d % 128 != 0 || F % 128 != 0))
     return set_error(FOREMOE_EUNSUPPORTED, "%s: bf16 needs d %% 128 == 0 and F %% 128 == 0 (d=%d, F=%d)", who, d, F);
-  if (dtype == FOREMOE_BF16 && (n_cap + 256) * (int64_t)(d > 2 * F ? d : 2 * F) * 2 >= ((int64_t)1 << 31))
-    return set_error(FOREMOE_EUNSUPPORTED, "%s: n_cap * row bytes must stay below 2 GiB", who);
+  // 32-bit buffer offsets: (rows of one slot + one tile) * row bytes must fit
+  if (dtype == FOREMOE_BF16 && (n_cap + 256) * (int64_t)(d > 2 * F ? d : 2 * F) * 2 >= ((int64_t)1 << 32))
+    return set_error(FOREMOE_EUNSUPPORTED, "%s: (n_cap + 256) * row bytes must stay below 4 GiB", who);
   return FOREMOE_OK;
 }
 
@@ -1104,15 +1294,17 @@ static int wgrad_common(const char* who, const void* A, int lda, const void* B, 
     a.ldc = N;
     a.gstride = (int64_t)M * N;
     a.part = (float*)ws;
-    const dim3 grid(persistent_grid()), block(kThreads);
+    const dim3 grid(persistent_grid()), block(256);
     if (M % 256 == 0 && N % 256 == 0) {
+      constexpr int WGM = FM_WG_WGM, WGN = FM_WG_WGN;
       a.p_max = (int)(ws_bytes / (256 * 256 * 4));
-      hipLaunchKernelGGL((gemm_wgrad_kernel<256, 256, 64, 2>), grid, block, 0, st, a);
-      if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<256, 256, 64>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((gemm_wgrad_kernel<256, 256, FM_WG_BK, FM_WG_NS, WGM, WGN>), grid, dim3(64 * WGM * WGN), 0,
+                         st, a);
+      if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<256, 256, FM_WG_BK>), dim3(persistent_grid() * 4), block, 0, st, a);
     } else {
       a.p_max = (int)(ws_bytes / (128 * 128 * 4));
-      hipLaunchKernelGGL((gemm_wgrad_kernel<128, 128, 64, 3>), grid, block, 0, st, a);
-      if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<128, 128, 64>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((gemm_wgrad_kernel<128, 128, 64, 3, 2, 2>), grid, block, 0, st, a);
+      if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<128, 128, 64>), dim3(persistent_grid() * 4), block, 0, st, a);
     }
   } else {
     hipLaunchKernelGGL(f32_wgrad_kernel, dim3((N + 15) / 16, (M + 15) / 16, G), dim3(256), 0, st, (const float*)A, lda,

@@ -103,8 +103,8 @@ def test_ffn_rejects_unsupported_bf16_shapes(lib):
     rc = lib.foremoe_grouped_ffn_wgrad(FAKE, FAKE, FAKE, FAKE, 1, 128, 128, 4, FAKE, FAKE, 2, 64, FAKE, FAKE,
                                        None, 1024, None)
     assert rc == -1  # ws NULL with ws_bytes > 0
-    # n_cap * row bytes must stay below 2 GiB for 32-bit buffer offsets
-    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 4096, 1024, 4, FAKE, FAKE, 3, FAKE, FAKE, 1 << 18, FAKE, FAKE, None,
+    # (n_cap + 256) * row bytes must stay below 4 GiB for 32-bit buffer offsets
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 8192, 1024, 4, FAKE, FAKE, 3, FAKE, FAKE, 1 << 18, FAKE, FAKE, None,
                                      None)
     assert rc == -2
     assert lib.foremoe_wgrad_workspace_size(2048, 768) > 0
