@@ -11,7 +11,7 @@ namespace foremoe {
 // Pairs handled by one workgroup of the histogram and rank kernels. The two
 // kernels must agree: the rank kernel starts each block from the prefix of
 // the histogram's per-block counts.
-constexpr int kHistChunk = 2048;
+constexpr int kHistChunk = 512;
 constexpr int kHistThreads = 256;
 constexpr int kWsHeaderBytes = 256;
 

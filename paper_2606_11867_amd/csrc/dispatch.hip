@@ -282,9 +282,32 @@ __global__ __launch_bounds__(kHistThreads) void permute_rank_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Step 3b: gather token rows into slot order, 16-byte vectors, one row per
-// wavefront iteration, four vectors in flight per lane.
+// Step 3b: gather token rows into slot order. A wavefront moves kRowsPerWave
+// rows at a time: their pair indices arrive in one lane-parallel load, then
+// every 16-byte load of the group is issued before the stores.
 // ---------------------------------------------------------------------------
+constexpr int kRowsPerWave = 4;
+constexpr int kVecPerLane = 4;  // 16-byte vectors per lane per row and pass
+
+// Range-checked 16-byte loads from one wave-uniform byte range: offsets at or
+// past `bytes` read as zero without touching memory, so loads need no branch
+// (and a zero-byte range turns a whole row of loads into zeros).
+struct RowReader {
+  __amdgpu_buffer_rsrc_t rs;
+  __device__ __forceinline__ RowReader(const void* base, uint32_t bytes)
+      : rs(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000)) {}
+  __device__ __forceinline__ uint4 load(uint32_t off) const {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+  }
+};
+
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 __global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restrict__ x, int64_t vec_per_row, int K,
                                                           int64_t npairs, const int32_t* __restrict__ row_to_pair,
                                                           const int32_t* __restrict__ n_rows_dev, int64_t n_cap,
@@ -294,20 +317,34 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restric
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   int64_t N = *n_rows_dev;
   if (N > n_cap) N = n_cap;
-  for (int64_t row = wave; row < N; row += nwaves) {
-    const int64_t p = row_to_pair[row];
-    if (p < 0 || p >= npairs) continue;  // never taken when the maps are consistent
-    const int64_t t = p / K;
-    const uint4* src = x + t * vec_per_row;
-    uint4* dst = x_perm + row * vec_per_row;
-    for (int64_t v0 = lane; v0 < vec_per_row; v0 += 256) {
-      uint4 a[4];
+  const uint32_t row_bytes = (uint32_t)(vec_per_row * 16);
+  for (int64_t r0 = wave * kRowsPerWave; r0 < N; r0 += nwaves * kRowsPerWave) {
+    int64_t mine = -1;
+    if (lane < kRowsPerWave && r0 + lane < N) {
+      const int64_t p = row_to_pair[r0 + lane];
+      if (p >= 0 && p < npairs) mine = p / K;  // never invalid when the maps are consistent
+    }
+    int64_t tok[kRowsPerWave];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (v0 + u * 64 < vec_per_row) a[u] = src[v0 + u * 64];
+    for (int r = 0; r < kRowsPerWave; ++r) tok[r] = uniform64(__shfl(mine, r, 64));
+    for (int64_t v0 = 0; v0 < vec_per_row; v0 += 64 * kVecPerLane) {
+      uint4 a[kRowsPerWave][kVecPerLane];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (v0 + u * 64 < vec_per_row) dst[v0 + u * 64] = a[u];
+      for (int r = 0; r < kRowsPerWave; ++r) {
+        const RowReader rd(tok[r] >= 0 ? (const void*)(x + tok[r] * vec_per_row) : (const void*)x,
+                           tok[r] >= 0 ? row_bytes : 0u);
+#pragma unroll
+        for (int u = 0; u < kVecPerLane; ++u) a[r][u] = rd.load((uint32_t)((v0 + u * 64 + lane) * 16));
+      }
+#pragma unroll
+      for (int r = 0; r < kRowsPerWave; ++r) {
+        if (tok[r] < 0) continue;
+#pragma unroll
+        for (int u = 0; u < kVecPerLane; ++u) {
+          const int64_t vi = v0 + u * 64 + lane;
+          if (vi < vec_per_row) x_perm[(r0 + r) * vec_per_row + vi] = a[r][u];
+        }
+      }
     }
   }
 }
@@ -322,8 +359,7 @@ struct Vec;
 template <>
 struct Vec<uint16_t> {
   static constexpr int N = 8;
-  __device__ static void load(const uint16_t* p, float* f) {
-    const uint4 v = *reinterpret_cast<const uint4*>(p);
+  __device__ static void widen(const uint4& v, float* f) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -348,12 +384,11 @@ struct Vec<uint16_t> {
 template <>
 struct Vec<float> {
   static constexpr int N = 4;
-  __device__ static void load(const float* p, float* f) {
-    const float4 v = *reinterpret_cast<const float4*>(p);
-    f[0] = v.x;
-    f[1] = v.y;
-    f[2] = v.z;
-    f[3] = v.w;
+  __device__ static void widen(const uint4& v, float* f) {
+    f[0] = __uint_as_float(v.x);
+    f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z);
+    f[3] = __uint_as_float(v.w);
   }
   template <int M>
   __device__ static void store(float* p, const float* f) {
@@ -362,11 +397,38 @@ struct Vec<float> {
   }
 };
 
-constexpr int kGatherChunk = 4;  // 16-byte vectors per lane per pass
+constexpr int kGatherChunk = 2;  // 16-byte vectors per lane per pass
+constexpr int kPairGroup = 4;    // pairs of a token whose rows are loaded together
+
+// The row and gate of the token's pairs: lane k < K holds pair k; `valid`
+// has bit k set when that pair was computed here.
+struct TokenPairs {
+  int row;
+  float gate;
+  uint64_t valid;
+};
+
+__device__ __forceinline__ TokenPairs token_pairs(const int32_t* __restrict__ pair_to_row,
+                                                  const float* __restrict__ gates, int64_t t, int K, int64_t n_cap) {
+  // K <= FOREMOE_MAX_TOPK = 64: one lane per pair
+  const int lane = threadIdx.x & 63;
+  TokenPairs tp;
+  tp.row = -1;
+  tp.gate = 1.0f;
+  const int k = lane;
+  if (k < K) {
+    const int r = pair_to_row[t * K + k];
+    if (r >= 0 && r < n_cap) tp.row = r;
+    if (gates) tp.gate = gates[t * K + k];
+  }
+  tp.valid = __ballot(tp.row >= 0);
+  return tp;
+}
 
 // ---------------------------------------------------------------------------
 // Step 5 (and the backward of step 3 with unit weights): one wavefront per
-// token, y[t] = sum_k g_k * Y[row_k] in ascending k, fp32 accumulation.
+// token, y[t] = sum_k g_k * Y[row_k] in ascending k, fp32 accumulation. The
+// rows of up to kPairGroup pairs are loaded together before accumulating.
 // ---------------------------------------------------------------------------
 template <typename Tin, typename Tout>
 __global__ __launch_bounds__(256) void combine_kernel(const Tin* __restrict__ y_perm, const int32_t* __restrict__ pair_to_row,
@@ -377,28 +439,47 @@ __global__ __launch_bounds__(256) void combine_kernel(const Tin* __restrict__ y_
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   const int nvec = d / VE;
+  const uint32_t row_bytes = (uint32_t)d * (uint32_t)sizeof(Tin);
   for (int64_t t = wave; t < T; t += nwaves) {
+    const TokenPairs tp = token_pairs(pair_to_row, gates, t, K, n_cap);
     for (int v0 = 0; v0 < nvec; v0 += 64 * kGatherChunk) {
       float acc[kGatherChunk][VE];
 #pragma unroll
       for (int u = 0; u < kGatherChunk; ++u)
 #pragma unroll
         for (int i = 0; i < VE; ++i) acc[u][i] = 0.f;
-      for (int k = 0; k < K; ++k) {
-        const int row = pair_to_row[t * K + k];
-        if (row < 0 || row >= n_cap) continue;
-        const float g = gates ? gates[t * K + k] : 1.0f;
-        const Tin* src = y_perm + (int64_t)row * d;
-        float v[kGatherChunk][VE];
+      uint64_t m = tp.valid;
+      while (m) {
+        int ks[kPairGroup];
+        int n = 0;
 #pragma unroll
-        for (int u = 0; u < kGatherChunk; ++u) {
-          const int vi = v0 + u * 64 + lane;
-          if (vi < nvec) Vec<Tin>::load(src + (int64_t)vi * VE, v[u]);
+        for (int q = 0; q < kPairGroup; ++q) {
+          ks[q] = m ? __builtin_ctzll(m) : -1;
+          if (m) {
+            m &= m - 1;
+            ++n;
+          }
+        }
+        uint4 raw[kPairGroup][kGatherChunk];
+#pragma unroll
+        for (int q = 0; q < kPairGroup; ++q) {
+          const int row = __builtin_amdgcn_readfirstlane(q < n ? __shfl(tp.row, ks[q], 64) : 0);
+          const RowReader rd(y_perm + (int64_t)row * d, q < n ? row_bytes : 0u);
+#pragma unroll
+          for (int u = 0; u < kGatherChunk; ++u) raw[q][u] = rd.load((uint32_t)((v0 + u * 64 + lane) * 16));
         }
 #pragma unroll
-        for (int u = 0; u < kGatherChunk; ++u)
+        for (int q = 0; q < kPairGroup; ++q) {
+          if (q >= n) break;
+          const float g = __shfl(tp.gate, ks[q], 64);
 #pragma unroll
-          for (int i = 0; i < VE; ++i) acc[u][i] += g * v[u][i];
+          for (int u = 0; u < kGatherChunk; ++u) {
+            float v[VE];
+            Vec<Tin>::widen(raw[q][u], v);
+#pragma unroll
+            for (int i = 0; i < VE; ++i) acc[u][i] += g * v[i];
+          }
+        }
       }
       Tout* dst = y + t * d;
 #pragma unroll
@@ -412,8 +493,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const Tin* __restrict__ y_
 
 // ---------------------------------------------------------------------------
 // Backward of step 5: one wavefront per token; for each local pair write
-// dY[row] = g * dy[t] and dgates[p] = <dy[t], Y[row]> (deterministic
-// butterfly reduction); dgates of non-local pairs = 0.
+// dY[row] = g * dy[t] and dgates[p] = <dy[t], Y[row]> (fixed-order butterfly
+// and chunk sums); dgates of non-local pairs = 0. dy[t] is loaded once per
+// column chunk, the rows of up to kPairGroup pairs together.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(const T* __restrict__ dy, const T* __restrict__ y_perm,
@@ -425,44 +507,71 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const T* __restrict__ 
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   const int nvec = d / VE;
+  const uint32_t row_bytes = (uint32_t)d * (uint32_t)sizeof(T);
   for (int64_t t = wave; t < Ttok; t += nwaves) {
     const T* dyt = dy + t * d;
-    for (int k = 0; k < K; ++k) {
-      const int64_t p = t * K + k;
-      const int row = pair_to_row[p];
-      if (row < 0 || row >= n_cap) {
-        if (dgates && lane == 0) dgates[p] = 0.f;
-        continue;
-      }
-      const float g = gates[p];
-      float part = 0.f;
-      for (int v0 = 0; v0 < nvec; v0 += 64 * kGatherChunk) {
-        float a[kGatherChunk][VE], b[kGatherChunk][VE];
+    {
+      const TokenPairs tp = token_pairs(pair_to_row, gates, t, K, n_cap);
+      // pairs not computed here get a zero gate gradient
+      if (dgates && lane < K && tp.row < 0) dgates[t * K + lane] = 0.f;
+      uint64_t m = tp.valid;
+      while (m) {
+        int ks[kPairGroup];
+        int n = 0;
 #pragma unroll
-        for (int u = 0; u < kGatherChunk; ++u) {
-          const int vi = v0 + u * 64 + lane;
-          if (vi < nvec) {
-            Vec<T>::load(dyt + (int64_t)vi * VE, a[u]);
-            if (dgates) Vec<T>::load(y_perm + (int64_t)row * d + (int64_t)vi * VE, b[u]);
+        for (int q = 0; q < kPairGroup; ++q) {
+          ks[q] = m ? __builtin_ctzll(m) : -1;
+          if (m) {
+            m &= m - 1;
+            ++n;
           }
         }
+        int rows[kPairGroup];
+        float gs[kPairGroup], part[kPairGroup];
 #pragma unroll
-        for (int u = 0; u < kGatherChunk; ++u) {
-          const int vi = v0 + u * 64 + lane;
-          if (vi < nvec) {
-            float o[VE];
+        for (int q = 0; q < kPairGroup; ++q) {
+          rows[q] = __builtin_amdgcn_readfirstlane(q < n ? __shfl(tp.row, ks[q], 64) : 0);
+          gs[q] = q < n ? __shfl(tp.gate, ks[q], 64) : 0.f;
+          part[q] = 0.f;
+        }
+        const RowReader rdy(dyt, row_bytes);
+        for (int v0 = 0; v0 < nvec; v0 += 64 * kGatherChunk) {
+          uint4 ra[kGatherChunk];
+          uint4 rb[kPairGroup][kGatherChunk];
 #pragma unroll
-            for (int i = 0; i < VE; ++i) {
-              o[i] = g * a[u][i];
-              if (dgates) part += a[u][i] * b[u][i];
+          for (int u = 0; u < kGatherChunk; ++u) ra[u] = rdy.load((uint32_t)((v0 + u * 64 + lane) * 16));
+#pragma unroll
+          for (int q = 0; q < kPairGroup; ++q) {
+            const RowReader rd(y_perm + (int64_t)rows[q] * d, (dgates && q < n) ? row_bytes : 0u);
+#pragma unroll
+            for (int u = 0; u < kGatherChunk; ++u) rb[q][u] = rd.load((uint32_t)((v0 + u * 64 + lane) * 16));
+          }
+#pragma unroll
+          for (int q = 0; q < kPairGroup; ++q) {
+            if (q >= n) break;
+#pragma unroll
+            for (int u = 0; u < kGatherChunk; ++u) {
+              const int vi = v0 + u * 64 + lane;
+              float a[VE], b[VE], o[VE];
+              Vec<T>::widen(ra[u], a);
+              Vec<T>::widen(rb[q][u], b);
+#pragma unroll
+              for (int i = 0; i < VE; ++i) {
+                o[i] = gs[q] * a[i];
+                part[q] += a[i] * b[i];
+              }
+              if (vi < nvec) Vec<T>::template store<VE>(dy_perm + (int64_t)rows[q] * d + (int64_t)vi * VE, o);
             }
-            Vec<T>::template store<VE>(dy_perm + (int64_t)row * d + (int64_t)vi * VE, o);
           }
         }
-      }
-      if (dgates) {
-        part = wave_sum(part);
-        if (lane == 0) dgates[p] = part;
+        if (dgates) {
+#pragma unroll
+          for (int q = 0; q < kPairGroup; ++q) {
+            if (q >= n) break;
+            const float s = wave_sum(part[q]);
+            if (lane == 0) dgates[t * K + ks[q]] = s;
+          }
+        }
       }
     }
   }

@@ -54,8 +54,9 @@ def test_workspace_size(lib):
     big = lib.foremoe_workspace_size(32768, 8, 256)
     assert big > small
     # status words, the replica->slot table, then [blocks][E+1] partial counts
-    assert big >= 256 + 4 * 1024 * 16 + 128 * 257 * 4
-    assert big - (256 + 4 * 1024 * 16 + 128 * 257 * 4) < 256
+    # (one block per 512 pairs)
+    assert big >= 256 + 4 * 1024 * 16 + 512 * 257 * 4
+    assert big - (256 + 4 * 1024 * 16 + 512 * 257 * 4) < 256
     assert lib.foremoe_workspace_size(-1, 2, 8) == 0
     assert lib.foremoe_workspace_size(10, 0, 8) == 0
     assert lib.foremoe_workspace_size(10, 2, 2000) == 0
