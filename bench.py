@@ -233,7 +233,7 @@ def main() -> int:
     roofline = {"bound": kd["bound"], "achieved": kd["achieved"],
                 "peak": round((acc.PEAK_BF16_DENSE_FLOPS / 1e12) if kd["bound"] == "mfma"
                               else acc.PEAK_HBM_BYTES_PER_S / 1e9, 1),
-                "unit": kd["unit"], "frac": kd["frac"], "traffic": None, "kernel": dom,
+                "unit": kd["unit"], "frac": kd["frac"], "traffic": measured_traffic(dom), "kernel": dom,
                 "avg_launch_us": round(per_launch_us, 2)}
 
     ffn = ["gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad"]
@@ -277,6 +277,27 @@ def main() -> int:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def measured_traffic(phase: str):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 counter
+    summary (FETCH_SIZE, WRITE_SIZE, each scaled by a calibration copy), or
+    None when no summary exists or the kernel source changed since then."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_qwen3_share.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    k = rec.get("kernels", {}).get(phase)
+    if not k:
+        return None
+    with open(os.path.join(ROOT, k["source"]), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != k["source_sha256"]:
+            return None
+    cal = rec["calibration"]
+    return round((k["fetch_kib_per_launch"] / cal["fetch_scale"] + k["write_kib_per_launch"] / cal["write_scale"])
+                 * 1024.0, 0)
 
 
 def cpu_baseline(w, budget_s: float = 10.0) -> dict:

@@ -37,7 +37,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 #define FM_ROWS_NS 4
 #endif
 #ifndef FM_ROWS_WGM
-#define FM_ROWS_WGM 2
+#define FM_ROWS_WGM 4
 #endif
 #ifndef FM_ROWS_WGN
 #define FM_ROWS_WGN 2
@@ -52,7 +52,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 #define FM_WG_WGM 2
 #endif
 #ifndef FM_WG_WGN
-#define FM_WG_WGN 2
+#define FM_WG_WGN 4
 #endif
 
 enum Epi { kEpiStore = 0, kEpiSwigluFwd = 1, kEpiSwigluBwd = 2 };
