@@ -31,10 +31,10 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 // Tile configurations (overridable at build time for tuning sweeps).
 #ifndef FM_ROWS_BK
-#define FM_ROWS_BK 32
+#define FM_ROWS_BK 64
 #endif
 #ifndef FM_ROWS_NS
-#define FM_ROWS_NS 4
+#define FM_ROWS_NS 2
 #endif
 #ifndef FM_ROWS_WGM
 #define FM_ROWS_WGM 4
@@ -43,10 +43,10 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 #define FM_ROWS_WGN 2
 #endif
 #ifndef FM_WG_BK
-#define FM_WG_BK 32
+#define FM_WG_BK 64
 #endif
 #ifndef FM_WG_NS
-#define FM_WG_NS 4
+#define FM_WG_NS 2
 #endif
 #ifndef FM_WG_WGM
 #define FM_WG_WGM 2
@@ -145,17 +145,19 @@ struct KTile {
     if constexpr (CPR == 8) return (r >> 1) & 7;
     else return (r >> 2) & 3;
   }
-  // rowoff(r): byte offset (in the buffer) of tile row r at k = 0; k0: first k.
+  // This lane's source offset in load i (0 <= i < PER_WAVE) of this
+  // wavefront's share of the tile, relative to the stage's first k; rowoff(r)
+  // is the byte offset of tile row r. Fixed for a whole tile: each stage
+  // moves the buffer resource instead.
   template <class RowOff>
-  __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, RowOff rowoff, int k0) {
+  __device__ __forceinline__ static uint32_t voff(RowOff rowoff, int i) {
     const int l = lane64(), w = wave_id();
-#pragma unroll
-    for (int i = 0; i < PER_WAVE; ++i) {
-      const int q = w + NW * i;
-      const int r = q * RPI + l / CPR;
-      const int c = (l % CPR) ^ swz(r);
-      dma16(rs, lds + q * 1024, rowoff(r) + (uint32_t)(k0 + c * 8) * 2u);
-    }
+    const int r = (w + NW * i) * RPI + l / CPR;
+    const int c = (l % CPR) ^ swz(r);
+    return rowoff(r) + (uint32_t)c * 16u;
+  }
+  __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, uint32_t voff, int i) {
+    dma16(rs, lds + (wave_id() + NW * i) * 1024, voff);
   }
   // MFMA operand for rows mn0..mn0+31 of the tile, k-step kk (16 k values):
   // lane l gets row mn0 + l % 32, k = 16 kk + 8 (l / 32) + 0..7. The swizzle
@@ -182,17 +184,18 @@ struct MTile {
   static constexpr int BYTES = ROWS * BK * 2;
   static_assert(NI % NW == 0 && KPI >= 1, "tile must split over the wavefronts");
   __device__ __forceinline__ static int swz(int k) { return 4 * (k & 3); }
-  // koff(k): byte offset of tile k-row k at the tile's first m/n.
+  // This lane's source offset in load i (0 <= i < PER_WAVE) of this
+  // wavefront's share of the tile; koff(k) is the byte offset of the tile's
+  // k-row k (relative to the stage's first k row) at the tile's first m/n.
   template <class KOff>
-  __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, KOff koff) {
+  __device__ __forceinline__ static uint32_t voff(KOff koff, int i) {
     const int l = lane64(), w = wave_id();
-#pragma unroll
-    for (int i = 0; i < PER_WAVE; ++i) {
-      const int q = w + NW * i;
-      const int k = q * KPI + (l * 16) / RB;
-      const int c = ((l * 16) % RB) / 16 ^ swz(k);
-      dma16(rs, lds + q * 1024, koff(k) + (uint32_t)c * 16u);
-    }
+    const int k = (w + NW * i) * KPI + (l * 16) / RB;
+    const int c = ((l * 16) % RB) / 16 ^ swz(k);
+    return koff(k) + (uint32_t)c * 16u;
+  }
+  __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, uint32_t voff, int i) {
+    dma16(rs, lds + (wave_id() + NW * i) * 1024, voff);
   }
   // Same operand layout as KTile::frag, assembled from two transpose reads:
   // in each 16-lane group g, lane i addresses 4 consecutive m/n of one k row
@@ -288,20 +291,30 @@ struct Core {
   // The MFMAs of one k-step from register set `set`, with the LDS reads of
   // the next k-step's fragments (if any) interleaved: one read after each of
   // the first MB + NB MFMAs, so the reads complete under the matrix work.
-  template <class AT, class BT, int BK>
+  // extra(q), q < NX, runs right after MFMA s when q < (s + 1) NX / (MB NB)
+  // and q >= s NX / (MB NB), evenly over the k-step: the loads
+  // of a later stage, spread over the k-step so that the address unit
+  // drains them while the matrix cores keep working.
+  template <class AT, class BT, int BK, int NX, class Extra>
   __device__ __forceinline__ void mfma_step(Frags& f, int set, bool prefetch, const char* nAs, const char* nBs,
-                                            const Offsets<AT, BT, BK>& o, int nkk) {
+                                            const Offsets<AT, BT, BK>& o, int nkk, Extra&& extra) {
+    constexpr int NM = MB * NB;
+    static_assert(NX >= 0 && NX <= NM, "loads per k-step");
 #pragma unroll
-    for (int s = 0; s < MB * NB; ++s) {
+    for (int s = 0; s < NM; ++s) {
       const int i = s / NB, j = s % NB;
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[set][j], f.a[set][i], acc[i][j], 0, 0, 0);
       if (prefetch && s < MB + NB) {
         if (s < MB) f.a[set ^ 1][s] = AT::frag(nAs, o.a[s], o.ka, nkk);
         else f.b[set ^ 1][s - MB] = BT::frag(nBs, o.b[s - MB], o.kb, nkk);
       }
+      if constexpr (NX > 0) {
+#pragma unroll
+        for (int q = s * NX / NM; q < (s + 1) * NX / NM; ++q) extra(q);
+      }
     }
 #pragma unroll
-    for (int s = 0; s < MB * NB; ++s) {
+    for (int s = 0; s < NM; ++s) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
       if (s < MB + NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
     }
@@ -326,67 +339,87 @@ struct Core {
 };
 
 // Wait for the loads of the stage about to be computed: `ahead` younger
-// stages (of `per` loads each) may stay in flight.
+// stages (of PER loads each) may stay in flight.
 template <int NS, int PER>
 __device__ __forceinline__ void wait_stage(int ahead) {
-  static_assert(NS >= 2 && NS <= 4, "stages");
+  static_assert(NS >= 2 && NS <= 4 && (NS - 1) * PER < 64, "stages");
   if constexpr (NS >= 4) {
+    if (ahead >= 3) {
+      wait_vm<3 * PER>();
+      return;
+    }
+  }
+  if constexpr (NS >= 3) {
     if (ahead >= 2) {
       wait_vm<2 * PER>();
       return;
     }
   }
-  if constexpr (NS >= 3) {
-    if (ahead >= 1) {
-      wait_vm<PER>();
-      return;
-    }
+  if (ahead >= 1) {
+    wait_vm<PER>();
+    return;
   }
   wait_vm<0>();
 }
 
 // ---------------------------------------------------------------------------
-// Software-pipelined K loop over an LDS ring of NS >= 3 stages.
+// Software-pipelined K loop over an LDS ring of NS >= 2 stages.
 //
 // Stage kt's first fragments are already in registers when iteration kt
-// starts. Before the last k-step of a stage, each wavefront waits for its own
-// loads of stage kt+1, the workgroup barrier publishes them (and retires all
-// reads of the stage kt-1 buffer), the loads of stage kt+NS-1 are issued into
-// that buffer, and the last k-step's MFMAs run while the next stage's first
-// fragments are read. issue(kt) issues the loads of stage kt; next() tells
-// whether more stages follow (stage count known up front: KT).
+// starts, and every later k-step's fragments are read one k-step ahead. So
+// when the last k-step of stage kt begins, every read of stage kt's buffer
+// has been issued: each wavefront waits for its own loads of stage kt+1, and
+// the workgroup barrier (which also retires all LDS reads) both publishes
+// stage kt+1 and frees stage kt's buffer. The loads of stage kt+NS go into
+// that buffer, spread over the MFMAs of the last k-step of stage kt and the
+// first k-step of stage kt+1 (issued in one burst, they would stall every
+// wavefront behind the address unit at once). issue(s, p) issues load p
+// (0 <= p < PER) of stage s; stages are issued in increasing s, each one
+// whole before the next; KT stages in all.
 // ---------------------------------------------------------------------------
 template <class CoreT, class AT, class BT, int BK, int NS, class Issue>
 __device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
                                                  const typename CoreT::template Offsets<AT, BT, BK>& o,
                                                  Issue&& issue) {
-  static_assert(NS >= 3, "the prefetch across the barrier needs three stages");
+  static_assert(BK % 32 == 0, "the last k-step's fragments must be read before the barrier");
   constexpr int KK = BK / 16;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
   constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
+  static_assert(PER % 2 == 0, "a stage's loads split over two k-steps");
+  constexpr int HALF = PER / 2;
   typename CoreT::Frags f;
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
-    if (s < KT) issue(s);
-  wait_stage<NS, PER>((NS - 2 < KT - 1 ? NS - 2 : KT - 1));
+  for (int s = 0; s < NS; ++s)
+    if (s < KT) {
+#pragma unroll
+      for (int p = 0; p < PER; ++p) issue(s, p);
+    }
+  wait_stage<NS, PER>((NS < KT ? NS : KT) - 1);
   __syncthreads();
   CoreT::template load_frags<AT, BT, BK>(f, 0, lds, lds + AT::BYTES, o, 0);
+  int pend = -1;  // stage whose second half of loads rides on the next k-step 0
   for (int kt = 0; kt < KT; ++kt) {
     const char* st = lds + (kt % NS) * STAGE;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int set = kk & 1;
-      if (kk < KK - 1) {
-        core.template mfma_step<AT, BT, BK>(f, set, true, st, st + AT::BYTES, o, kk + 1);
+      if (kk == 0 && kk < KK - 1) {
+        core.template mfma_step<AT, BT, BK, HALF>(f, set, true, st, st + AT::BYTES, o, kk + 1, [&](int q) {
+          if (pend >= 0) issue(pend, HALF + q);
+        });
+      } else if (kk < KK - 1) {
+        core.template mfma_step<AT, BT, BK, 0>(f, set, true, st, st + AT::BYTES, o, kk + 1, [](int) {});
       } else {
         if (kt + 1 < KT) {
-          const int last = kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1;
+          const int last = kt + NS - 1 < KT - 1 ? kt + NS - 1 : KT - 1;  // youngest stage issued
           wait_stage<NS, PER>(last - (kt + 1));
         }
         __syncthreads();
-        if (kt + NS - 1 < KT) issue(kt + NS - 1);
         const char* nst = lds + ((kt + 1) % NS) * STAGE;
-        core.template mfma_step<AT, BT, BK>(f, set, kt + 1 < KT, nst, nst + AT::BYTES, o, 0);
+        pend = kt + NS < KT ? kt + NS : -1;
+        core.template mfma_step<AT, BT, BK, HALF>(f, set, kt + 1 < KT, nst, nst + AT::BYTES, o, 0, [&](int q) {
+          if (pend >= 0) issue(pend, q);
+        });
       }
     }
   }
@@ -440,6 +473,200 @@ __device__ void build_slot_tiles(const int32_t* __restrict__ off, int S, int64_t
   __syncthreads();
 }
 
+// ---------------------------------------------------------------------------
+// Row-GEMM epilogue through LDS. The MFMA leaves each lane with 4-column
+// pieces of 32 different rows; stored directly, every store instruction
+// would touch 32 partly written lines. Instead each wavefront converts one
+// 32-row block at a time to bf16 in its own LDS region and reads it back as
+// whole row segments, 16 bytes per lane with consecutive lanes along a row,
+// so each store instruction writes complete 128-byte lines. The staged rows
+// are XOR-swizzled in 16-byte chunks so that the 8-byte writes of 32 rows
+// spread over the LDS banks.
+// ---------------------------------------------------------------------------
+template <int RB>  // bytes per staged row
+struct StagedRows {
+  static constexpr int CPR = RB / 16;                   // 16-byte chunks per row
+  static constexpr int RPB = RB >= 256 ? 1 : 256 / RB;  // rows per 256-byte bank cycle
+  static constexpr int RPI = 64 / CPR;                  // rows per wavefront instruction
+  static constexpr int NI = 32 / RPI;                   // instructions per 32-row block
+  static constexpr int BYTES = 32 * RB;
+  static_assert(CPR >= 1 && CPR <= 64 && 32 % RPI == 0, "staged row width");
+  __device__ __forceinline__ static uint32_t chunk(int r, int c) {
+    return (uint32_t)(r * RB + ((c ^ ((r / RPB) % CPR)) << 4));
+  }
+  // 4 consecutive values at column col (a multiple of 4) of row r
+  __device__ __forceinline__ static void put4(char* base, int r, int col, float v0, float v1, float v2, float v3) {
+    *reinterpret_cast<uint2*>(base + chunk(r, col >> 3) + ((col & 4) << 1)) =
+        make_uint2(pack_bf2(v0, v1), pack_bf2(v2, v3));
+  }
+  // the 16-byte chunk lane l reads back in instruction it: row, chunk index
+  __device__ __forceinline__ static int row_of(int it) { return it * RPI + lane64() / CPR; }
+  __device__ __forceinline__ static int col_of() { return lane64() % CPR; }
+  __device__ __forceinline__ static uint4 get(const char* base, int r, int c) {
+    return *reinterpret_cast<const uint4*>(base + chunk(r, c));
+  }
+};
+
+// fp32 staging (the SwiGLU backward keeps dH in fp32): RB bytes per row,
+// 16-byte chunks of 4 floats; lane l reads back 8 consecutive floats.
+template <int RB>
+struct StagedRowsF32 {
+  static constexpr int CPR = RB / 16;
+  static constexpr int LPR = CPR / 2;  // lanes per row in the read-back
+  static constexpr int RPI = 64 / LPR;
+  static constexpr int NI = 32 / RPI;
+  static constexpr int BYTES = 32 * RB;
+  static_assert(RB % 256 == 0 && LPR >= 1 && LPR <= 64 && 32 % RPI == 0, "staged row width");
+  __device__ __forceinline__ static uint32_t chunk(int r, int c) { return (uint32_t)(r * RB + ((c ^ (r % 16)) << 4)); }
+  __device__ __forceinline__ static void put4(char* base, int r, int col, float v0, float v1, float v2, float v3) {
+    *reinterpret_cast<float4*>(base + chunk(r, col >> 2)) = make_float4(v0, v1, v2, v3);
+  }
+  __device__ __forceinline__ static int row_of(int it) { return it * RPI + lane64() / LPR; }
+  __device__ __forceinline__ static int col_of() { return lane64() % LPR; }  // in units of 8 values
+  __device__ __forceinline__ static void get8(const char* base, int r, int c8, float* f) {
+    const float4 lo = *reinterpret_cast<const float4*>(base + chunk(r, 2 * c8));
+    const float4 hi = *reinterpret_cast<const float4*>(base + chunk(r, 2 * c8 + 1));
+    f[0] = lo.x; f[1] = lo.y; f[2] = lo.z; f[3] = lo.w;
+    f[4] = hi.x; f[5] = hi.y; f[6] = hi.z; f[7] = hi.w;
+  }
+};
+
+template <class CoreT, int EPI>
+struct EpiBytes {
+  // SwiGLU forward stages H, A and U (GW bf16 columns each), the backward
+  // WN fp32 columns, the plain store WN bf16 columns
+  static constexpr int PER_WAVE = EPI == kEpiSwigluFwd   ? 3 * StagedRows<CoreT::GW * 2>::BYTES
+                                  : EPI == kEpiSwigluBwd ? StagedRowsF32<CoreT::WN * 4>::BYTES
+                                                         : StagedRows<CoreT::WN * 2>::BYTES;
+};
+
+__device__ __forceinline__ void unpack8(uint4 v, float* f) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = bf2f(w[i] & 0xFFFFu);
+    f[2 * i + 1] = bf2f(w[i] >> 16);
+  }
+}
+
+__device__ __forceinline__ uint4 pack8(const float* f) {
+  return make_uint4(pack_bf2(f[0], f[1]), pack_bf2(f[2], f[3]), pack_bf2(f[4], f[5]), pack_bf2(f[6], f[7]));
+}
+
+// Writes this wave's output block: rows wrow0 .. wrow0 + WM - 1 (those below
+// rend), output columns n0 + wn * WN .. (SwiGLU forward: H columns
+// f0 + wn * GW ..). `ep` is the wave's private LDS region.
+template <class CoreT, int EPI>
+__device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& core, char* ep, int64_t wrow0,
+                                              int64_t rend, int n0, int f0, int wn) {
+  const int lane = lane64();
+  const int l32 = lane & 31, c4 = (lane >> 5) * 4;
+#pragma unroll
+  for (int i = 0; i < CoreT::MB; ++i) {
+    const int64_t prow0 = wrow0 + i * 32;
+    if (prow0 >= rend) break;
+    if constexpr (EPI == kEpiSwigluFwd) {
+      using SR = StagedRows<CoreT::GW * 2>;
+      constexpr int H = CoreT::NB / 2;
+      char* sh = ep;
+      char* sa = ep + SR::BYTES;
+      char* su = ep + 2 * SR::BYTES;
+#pragma unroll
+      for (int jj = 0; jj < H; ++jj)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = jj * 32 + g * 8 + c4;
+          float hv[4], av[4], uv[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            av[e] = core.acc[i][jj][g * 4 + e];
+            uv[e] = core.acc[i][jj + H][g * 4 + e];
+            hv[e] = silu_f(av[e]) * uv[e];
+          }
+          SR::put4(sh, l32, col, hv[0], hv[1], hv[2], hv[3]);
+          SR::put4(sa, l32, col, av[0], av[1], av[2], av[3]);
+          SR::put4(su, l32, col, uv[0], uv[1], uv[2], uv[3]);
+        }
+      const int fc = f0 + wn * CoreT::GW + SR::col_of() * 8;
+#pragma unroll
+      for (int it = 0; it < SR::NI; ++it) {
+        const int r = SR::row_of(it);
+        const int64_t row = prow0 + r;
+        const uint4 vh = SR::get(sh, r, SR::col_of());
+        const uint4 va = SR::get(sa, r, SR::col_of());
+        const uint4 vu = SR::get(su, r, SR::col_of());
+        if (row < rend) {
+          *reinterpret_cast<uint4*>(a.C + row * a.ldc + fc) = vh;
+          if (a.C2) {
+            *reinterpret_cast<uint4*>(a.C2 + row * a.ldc2 + fc) = va;
+            *reinterpret_cast<uint4*>(a.C2 + row * a.ldc2 + a.F + fc) = vu;
+          }
+        }
+      }
+    } else if constexpr (EPI == kEpiSwigluBwd) {
+      using SR = StagedRowsF32<CoreT::WN * 4>;
+      const int nc = n0 + wn * CoreT::WN + SR::col_of() * 8;
+      // saved A and U of the rows this lane stores, loaded before the staging
+      // so that their latency overlaps it
+      uint4 xa[SR::NI], xu[SR::NI];
+#pragma unroll
+      for (int it = 0; it < SR::NI; ++it) {
+        const int64_t row = prow0 + SR::row_of(it);
+        xa[it] = xu[it] = make_uint4(0, 0, 0, 0);
+        if (row < rend) {
+          xa[it] = *reinterpret_cast<const uint4*>(a.AU + row * a.ldau + nc);
+          xu[it] = *reinterpret_cast<const uint4*>(a.AU + row * a.ldau + a.F + nc);
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < CoreT::NB; ++jj)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int q = g * 4;
+          SR::put4(ep, l32, jj * 32 + g * 8 + c4, core.acc[i][jj][q], core.acc[i][jj][q + 1], core.acc[i][jj][q + 2],
+                   core.acc[i][jj][q + 3]);
+        }
+#pragma unroll
+      for (int it = 0; it < SR::NI; ++it) {
+        const int r = SR::row_of(it);
+        const int64_t row = prow0 + r;
+        // dH at columns nc .. nc + 7; saved A in [0, F), U in [F, 2F)
+        float dh[8], A8[8], U8[8], da[8], du[8];
+        SR::get8(ep, r, SR::col_of(), dh);
+        if (row >= rend) continue;
+        unpack8(xa[it], A8);
+        unpack8(xu[it], U8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float sg = 1.0f / (1.0f + __expf(-A8[e]));
+          da[e] = dh[e] * U8[e] * (sg + A8[e] * sg * (1.0f - sg));
+          du[e] = dh[e] * A8[e] * sg;
+        }
+        *reinterpret_cast<uint4*>(a.C + row * a.ldc + nc) = pack8(da);
+        *reinterpret_cast<uint4*>(a.C + row * a.ldc + a.F + nc) = pack8(du);
+      }
+    } else {
+      using SR = StagedRows<CoreT::WN * 2>;
+      const int nc = n0 + wn * CoreT::WN + SR::col_of() * 8;
+#pragma unroll
+      for (int jj = 0; jj < CoreT::NB; ++jj)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int q = g * 4;
+          SR::put4(ep, l32, jj * 32 + g * 8 + c4, core.acc[i][jj][q], core.acc[i][jj][q + 1], core.acc[i][jj][q + 2],
+                   core.acc[i][jj][q + 3]);
+        }
+#pragma unroll
+      for (int it = 0; it < SR::NI; ++it) {
+        const int r = SR::row_of(it);
+        const int64_t row = prow0 + r;
+        const uint4 v = SR::get(ep, r, SR::col_of());
+        if (row < rend) *reinterpret_cast<uint4*>(a.C + row * a.ldc + nc) = v;
+      }
+    }
+  }
+}
+
 template <int BM, int BN, int BK, int NS, int WGM, int WGN, bool B_KMAJ, int EPI>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   constexpr bool SW = (EPI == kEpiSwigluFwd);
@@ -448,7 +675,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   using AT = KTile<BM, BK, NW>;
   using BT = typename std::conditional<B_KMAJ, KTile<BN, BK, NW>, MTile<BN, BK, NW>>::type;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
-  constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
   __shared__ int s_mt[FOREMOE_MAX_SLOTS + 1];
   __shared__ int s_tmp[16];
@@ -456,7 +682,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   build_slot_tiles<BM>(a.slot_offset, a.S, a.n_cap, s_mt, s_tmp);
   const int n_tiles = a.N / BN;
   const int total = s_mt[a.S] * n_tiles;
-  const int lane = lane64(), wave = wave_id();
+  const int wave = wave_id();
   const int wm = wave / WGN, wn = wave % WGN;
   const int KT = a.K / BK;
   const uint32_t lds0 = lds_addr(lds);
@@ -483,121 +709,55 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     const int n0 = nt * BN;           // first output column of the tile grid
     const int f0 = nt * (BN / 2);     // SwiGLU: first H column
 
-    // operand A: the slot's rows only (rows past the slot read as zero)
-    const i32x4 rsa = buf_rsrc(a.A + rbeg * a.lda, (uint32_t)((rend - rbeg) * a.lda * 2));
-    const uint32_t lda2 = (uint32_t)(a.lda * 2);
-    auto arow = [&](int r) -> uint32_t { return (uint32_t)(mrel + r) * lda2; };
-    // operand B: weight matrix w
-    const i32x4 rsb = buf_rsrc(a.B + (int64_t)w * a.wstride, (uint32_t)(a.wstride * 2));
-    const uint32_t ldb2 = (uint32_t)(a.ldb * 2);
-    auto brow = [&](int r) -> uint32_t {
-      int wr;
-      if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
-      else wr = n0 + r;
-      return (uint32_t)wr * ldb2;
-    };
-    auto issue = [&](int kt) {
-      const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
-      AT::issue(rsa, sa, arow, kt * BK);
+    // operand A: the slot's rows only (rows past the slot read as zero);
+    // operand B: weight matrix w. Lane offsets are fixed for the tile; each
+    // stage moves the start of the buffer resource to its first k, so the
+    // range check still ends at the slot's last row.
+    const uint32_t lda2 = (uint32_t)(a.lda * 2), ldb2 = (uint32_t)(a.ldb * 2);
+    const uint16_t* abase = a.A + rbeg * a.lda;
+    const uint32_t abytes = (uint32_t)((rend - rbeg) * a.lda * 2);
+    const uint16_t* bbase = a.B + (int64_t)w * a.wstride;
+    const uint32_t bbytes = (uint32_t)(a.wstride * 2);
+    uint32_t va[AT::PER_WAVE], vb[BT::PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < AT::PER_WAVE; ++i)
+      va[i] = AT::voff([&](int r) -> uint32_t { return (uint32_t)(mrel + r) * lda2; }, i);
+#pragma unroll
+    for (int i = 0; i < BT::PER_WAVE; ++i) {
       if constexpr (B_KMAJ) {
-        BT::issue(rsb, sa + AT::BYTES, brow, kt * BK);
+        vb[i] = BT::voff(
+            [&](int r) -> uint32_t {
+              int wr;
+              if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
+              else wr = n0 + r;
+              return (uint32_t)wr * ldb2;
+            },
+            i);
       } else {
         // K-major weights: element (n, k) at (k * ldb + n) * 2
-        BT::issue(rsb, sa + AT::BYTES,
-                  [&](int k) -> uint32_t { return (uint32_t)(kt * BK + k) * ldb2 + (uint32_t)n0 * 2u; });
+        vb[i] = BT::voff([&](int k) -> uint32_t { return (uint32_t)k * ldb2 + (uint32_t)n0 * 2u; }, i);
+      }
+    }
+    auto issue = [&](int kt, int p) {
+      const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
+      const uint32_t k0 = (uint32_t)(kt * BK);
+      if (p < AT::PER_WAVE) {
+        AT::issue(buf_rsrc(abase + k0, abytes - 2u * k0), sa, va[p], p);
+      } else if constexpr (B_KMAJ) {
+        BT::issue(buf_rsrc(bbase + k0, bbytes - 2u * k0), sa + AT::BYTES, vb[p - AT::PER_WAVE], p - AT::PER_WAVE);
+      } else {
+        BT::issue(buf_rsrc(bbase + (int64_t)k0 * a.ldb, bbytes - k0 * ldb2), sa + AT::BYTES, vb[p - AT::PER_WAVE],
+                  p - AT::PER_WAVE);
       }
     };
 
     core.zero();
-    if constexpr (NS >= 3 && BK % 32 == 0) {
-      pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
-    } else {
-#pragma unroll
-      for (int s = 0; s < NS - 1; ++s)
-        if (s < KT) issue(s);
-      for (int kt = 0; kt < KT; ++kt) {
-        const int ahead = (kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1) - kt;
-        wait_stage<NS, PER>(ahead);
-        __syncthreads();
-        if (kt + NS - 1 < KT) issue(kt + NS - 1);
-        const char* st = lds + (kt % NS) * STAGE;
-        core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
-      }
-    }
-    __syncthreads();  // all reads of this tile's stages done before the next tile's loads
-
-    // ---------------- epilogue ----------------
-    const int l32 = lane & 31, c4 = (lane >> 5) * 4;
-#pragma unroll
-    for (int i = 0; i < CoreT::MB; ++i) {
-      const int64_t row = m0 + wm * CoreT::WM + i * 32 + l32;
-      if (row >= rend) continue;
-      if constexpr (EPI == kEpiSwigluFwd) {
-        constexpr int H = CoreT::NB / 2;
-#pragma unroll
-        for (int jj = 0; jj < H; ++jj) {
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int f = f0 + wn * CoreT::GW + jj * 32 + g * 8 + c4;
-            float hv[4], av[4], uv[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              av[e] = core.acc[i][jj][g * 4 + e];
-              uv[e] = core.acc[i][jj + H][g * 4 + e];
-              hv[e] = silu_f(av[e]) * uv[e];
-            }
-            *reinterpret_cast<uint2*>(a.C + row * a.ldc + f) = make_uint2(pack_bf2(hv[0], hv[1]), pack_bf2(hv[2], hv[3]));
-            if (a.C2) {
-              *reinterpret_cast<uint2*>(a.C2 + row * a.ldc2 + f) =
-                  make_uint2(pack_bf2(av[0], av[1]), pack_bf2(av[2], av[3]));
-              *reinterpret_cast<uint2*>(a.C2 + row * a.ldc2 + a.F + f) =
-                  make_uint2(pack_bf2(uv[0], uv[1]), pack_bf2(uv[2], uv[3]));
-            }
-          }
-        }
-      } else {
-        [[maybe_unused]] uint2 ra[CoreT::NB][4], ru[CoreT::NB][4];
-        if constexpr (EPI == kEpiSwigluBwd) {
-          // all saved-activation loads of this row block first
-#pragma unroll
-          for (int jj = 0; jj < CoreT::NB; ++jj)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const int n = n0 + wn * CoreT::WN + jj * 32 + g * 8 + c4;
-              ra[jj][g] = *reinterpret_cast<const uint2*>(a.AU + row * a.ldau + n);
-              ru[jj][g] = *reinterpret_cast<const uint2*>(a.AU + row * a.ldau + a.F + n);
-            }
-        }
-#pragma unroll
-        for (int jj = 0; jj < CoreT::NB; ++jj) {
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int n = n0 + wn * CoreT::WN + jj * 32 + g * 8 + c4;
-            float v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = core.acc[i][jj][g * 4 + e];
-            if constexpr (EPI == kEpiSwigluBwd) {
-              // v = dH at columns f = n..n+3; saved A in [0, F), U in [F, 2F)
-              const uint2 xa = ra[jj][g], xu = ru[jj][g];
-              const float A4[4] = {bf2f(xa.x & 0xFFFF), bf2f(xa.x >> 16), bf2f(xa.y & 0xFFFF), bf2f(xa.y >> 16)};
-              const float U4[4] = {bf2f(xu.x & 0xFFFF), bf2f(xu.x >> 16), bf2f(xu.y & 0xFFFF), bf2f(xu.y >> 16)};
-              float da[4], du[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float sg = 1.0f / (1.0f + __expf(-A4[e]));
-                da[e] = v[e] * U4[e] * (sg + A4[e] * sg * (1.0f - sg));
-                du[e] = v[e] * A4[e] * sg;
-              }
-              *reinterpret_cast<uint2*>(a.C + row * a.ldc + n) = make_uint2(pack_bf2(da[0], da[1]), pack_bf2(da[2], da[3]));
-              *reinterpret_cast<uint2*>(a.C + row * a.ldc + a.F + n) =
-                  make_uint2(pack_bf2(du[0], du[1]), pack_bf2(du[2], du[3]));
-            } else {
-              *reinterpret_cast<uint2*>(a.C + row * a.ldc + n) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
-            }
-          }
-        }
-      }
-    }
+    pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
+    static_assert(NW * EpiBytes<CoreT, EPI>::PER_WAVE <= NS * STAGE, "epilogue staging must fit in the ring");
+    __syncthreads();  // every wave is done reading the ring: it now stages the epilogue
+    rows_epilogue<CoreT, EPI>(a, core, lds + wave * EpiBytes<CoreT, EPI>::PER_WAVE, m0 + wm * CoreT::WM, rend, n0,
+                              f0, wn);
+    __syncthreads();  // staging reads done before the next tile's loads overwrite the ring
   }
 }
 
@@ -795,34 +955,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
     for (KCursor cc = cursor_begin(P, S, g, s0, s1); !cc.done; cursor_next_slot(P, S, g, s1, cc))
       KT += (cc.hi - cc.lo + BK - 1) / BK;
     KCursor ic = cursor_begin(P, S, g, s0, s1);
-    auto issue = [&](int kt) {
-      // called once per k-tile, in order: load the cursor's tile, then advance
+    uint32_t va[AT::PER_WAVE], vb[BT::PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < AT::PER_WAVE; ++i)
+      va[i] = AT::voff([&](int k) -> uint32_t { return (uint32_t)k * lda2 + (uint32_t)m0 * 2u; }, i);
+#pragma unroll
+    for (int i = 0; i < BT::PER_WAVE; ++i)
+      vb[i] = BT::voff([&](int k) -> uint32_t { return (uint32_t)k * ldb2 + (uint32_t)n0 * 2u; }, i);
+    auto issue = [&](int kt, int p) {
+      // the loads of one k-tile are issued in order p = 0 .. PER-1, k-tiles
+      // in order: load the cursor's k-tile, advance after its last load. The
+      // resource starts at the k-tile's first row and ends at the segment's
+      // last, so rows past the segment read as zero.
       const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
-      // the segment's rows [lo, hi): rows past hi read as zero
-      const i32x4 rsa = buf_rsrc(a.A + (int64_t)ic.lo * a.lda, (uint32_t)(ic.hi - ic.lo) * lda2);
-      const i32x4 rsb = buf_rsrc(a.B + (int64_t)ic.lo * a.ldb, (uint32_t)(ic.hi - ic.lo) * ldb2);
-      const int kr = ic.k - ic.lo;
-      AT::issue(rsa, sa, [&](int k) -> uint32_t { return (uint32_t)(kr + k) * lda2 + (uint32_t)m0 * 2u; });
-      BT::issue(rsb, sa + AT::BYTES,
-                [&](int k) -> uint32_t { return (uint32_t)(kr + k) * ldb2 + (uint32_t)n0 * 2u; });
-      cursor_advance<BK>(P, S, g, s1, ic);
+      const uint32_t nrow = (uint32_t)(ic.hi - ic.k);
+      if (p < AT::PER_WAVE) {
+        AT::issue(buf_rsrc(a.A + (int64_t)ic.k * a.lda, nrow * lda2), sa, va[p], p);
+      } else {
+        BT::issue(buf_rsrc(a.B + (int64_t)ic.k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb[p - AT::PER_WAVE],
+                  p - AT::PER_WAVE);
+      }
+      if (p == AT::PER_WAVE + BT::PER_WAVE - 1) cursor_advance<BK>(P, S, g, s1, ic);
     };
 
     core.zero();
-    if constexpr (NS >= 3 && BK % 32 == 0) {
-      pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
-    } else {
-#pragma unroll
-      for (int s = 0; s < NS - 1; ++s)
-        if (s < KT) issue(s);
-      for (int kt = 0; kt < KT; ++kt) {
-        wait_stage<NS, PER>((kt + NS - 2 < KT - 1 ? kt + NS - 2 : KT - 1) - kt);
-        __syncthreads();
-        if (kt + NS - 1 < KT) issue(kt + NS - 1);
-        const char* st = lds + (kt % NS) * STAGE;
-        core.template compute<AT, BT, BK>(st, st + AT::BYTES, offs);
-      }
-    }
+    pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
     __syncthreads();
 
     const int l32 = lane & 31, c4 = (lane >> 5) * 4;
