@@ -46,16 +46,35 @@ def parse():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run three plain 1 GiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_calibration() -> int:
+    """Three device copies of 1 GiB: a kernel whose HBM bytes are known, so
+    that FETCH_SIZE / WRITE_SIZE counter readings can be scaled to bytes."""
+    import torch
+    x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    x.fill_(1)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print("copied 3 x 1 GiB", flush=True)
+    return 0
 
 
 def main() -> int:
     args = parse()
+    if args.copy_calibration:
+        return copy_calibration()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU's share of the expert layer; --gpus {args.gpus} "
               f"(WORLD_SIZE={world}) is not supported: the multi-GPU path (EP All-to-All over xGMI) "
-              "is not part of this build", file=sys.stderr)
+              "is not implemented here", file=sys.stderr)
         return 2
 
     import numpy as np

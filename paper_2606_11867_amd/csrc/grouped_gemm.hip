@@ -54,6 +54,10 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 #ifndef FM_WG_WGN
 #define FM_WG_WGN 4
 #endif
+// k-steps over which one stage's loads are spread (capped at the k-steps of a stage)
+#ifndef FM_LOAD_SPREAD
+#define FM_LOAD_SPREAD 2
+#endif
 
 enum Epi { kEpiStore = 0, kEpiSwigluFwd = 1, kEpiSwigluBwd = 2 };
 
@@ -372,11 +376,22 @@ __device__ __forceinline__ void wait_stage(int ahead) {
 // the workgroup barrier (which also retires all LDS reads) both publishes
 // stage kt+1 and frees stage kt's buffer. The loads of stage kt+NS go into
 // that buffer, spread over the MFMAs of the last k-step of stage kt and the
-// first k-step of stage kt+1 (issued in one burst, they would stall every
+// first k-steps of stage kt+1 (issued in one burst, they would stall every
 // wavefront behind the address unit at once). issue(s, p) issues load p
-// (0 <= p < PER) of stage s; stages are issued in increasing s, each one
-// whole before the next; KT stages in all.
+// (0 <= p < PER) of stage s, in increasing s, each stage whole before the
+// next. Stages s >= KT must issue loads of nothing (zero-size buffer
+// resources, which still write zeros to their LDS stage): every iteration
+// then issues the same loads, with no branch among the MFMAs, and the
+// counter waits stay exact.
 // ---------------------------------------------------------------------------
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 template <class CoreT, class AT, class BT, int BK, int NS, class Issue>
 __device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
                                                  const typename CoreT::template Offsets<AT, BT, BK>& o,
@@ -385,44 +400,44 @@ __device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
   constexpr int KK = BK / 16;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
   constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
-  static_assert(PER % 2 == 0, "a stage's loads split over two k-steps");
-  constexpr int HALF = PER / 2;
+  // the loads of a stage ride on SPREAD k-steps: the last one of the stage
+  // before and the first SPREAD - 1 of the next; load p goes with k-step
+  // j when lo(j) <= p < lo(j + 1)
+  constexpr int SPREAD = FM_LOAD_SPREAD < KK ? FM_LOAD_SPREAD : KK;
+  static_assert(SPREAD >= 1, "load spread");
+  auto lo = [](int j) constexpr { return j * PER / SPREAD; };
   typename CoreT::Frags f;
+  // stages 0 .. NS-2 whole, and the part of stage NS-1 that a previous
+  // iteration's last k-step would have carried
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
-    if (s < KT) {
+  for (int s = 0; s < NS; ++s) {
 #pragma unroll
-      for (int p = 0; p < PER; ++p) issue(s, p);
-    }
-  wait_stage<NS, PER>((NS < KT ? NS : KT) - 1);
+    for (int p = 0; p < (s < NS - 1 ? PER : lo(1)); ++p) issue(s, p);
+  }
+  wait_vm<(NS - 2) * PER + lo(1)>();
   __syncthreads();
   CoreT::template load_frags<AT, BT, BK>(f, 0, lds, lds + AT::BYTES, o, 0);
-  int pend = -1;  // stage whose second half of loads rides on the next k-step 0
   for (int kt = 0; kt < KT; ++kt) {
     const char* st = lds + (kt % NS) * STAGE;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int set = kk & 1;
-      if (kk == 0 && kk < KK - 1) {
-        core.template mfma_step<AT, BT, BK, HALF>(f, set, true, st, st + AT::BYTES, o, kk + 1, [&](int q) {
-          if (pend >= 0) issue(pend, HALF + q);
-        });
-      } else if (kk < KK - 1) {
-        core.template mfma_step<AT, BT, BK, 0>(f, set, true, st, st + AT::BYTES, o, kk + 1, [](int) {});
+    static_for<0, KK>([&](auto kkc) {
+      constexpr int kk = decltype(kkc)::value;
+      constexpr int set = kk & 1;
+      if constexpr (kk < KK - 1) {
+        constexpr int j = kk + 1;  // position in the load window of stage kt - 1 + NS
+        core.template mfma_step<AT, BT, BK, (j < SPREAD ? lo(j + 1) - lo(j) : 0)>(
+            f, set, true, st, st + AT::BYTES, o, kk + 1, [&](int q) { issue(kt - 1 + NS, lo(j) + q); });
       } else {
-        if (kt + 1 < KT) {
-          const int last = kt + NS - 1 < KT - 1 ? kt + NS - 1 : KT - 1;  // youngest stage issued
-          wait_stage<NS, PER>(last - (kt + 1));
-        }
+        wait_stage<NS, PER>(NS - 2);  // stage kt+1 (past the last: empty) has landed
         __syncthreads();
         const char* nst = lds + ((kt + 1) % NS) * STAGE;
-        pend = kt + NS < KT ? kt + NS : -1;
-        core.template mfma_step<AT, BT, BK, HALF>(f, set, kt + 1 < KT, nst, nst + AT::BYTES, o, 0, [&](int q) {
-          if (pend >= 0) issue(pend, q);
-        });
+        // (after the last stage this reads a stale buffer: harmless, and no
+        // branch among the MFMAs)
+        core.template mfma_step<AT, BT, BK, lo(1)>(f, set, true, nst, nst + AT::BYTES, o, 0,
+                                                   [&](int q) { issue(kt + NS, q); });
       }
-    }
+    });
   }
+  wait_vm<0>();  // the (empty) loads of stages past the last have landed too
 }
 
 // ---------------------------------------------------------------------------
@@ -739,15 +754,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
       }
     }
     auto issue = [&](int kt, int p) {
+      // stages past the last load nothing (zero-size resources)
+      const bool live = kt < KT;
       const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
-      const uint32_t k0 = (uint32_t)(kt * BK);
+      const uint32_t k0 = live ? (uint32_t)(kt * BK) : 0u;
       if (p < AT::PER_WAVE) {
-        AT::issue(buf_rsrc(abase + k0, abytes - 2u * k0), sa, va[p], p);
+        AT::issue(buf_rsrc(abase + k0, live ? abytes - 2u * k0 : 0u), sa, va[p], p);
       } else if constexpr (B_KMAJ) {
-        BT::issue(buf_rsrc(bbase + k0, bbytes - 2u * k0), sa + AT::BYTES, vb[p - AT::PER_WAVE], p - AT::PER_WAVE);
-      } else {
-        BT::issue(buf_rsrc(bbase + (int64_t)k0 * a.ldb, bbytes - k0 * ldb2), sa + AT::BYTES, vb[p - AT::PER_WAVE],
+        BT::issue(buf_rsrc(bbase + k0, live ? bbytes - 2u * k0 : 0u), sa + AT::BYTES, vb[p - AT::PER_WAVE],
                   p - AT::PER_WAVE);
+      } else {
+        BT::issue(buf_rsrc(bbase + (int64_t)k0 * a.ldb, live ? bbytes - k0 * ldb2 : 0u), sa + AT::BYTES,
+                  vb[p - AT::PER_WAVE], p - AT::PER_WAVE);
       }
     };
 
@@ -966,16 +984,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
       // the loads of one k-tile are issued in order p = 0 .. PER-1, k-tiles
       // in order: load the cursor's k-tile, advance after its last load. The
       // resource starts at the k-tile's first row and ends at the segment's
-      // last, so rows past the segment read as zero.
+      // last, so rows past the segment read as zero; once the cursor is
+      // done, the stages past the last load nothing.
+      const bool live = !ic.done;
       const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
-      const uint32_t nrow = (uint32_t)(ic.hi - ic.k);
+      const int k = live ? ic.k : 0;
+      const uint32_t nrow = live ? (uint32_t)(ic.hi - ic.k) : 0u;
       if (p < AT::PER_WAVE) {
-        AT::issue(buf_rsrc(a.A + (int64_t)ic.k * a.lda, nrow * lda2), sa, va[p], p);
+        AT::issue(buf_rsrc(a.A + (int64_t)k * a.lda, nrow * lda2), sa, va[p], p);
       } else {
-        BT::issue(buf_rsrc(a.B + (int64_t)ic.k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb[p - AT::PER_WAVE],
+        BT::issue(buf_rsrc(a.B + (int64_t)k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb[p - AT::PER_WAVE],
                   p - AT::PER_WAVE);
       }
-      if (p == AT::PER_WAVE + BT::PER_WAVE - 1) cursor_advance<BK>(P, S, g, s1, ic);
+      if (p == AT::PER_WAVE + BT::PER_WAVE - 1 && live) cursor_advance<BK>(P, S, g, s1, ic);
     };
 
     core.zero();
