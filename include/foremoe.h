@@ -221,11 +221,15 @@ int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, 
  * summed over the rows of every slot j with slot_gidx[j] == g, in slot
  * order. ACCUMULATES (+=) into fp32 dw_gate_up [G, 2F, d] and
  * dw_down [G, d, F], so gradients add up over micro-steps.
- * ws, ws_bytes: optional device scratch for splitting one expert's rows over
- *   many workgroups (fp32 partial tiles, summed in a fixed order by a second
- *   kernel of the same call). foremoe_wgrad_workspace_size(d, F) bytes give
- *   the full split; NULL/0 runs without splitting (slower for skewed loads,
- *   same result). Calls sharing one ws must be ordered on one stream.
+ * ws, ws_bytes: optional device scratch, caller-owned: a 256-byte header of
+ *   work counters (workgroups take the next (tile, row chunk) item when they
+ *   are free), then fp32 partial tiles for splitting one expert's rows over
+ *   many workgroups, summed in a fixed order by a second kernel of the same
+ *   call. foremoe_wgrad_workspace_size(d, F) bytes give the full split. The
+ *   header must be zero-filled before the first call; every call leaves it
+ *   zero again (the rest needs no initialisation). NULL/0 runs with a fixed
+ *   item order and no split (slower for skewed loads, same result). Calls
+ *   sharing one ws must be ordered on one stream.
  * No float atomics: each output element's summation order is fixed, so the
  * result is deterministic. 1 <= G <= FOREMOE_MAX_SLOTS.
  * = foremoe_ffn_gate_up_wgrad then foremoe_ffn_down_wgrad (each one main

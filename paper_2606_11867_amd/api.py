@@ -164,9 +164,11 @@ def grouped_ffn_dgrad(dy_perm: torch.Tensor, save_au: torch.Tensor, slot_offset:
 
 
 def wgrad_workspace(d: int, F: int, device) -> torch.Tensor:
-    """Scratch for splitting hot experts' weight gradients over many CUs."""
+    """Scratch for scheduling and splitting the weight-gradient work over many
+    CUs. Zero-filled here, as its work-counter header must be before first
+    use; each call leaves that header zero again."""
     n = _lib.load().foremoe_wgrad_workspace_size(d, F)
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def grouped_ffn_wgrad(x_perm: torch.Tensor, h: torch.Tensor, dy_perm: torch.Tensor, d_au: torch.Tensor,

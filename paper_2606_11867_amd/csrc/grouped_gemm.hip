@@ -806,6 +806,9 @@ struct WgradArgs {
   int64_t gstride;
   float* part;  // partial tiles [p_max][BM * BN]
   int p_max;
+  // work counters {next item, finished workgroups} (zero on entry, zeroed
+  // again by the last workgroup), or NULL for a static item order
+  unsigned* sched;
 };
 
 struct WgradPlan {
@@ -952,7 +955,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
   CoreT core;
   const typename CoreT::template Offsets<AT, BT, BK> offs(wm, wn);
 
-  for (int t = xcd_virtual_id(); t < total; t += gridDim.x) {
+  // Items (output tile x row chunk) come in descending group size. With
+  // work counters each workgroup takes the next item when it is free, which
+  // balances the very uneven item sizes; without, a fixed stride (XCD-aware).
+  __shared__ int s_item;
+  auto next_item = [&](int prev) -> int {
+    if (!a.sched) return prev < 0 ? xcd_virtual_id() : prev + (int)gridDim.x;
+    if (threadIdx.x == 0) s_item = (int)atomicAdd(&a.sched[0], 1u);
+    __syncthreads();
+    return s_item;
+  };
+  for (int t = next_item(-1); t < total; t = next_item(t)) {
     int lo = 0, hi = P.nne - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -1075,6 +1088,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
       }
     }
     __syncthreads();  // the epilogue's LDS staging is done before the next item's loads
+  }
+  if (a.sched && threadIdx.x == 0) {
+    // each workgroup counts itself finished after its last take returned, so
+    // the last one to finish can zero the counters for the next call
+    if (atomicAdd(&a.sched[1], 1u) == gridDim.x - 1) {
+      atomicExch(&a.sched[0], 0u);
+      atomicExch(&a.sched[1], 0u);
+    }
   }
 }
 
@@ -1249,9 +1270,11 @@ void launch_rows(const RowsArgs& a, hipStream_t st) {
   }
 }
 
-// Partial-tile budget of the weight-gradient split (tiles of 256 x 256 fp32).
+// Weight-gradient workspace: a 256-byte header of work counters, then the
+// partial-tile budget of the split (tiles of 256 x 256 fp32).
+constexpr size_t kWgradHeaderBytes = 256;
 constexpr size_t kWgradPartialTiles = 256;
-constexpr size_t kWgradWorkspaceBytes = kWgradPartialTiles * 256 * 256 * 4;
+constexpr size_t kWgradWorkspaceBytes = kWgradHeaderBytes + kWgradPartialTiles * 256 * 256 * 4;
 
 }  // namespace
 }  // namespace foremoe
@@ -1471,16 +1494,20 @@ static int wgrad_common(const char* who, const void* A, int lda, const void* B, 
     a.C = dw;
     a.ldc = N;
     a.gstride = (int64_t)M * N;
-    a.part = (float*)ws;
+    // the workspace header holds the work counters; the rest partial tiles
+    const bool has_ws = ws && ws_bytes >= kWgradHeaderBytes;
+    a.sched = has_ws ? (unsigned*)ws : nullptr;
+    a.part = has_ws ? (float*)((char*)ws + kWgradHeaderBytes) : nullptr;
+    const size_t part_bytes = has_ws ? ws_bytes - kWgradHeaderBytes : 0;
     const dim3 grid(persistent_grid()), block(256);
     if (M % 256 == 0 && N % 256 == 0) {
       constexpr int WGM = FM_WG_WGM, WGN = FM_WG_WGN;
-      a.p_max = (int)(ws_bytes / (256 * 256 * 4));
+      a.p_max = (int)(part_bytes / (256 * 256 * 4));
       hipLaunchKernelGGL((gemm_wgrad_kernel<256, 256, FM_WG_BK, FM_WG_NS, WGM, WGN>), grid, dim3(64 * WGM * WGN), 0,
                          st, a);
       if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<256, 256, FM_WG_BK>), dim3(persistent_grid() * 4), block, 0, st, a);
     } else {
-      a.p_max = (int)(ws_bytes / (128 * 128 * 4));
+      a.p_max = (int)(part_bytes / (128 * 128 * 4));
       hipLaunchKernelGGL((gemm_wgrad_kernel<128, 128, 64, 3, 2, 2>), grid, block, 0, st, a);
       if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<128, 128, 64>), dim3(persistent_grid() * 4), block, 0, st, a);
     }

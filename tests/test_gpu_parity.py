@@ -241,16 +241,21 @@ def test_ffn_backward(gpu, name):
     start_dn = rng.standard_normal((G, w.spec.d, F)).astype(np.float32)
     rgu, rdn = O.ffn_wgrad(x_perm, hq, dy_perm, dau_q[:, :F], dau_q[:, F:], ref["slot_offset"], m.plan.slot_gidx, G,
                            start_gu.astype(np.float64), start_dn.astype(np.float64))
-    # without a workspace (one workgroup per output tile) and with the split over row chunks
-    for ws in (None, api.wgrad_workspace(w.spec.d, F, gpu)):
+    # without a workspace (fixed item order, one workgroup per output tile),
+    # with only the work-counter header (items taken as workgroups free up),
+    # and with the split over row chunks; the workspace is used by both
+    # weight-gradient calls, and the counters must be zero again after each
+    full = api.wgrad_workspace(w.spec.d, F, gpu)
+    for tag, ws in (("whole", None), ("counters", torch.zeros(256, dtype=torch.uint8, device=gpu)), ("split", full)):
         dwgu = torch.from_numpy(start_gu.copy()).to(gpu)
         dwdn = torch.from_numpy(start_dn.copy()).to(gpu)
         api.grouped_ffn_wgrad(to_dev(x_perm, dt, gpu), to_dev(hq, dt, gpu), to_dev(dy_perm, dt, gpu),
                               to_dev(dau_q, dt, gpu), so, gidx, dwgu, dwdn, ws=ws)
         torch.cuda.synchronize()
-        tag = "split" if ws is not None else "whole"
         check_close(f"dW_gate_up[{tag}]", to_np(dwgu), rgu)
         check_close(f"dW_down[{tag}]", to_np(dwdn), rdn)
+        if ws is not None:
+            assert not ws[:256].any().item(), f"{tag}: work counters not reset"
 
 
 # ---------------------------------------------------------------------------
