@@ -121,7 +121,7 @@ int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E,
                       int32_t* counts, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Step 2 (Sec. 7.2 token conservation; Sec. 8 Stage 4; App. E Stage 4).
+ * Step 2 (Sec. 7.2 token conservation; Sec. 8 Stage 4; App. D Stage 4).
  * For expert e with R_e replicas and weights w (equal if NULL), replica r
  * takes the contiguous block [B_r, B_{r+1}) of e's token list (ascending
  * pair index), B_r = floor(n_e * (w_0 + .. + w_{r-1}) / (w_0 + .. + w_{R_e-1})).

@@ -8,7 +8,7 @@ is sent to its top-K experts and the layer output is the router-probability
 weighted sum of those experts' outputs. ForeMoE's placement (Sec. 7) only
 changes *where* a (token, k) pair is computed: expert replicas hold the same
 weights, and the token-conservation and feasibility constraints of the MILP
-(Sec. 7.2, App. D) say that every pair of an expert is processed by exactly
+(Sec. 7.2, App. C) say that every pair of an expert is processed by exactly
 one slot that holds that expert. So the oracle is that definition written out
 step by step for one GPU's slots, in float64, with no blocking or fusion:
 
@@ -16,7 +16,7 @@ step by step for one GPU's slots, in float64, with no blocking or fusion:
                 Routing Collector; load w_{s,e} of Table 1);
 2. assign     - contiguous split of each expert's token list over its
                 replicas in the proportions of the token-assignment fractions
-                r_{s,e,j} (Sec. 7.2; Sec. 8 Stage 4; App. E Stage 4);
+                r_{s,e,j} (Sec. 7.2; Sec. 8 Stage 4; App. D Stage 4);
 3. permute    - gather tokens into slot-contiguous order;
 4. grouped FFN- SwiGLU expert with gate, up and down matrices (App. A,
                 Eq. flops_moe) per slot; backward by the chain rule, with the
@@ -64,7 +64,7 @@ def histogram(ids: np.ndarray, E: int) -> Tuple[np.ndarray, int]:
 
 
 # ----------------------------------------------------------------------------
-# Step 2: replica split (token conservation, Sec. 7.2 / App. D)
+# Step 2: replica split (token conservation, Sec. 7.2 / App. C)
 # ----------------------------------------------------------------------------
 def replica_bounds(n: int, weights: List[int]) -> List[int]:
     """Boundaries B[0..R] of the contiguous split of n tokens over R replicas.

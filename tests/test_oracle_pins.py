@@ -1,7 +1,7 @@
 """Pins of the fp64 oracle against facts fixed outside the oracle itself.
 
 Every check here is an independent formulation: brute force on tiny inputs,
-invariants of the MILP constraints (Sec. 7.2, App. D), a dense non-MoE
+invariants of the MILP constraints (Sec. 7.2, App. C), a dense non-MoE
 reference of the MoE layer (Sec. 2.1), a plain SwiGLU MLP written in pure
 Python (App. A), placement invariance, central finite differences of the
 backward, and the analytic numbers printed in App. A.4. Mutation tests plant
@@ -220,7 +220,7 @@ def test_permute_overflow_drops_tail():
 
 
 def test_every_pair_dispatched_once_over_all_ranks():
-    """Coverage + conservation over a whole EP group (App. D): simulate every
+    """Coverage + conservation over a whole EP group (App. C): simulate every
     rank's slot table; each valid pair lands on exactly one slot."""
     rng = np.random.default_rng(11)
     T, K, E, P = 64, 4, 16, 4
