@@ -283,6 +283,78 @@ int foremoe_permute_bwd(const void* dx_perm, foremoe_dtype in_dtype, const int32
                         int64_t T, int32_t K, int32_t d, int64_t n_cap, void* dx,
                         foremoe_dtype out_dtype, void* stream);
 
+/*
+ * Placement planner (host only: HOST arrays, no GPU work, synchronous).
+ * Produces the placement that the GPU steps consume, from the routing
+ * foreseen during rollout (Sec. 5). Ranks are numbered machine-major:
+ * rank r sits on machine r / R; P = M * R ranks, which are also the source
+ * ranks s of the load matrices (w[s, e] = tokens of source rank s routed to
+ * expert e, int32, row-major [P, E]).
+ *
+ *  M    machines, R ranks per machine (M * R <= 4096)
+ *  N_b  base slots per rank (E <= P * N_b), N_r redundant slots per rank
+ *
+ * Ties are broken the same way everywhere: lowest expert id, rank id or
+ * copy index among equals; all arithmetic is integer, so plans are exactly
+ * reproducible. Errors: FOREMOE_EINVAL with foremoe_last_error().
+ */
+typedef struct foremoe_machine {
+  int32_t M;
+  int32_t R;
+  int32_t N_b;
+  int32_t N_r;
+} foremoe_machine;
+
+/*
+ * Stage 1 (Sec. 8 Stage 1, Alg. 1): base rank of every expert from the
+ * step's aggregate load w_agg [P, E]. Experts go, in descending aggregate
+ * load, to the machine with the least
+ *   c_load * (ML[m] + w_e) + c_traffic * (MC[m] + Delta_{m,e})
+ * (ML: load placed on m, MC: its inbound cross-machine tokens, Delta: tokens
+ * of e from other machines; c_load : c_traffic is n1*K1 : n2*K2 of the time
+ * model, Sec. 7.1, as integers in [0, 2^20]) that has a free base slot, then
+ * by LPT onto the machine's ranks (at most N_b each).
+ * base_rank [E] out.
+ */
+int foremoe_plan_base(const int32_t* w_agg, int32_t E, const foremoe_machine* mc, int64_t c_load,
+                      int64_t c_traffic, int32_t* base_rank);
+
+/*
+ * Policy-update Stages 2-4 (App. D, Alg. 3) for one micro-step with load
+ * w [P, E], per machine:
+ *   Stage 2  LPT of the machine's experts over its ranks by this load;
+ *   Stage 3  R * N_r times: a replica of the expert with the largest load
+ *            per copy onto the rank with the least load (copies sharing
+ *            their expert's load evenly) that has a free redundant slot and
+ *            no copy of that expert yet; stops when no rank qualifies;
+ *   Stage 4  water-filling: replicated experts in descending load, sources
+ *            in ascending order, every token unit to the copy whose rank
+ *            has the least accumulated load (Sec. 7.2 r_{s,e,j} x w_{s,e}).
+ * base_rank [E] in (Stage 1). C_max: copies per expert the outputs hold
+ * (error if a plan needs more).
+ * copy_rank [E, C_max] out: rank of copy c of expert e (copy 0 = the main
+ *   expert, Sec. 6.2), -1 past the last copy.
+ * counts [P, E, C_max] out: tokens of source s for expert e that copy c
+ *   processes (sum over c = w[s, e]).
+ * rank_load [P] out (may be NULL): tokens each rank processes.
+ */
+int foremoe_plan_micro_step(const int32_t* w, int32_t E, const foremoe_machine* mc,
+                            const int32_t* base_rank, int32_t C_max, int32_t* copy_rank,
+                            int32_t* counts, int64_t* rank_load);
+
+/*
+ * One rank's slot table from a micro-step plan (the arrays of foremoe_plan,
+ * on the host): main copies on `rank` first, then replica copies on it, each
+ * in ascending (expert, copy). slot_widx[j] is the index of slot j's expert
+ * in local_experts (order of first appearance; use it as slot_gidx too),
+ * expert_nrep[e] the copies of e in the whole group. Arrays hold max_slots
+ * slots and E experts; *S_out slots and *W_out local experts are written.
+ */
+int foremoe_plan_rank_slots(const int32_t* copy_rank, int32_t E, int32_t C_max, int32_t rank,
+                            int32_t max_slots, int32_t* slot_expert, int32_t* slot_replica,
+                            int32_t* slot_widx, int32_t* expert_nrep, int32_t* local_experts,
+                            int32_t* S_out, int32_t* W_out);
+
 /* Utilities (host only, no GPU work). */
 const char* foremoe_status_string(int status);
 const char* foremoe_last_error(void); /* message of this thread's last failed call */

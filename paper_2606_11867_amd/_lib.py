@@ -33,6 +33,13 @@ class Plan(ctypes.Structure):
 
 PPlan = ctypes.POINTER(Plan)
 
+
+class Machine(ctypes.Structure):
+    _fields_ = [("M", c_i32), ("R", c_i32), ("N_b", c_i32), ("N_r", c_i32)]
+
+
+PMachine = ctypes.POINTER(Machine)
+
 # name -> (restype, argtypes)
 SIGNATURES = {
     "foremoe_workspace_size": (c_sz, [c_i64, c_i32, c_i32]),
@@ -63,6 +70,9 @@ SIGNATURES = {
     "foremoe_combine_bwd": (ctypes.c_int, [c_p, c_p, c_i32, c_p, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_p,
                                            c_p]),
     "foremoe_permute_bwd": (ctypes.c_int, [c_p, c_i32, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_i32, c_p]),
+    "foremoe_plan_base": (ctypes.c_int, [c_p, c_i32, PMachine, c_i64, c_i64, c_p]),
+    "foremoe_plan_micro_step": (ctypes.c_int, [c_p, c_i32, PMachine, c_p, c_i32, c_p, c_p, c_p]),
+    "foremoe_plan_rank_slots": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p, c_p, c_p, c_p]),
     "foremoe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "foremoe_last_error": (ctypes.c_char_p, []),
     "foremoe_version": (ctypes.c_char_p, []),

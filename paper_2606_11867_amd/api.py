@@ -222,3 +222,65 @@ def permute_bwd(dx_perm: torch.Tensor, pair_to_row: torch.Tensor, T: int, K: int
                                           dx.data_ptr(), _DT[out_dtype], _stream(dx_perm.device)),
           "foremoe_permute_bwd")
     return dx
+
+
+# ---------------------------------------------------------------------------
+# Placement planner (host arrays; see include/foremoe.h)
+# ---------------------------------------------------------------------------
+def _machine(M: int, R: int, N_b: int, N_r: int) -> _lib.Machine:
+    return _lib.Machine(int(M), int(R), int(N_b), int(N_r))
+
+
+def _host_i32(a, shape=None) -> np.ndarray:
+    out = np.ascontiguousarray(a, dtype=np.int32)
+    if shape is not None and out.shape != tuple(shape):
+        raise ValueError(f"expected shape {tuple(shape)}, got {out.shape}")
+    return out
+
+
+def plan_base(w_agg: np.ndarray, M: int, R: int, N_b: int, c_load: int = 1, c_traffic: int = 0) -> np.ndarray:
+    """Stage 1: base rank [E] of every expert from the aggregate load [P, E]."""
+    w = _host_i32(w_agg)
+    P, E = w.shape
+    if P != M * R:
+        raise ValueError("w_agg must have M * R rows")
+    out = np.empty(E, dtype=np.int32)
+    mc = _machine(M, R, N_b, 0)
+    check(_lib.load().foremoe_plan_base(w.ctypes.data, E, ctypes.byref(mc), int(c_load), int(c_traffic),
+                                        out.ctypes.data), "foremoe_plan_base")
+    return out
+
+
+def plan_micro_step(w: np.ndarray, base_rank: np.ndarray, M: int, R: int, N_b: int, N_r: int, C_max: int):
+    """Stages 2-4 of one micro-step: (copy_rank [E, C_max], counts [P, E, C_max], rank_load [P])."""
+    w = _host_i32(w)
+    P, E = w.shape
+    if P != M * R:
+        raise ValueError("w must have M * R rows")
+    base = _host_i32(base_rank, (E,))
+    copy_rank = np.empty((E, C_max), dtype=np.int32)
+    counts = np.empty((P, E, C_max), dtype=np.int32)
+    rank_load = np.empty(P, dtype=np.int64)
+    mc = _machine(M, R, N_b, N_r)
+    check(_lib.load().foremoe_plan_micro_step(w.ctypes.data, E, ctypes.byref(mc), base.ctypes.data, int(C_max),
+                                              copy_rank.ctypes.data, counts.ctypes.data, rank_load.ctypes.data),
+          "foremoe_plan_micro_step")
+    return copy_rank, counts, rank_load
+
+
+def plan_rank_slots(copy_rank: np.ndarray, rank: int, max_slots: int = _lib.MAX_SLOTS) -> dict:
+    """One rank's slot table from a micro-step plan (host arrays)."""
+    cr = _host_i32(copy_rank)
+    E, C_max = cr.shape
+    se = np.empty(max_slots, dtype=np.int32)
+    sr = np.empty(max_slots, dtype=np.int32)
+    sw = np.empty(max_slots, dtype=np.int32)
+    nrep = np.empty(E, dtype=np.int32)
+    local = np.empty(E, dtype=np.int32)
+    S = ctypes.c_int32(0)
+    W = ctypes.c_int32(0)
+    check(_lib.load().foremoe_plan_rank_slots(cr.ctypes.data, E, C_max, int(rank), int(max_slots), se.ctypes.data,
+                                              sr.ctypes.data, sw.ctypes.data, nrep.ctypes.data, local.ctypes.data,
+                                              ctypes.byref(S), ctypes.byref(W)), "foremoe_plan_rank_slots")
+    return dict(slot_expert=se[:S.value].copy(), slot_replica=sr[:S.value].copy(), slot_widx=sw[:S.value].copy(),
+                expert_nrep=nrep, local_experts=local[:W.value].copy())
