@@ -114,6 +114,91 @@ def assign_replicas(counts: np.ndarray, plan) -> Tuple[np.ndarray, np.ndarray, n
 
 
 # ----------------------------------------------------------------------------
+# Steps 1-2 per source rank (Sec. 7.2: r_{s,e,j} is a fraction per source
+# rank s; App. D Stage 4 water-fills source by source)
+# ----------------------------------------------------------------------------
+# Reading: source rank s owns the contiguous tokens [tb[s], tb[s+1]) of the
+# micro-step; for each (s, e) the pairs of s routed to e, in ascending p,
+# are split over e's replicas by the weights of (s, e) with the same floor
+# rule as above; a replica's slot takes its blocks source by source, so the
+# rows of a slot stay in ascending p. All-zero weights are an error only
+# when (s, e) has pairs (a planner gives zero weights to empty pairs).
+def histogram_src(ids: np.ndarray, E: int, src_token_begin) -> np.ndarray:
+    """counts[s, e] = #pairs of tokens of source s with ids == e."""
+    ids = np.asarray(ids)
+    tb = [int(v) for v in src_token_begin]
+    out = np.zeros((len(tb) - 1, E), dtype=np.int32)
+    for s in range(len(tb) - 1):
+        out[s], _ = histogram(ids[tb[s]:tb[s + 1]], E)
+    return out
+
+
+def _src_weights(plan, s: int, e: int, R: int) -> List[int]:
+    if getattr(plan, "src_rep_weight", None) is not None:
+        return [int(v) for v in np.asarray(plan.src_rep_weight)[s, e, :R]]
+    if plan.expert_rep_weight is not None:
+        return [int(v) for v in np.asarray(plan.expert_rep_weight).reshape(plan.E, plan.R_max)[e, :R]]
+    return [1] * R
+
+
+def assign_replicas_src(counts_src: np.ndarray, plan) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Per-(source, expert) replica ranges and the local slots' counts/offsets.
+
+    Returns rep_begin int32 [n_src, E, R_max+1] (entries past R_e hold n_{s,e}),
+    slot_count int32 [S] (summed over sources) and slot_offset int32 [S+1].
+    """
+    counts_src = np.asarray(counts_src)
+    n_src, E = counts_src.shape
+    R_max = plan.R_max
+    rep_begin = np.zeros((n_src, E, R_max + 1), dtype=np.int64)
+    for s in range(n_src):
+        for e in range(E):
+            R = int(plan.expert_nrep[e])
+            n = int(counts_src[s, e])
+            w = _src_weights(plan, s, e, R)
+            b = replica_bounds(n, w) if sum(w) > 0 else replica_bounds(n, [1] * R)
+            rep_begin[s, e, : R + 1] = b
+            rep_begin[s, e, R + 1:] = n
+    slot_count = np.zeros(plan.S, dtype=np.int64)
+    for j in range(plan.S):
+        e, r = int(plan.slot_expert[j]), int(plan.slot_replica[j])
+        slot_count[j] = int(np.sum(rep_begin[:, e, r + 1] - rep_begin[:, e, r]))
+    slot_offset = np.zeros(plan.S + 1, dtype=np.int64)
+    for j in range(plan.S):
+        slot_offset[j + 1] = slot_offset[j] + slot_count[j]
+    return rep_begin.astype(np.int32), slot_count.astype(np.int32), slot_offset.astype(np.int32)
+
+
+def permute_src(x: np.ndarray, ids: np.ndarray, plan, rep_begin_src: np.ndarray, slot_offset: np.ndarray,
+                n_cap: int, src_token_begin):
+    """permute() with per-source replica ranges: slot j holds, source by
+    source, the pairs of its replica's block in each source's list."""
+    ids = np.asarray(ids)
+    T, K = ids.shape
+    tb = [int(v) for v in src_token_begin]
+    d = x.shape[1]
+    x_perm = np.zeros((n_cap, d), dtype=np.float64)
+    row_to_pair = np.full(n_cap, -1, dtype=np.int32)
+    pair_to_row = np.full(T * K, -1, dtype=np.int32)
+    dropped = 0
+    for j in range(plan.S):
+        e, r = int(plan.slot_expert[j]), int(plan.slot_replica[j])
+        row = int(slot_offset[j])
+        for s in range(len(tb) - 1):
+            flat = ids[tb[s]:tb[s + 1]].reshape(-1)
+            plist = tb[s] * K + np.nonzero(flat == e)[0]   # source s's list of e, ascending p
+            for p in plist[int(rep_begin_src[s, e, r]):int(rep_begin_src[s, e, r + 1])]:
+                if row >= n_cap:
+                    dropped += 1
+                else:
+                    pair_to_row[p] = row
+                    row_to_pair[row] = p
+                    x_perm[row] = x[p // K]
+                row += 1
+    return x_perm, row_to_pair, pair_to_row, dropped
+
+
+# ----------------------------------------------------------------------------
 # Step 3: permute (dispatch of each pair to exactly one local slot)
 # ----------------------------------------------------------------------------
 def permute(x: np.ndarray, ids: np.ndarray, plan, rep_begin: np.ndarray,

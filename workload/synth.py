@@ -102,6 +102,15 @@ class Plan:
     slot_widx: np.ndarray
     slot_gidx: np.ndarray
     local_experts: np.ndarray
+    # per-source split (Sec. 7.2 r_{s,e,j} per source rank): source s owns
+    # tokens [src_token_begin[s], src_token_begin[s+1]); src_rep_weight
+    # [n_src, E, R_max] integer weights (None = the per-expert ones)
+    src_token_begin: Optional[np.ndarray] = None
+    src_rep_weight: Optional[np.ndarray] = None
+
+    @property
+    def n_src(self) -> int:
+        return 1 if self.src_token_begin is None else int(len(self.src_token_begin) - 1)
 
     @property
     def S(self) -> int:
