@@ -54,6 +54,7 @@ extern "C" {
 #define FOREMOE_MAX_SLOTS 1024
 #define FOREMOE_MAX_REPLICAS 16
 #define FOREMOE_MAX_TOPK 64
+#define FOREMOE_MAX_SOURCES 64
 
 typedef enum foremoe_dtype {
   FOREMOE_F32 = 0,
@@ -77,6 +78,20 @@ typedef enum foremoe_dtype {
  *                     may alias its source expert's weights
  *  slot_gidx[S]       gradient index (0..G-1) slot j accumulates into: the
  *                     main expert of slot j's expert (Sec. 6.2)
+ *  n_src              source ranks of the per-source split (0 or 1: one
+ *                     source, the arrays below unused), 2..FOREMOE_MAX_SOURCES
+ *                     with n_src * E <= FOREMOE_MAX_EXPERTS and
+ *                     n_src * S <= FOREMOE_MAX_SLOTS
+ *  src_token_begin    [n_src + 1] first token of each source rank (Sec. 7.2:
+ *                     r_{s,e,j} is set per source rank s): source s owns the
+ *                     tokens [src_token_begin[s], src_token_begin[s+1]),
+ *                     nondecreasing from 0 to T (pairs of tokens outside it
+ *                     count as invalid ids)
+ *  src_rep_weight     [n_src * E * R_max] integer split weights per (source,
+ *                     expert), e.g. a planner's water-filled token counts
+ *                     (App. D Stage 4), or NULL: expert_rep_weight for every
+ *                     source. All-zero weights are an error only when the
+ *                     (source, expert) block has pairs.
  *
  * Errors in the device arrays (a slot naming an expert or replica out of
  * range, two slots holding the same replica, a zero weight sum) cannot be
@@ -87,21 +102,23 @@ typedef struct foremoe_plan {
   int32_t E;
   int32_t S;
   int32_t R_max;
-  int32_t reserved;
+  int32_t n_src;
   const int32_t* slot_expert;
   const int32_t* slot_replica;
   const int32_t* expert_nrep;
   const int32_t* expert_rep_weight;
   const int32_t* slot_widx;
   const int32_t* slot_gidx;
+  const int32_t* src_token_begin;
+  const int32_t* src_rep_weight;
 } foremoe_plan;
 
 /*
  * Workspace. foremoe_histogram, foremoe_assign_replicas and foremoe_permute
  * of one micro-step share one caller-owned device workspace of at least
  * foremoe_workspace_size(T, K, E) bytes (256-byte aligned; returns 0 for
- * invalid sizes). Its first 256 bytes are int32 status words (read them
- * after the stream completes):
+ * invalid sizes; for a per-source plan pass n_src * E as E). Its first 256
+ * bytes are int32 status words (read them after the stream completes):
  */
 #define FOREMOE_WS_INVALID_IDS 0  /* ids outside [-1, E): skipped, written by histogram */
 #define FOREMOE_WS_DROPPED 1      /* local pairs beyond n_cap, written by permute       */
@@ -121,6 +138,17 @@ int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E,
                       int32_t* counts, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Step 1 per source rank (Sec. 7.2, load w_{s,e} of Table 1), for plans with
+ * n_src >= 2: counts [n_src, E] int32 out, counts[s][e] = #pairs of the
+ * tokens [src_token_begin[s], src_token_begin[s+1]) with ids[p] == e.
+ * src_token_begin [n_src + 1] device array as in foremoe_plan. Fills the
+ * workspace (sized for n_src * E experts) for foremoe_permute of such a plan.
+ */
+int foremoe_histogram_src(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t n_src,
+                          const int32_t* src_token_begin, int32_t* counts, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/*
  * Step 2 (Sec. 7.2 token conservation; Sec. 8 Stage 4; App. D Stage 4).
  * For expert e with R_e replicas and weights w (equal if NULL), replica r
  * takes the contiguous block [B_r, B_{r+1}) of e's token list (ascending
@@ -130,6 +158,11 @@ int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E,
  * slot_offset [S+1] int32 out: exclusive prefix sum of slot_count in slot
  *             order; slot_offset[S] = N, the local pairs of this GPU.
  * ws          the workspace foremoe_histogram filled for the same ids.
+ * Per-source plan (n_src >= 2): counts is [n_src, E] from
+ * foremoe_histogram_src, the split is done for every (source, expert) block
+ * with that source's weights, rep_begin is [n_src, E, R_max+1], and a slot
+ * takes its replica's blocks source by source (so its rows stay in
+ * ascending pair order); slot_count sums the blocks.
  */
 int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan,
                             int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset,
@@ -149,6 +182,9 @@ int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan,
  * x_perm   [n_cap, d] of `dtype`; row_to_pair [n_cap]; pair_to_row [T*K].
  * ws       the workspace filled by foremoe_histogram and
  *          foremoe_assign_replicas for the same ids and plan.
+ * Per-source plan: q is the rank within the pair's (source, expert) list,
+ * B the bounds of that block, and the row follows the source's earlier
+ * blocks in slot j (foremoe_histogram_src must have filled ws).
  */
 int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
                     const int32_t* ids, int32_t K, const foremoe_plan* plan,

@@ -19,15 +19,17 @@ MAX_EXPERTS = 1024
 MAX_SLOTS = 1024
 MAX_REPLICAS = 16
 MAX_TOPK = 64
+MAX_SOURCES = 64
 
 c_i32, c_i64, c_sz, c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
 
 
 class Plan(ctypes.Structure):
     _fields_ = [
-        ("E", c_i32), ("S", c_i32), ("R_max", c_i32), ("reserved", c_i32),
+        ("E", c_i32), ("S", c_i32), ("R_max", c_i32), ("n_src", c_i32),
         ("slot_expert", c_p), ("slot_replica", c_p), ("expert_nrep", c_p),
         ("expert_rep_weight", c_p), ("slot_widx", c_p), ("slot_gidx", c_p),
+        ("src_token_begin", c_p), ("src_rep_weight", c_p),
     ]
 
 
@@ -44,6 +46,7 @@ PMachine = ctypes.POINTER(Machine)
 SIGNATURES = {
     "foremoe_workspace_size": (c_sz, [c_i64, c_i32, c_i32]),
     "foremoe_histogram": (ctypes.c_int, [c_p, c_i64, c_i32, c_i32, c_p, c_p, c_sz, c_p]),
+    "foremoe_histogram_src": (ctypes.c_int, [c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_assign_replicas": (ctypes.c_int, [c_p, PPlan, c_p, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_permute": (ctypes.c_int, [c_p, c_i32, c_i64, c_i32, c_p, c_i32, PPlan, c_p, c_p, c_i64,
                                        c_p, c_p, c_p, c_p, c_sz, c_p]),

@@ -59,6 +59,9 @@ class DevicePlan:
     expert_rep_weight: Optional[torch.Tensor]
     slot_widx: torch.Tensor
     slot_gidx: torch.Tensor
+    n_src: int = 1
+    src_token_begin: Optional[torch.Tensor] = None
+    src_rep_weight: Optional[torch.Tensor] = None
 
     @classmethod
     def from_host(cls, plan, device) -> "DevicePlan":
@@ -67,17 +70,25 @@ class DevicePlan:
         def t(a):
             return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
 
-        w = None if plan.expert_rep_weight is None else t(np.asarray(plan.expert_rep_weight).reshape(-1))
+        def opt(a):
+            return None if a is None else t(np.asarray(a).reshape(-1))
+
+        tb = getattr(plan, "src_token_begin", None)
         return cls(E=plan.E, S=plan.S, R_max=plan.R_max, W=plan.W, G=plan.G,
                    slot_expert=t(plan.slot_expert), slot_replica=t(plan.slot_replica),
-                   expert_nrep=t(plan.expert_nrep), expert_rep_weight=w,
-                   slot_widx=t(plan.slot_widx), slot_gidx=t(plan.slot_gidx))
+                   expert_nrep=t(plan.expert_nrep), expert_rep_weight=opt(plan.expert_rep_weight),
+                   slot_widx=t(plan.slot_widx), slot_gidx=t(plan.slot_gidx),
+                   n_src=1 if tb is None else len(tb) - 1, src_token_begin=opt(tb),
+                   src_rep_weight=opt(getattr(plan, "src_rep_weight", None)))
 
     def c_struct(self) -> _lib.Plan:
-        return _lib.Plan(self.E, self.S, self.R_max, 0, self.slot_expert.data_ptr(),
-                         self.slot_replica.data_ptr(), self.expert_nrep.data_ptr(),
-                         None if self.expert_rep_weight is None else self.expert_rep_weight.data_ptr(),
-                         self.slot_widx.data_ptr(), self.slot_gidx.data_ptr())
+        def p(x):
+            return None if x is None else x.data_ptr()
+
+        return _lib.Plan(self.E, self.S, self.R_max, self.n_src, self.slot_expert.data_ptr(),
+                         self.slot_replica.data_ptr(), self.expert_nrep.data_ptr(), p(self.expert_rep_weight),
+                         self.slot_widx.data_ptr(), self.slot_gidx.data_ptr(), p(self.src_token_begin),
+                         p(self.src_rep_weight))
 
 
 def workspace(T: int, K: int, E: int, device) -> torch.Tensor:
@@ -101,9 +112,22 @@ def histogram(ids: torch.Tensor, E: int, ws: torch.Tensor) -> torch.Tensor:
     return counts
 
 
+def histogram_src(ids: torch.Tensor, E: int, src_token_begin: torch.Tensor, ws: torch.Tensor) -> torch.Tensor:
+    """Per-source counts [n_src, E] (src_token_begin: device int32 [n_src + 1])."""
+    _i32(ids, "ids")
+    _i32(src_token_begin, "src_token_begin")
+    T, K = ids.shape
+    n_src = src_token_begin.numel() - 1
+    counts = torch.empty((n_src, E), dtype=torch.int32, device=ids.device)
+    check(_lib.load().foremoe_histogram_src(_ptr(ids), T, K, E, n_src, _ptr(src_token_begin), _ptr(counts), _ptr(ws),
+                                            ws.numel(), _stream(ids.device)), "foremoe_histogram_src")
+    return counts
+
+
 def assign_replicas(counts: torch.Tensor, plan: DevicePlan, ws: torch.Tensor):
     dev = counts.device
-    rep_begin = torch.empty((plan.E, plan.R_max + 1), dtype=torch.int32, device=dev)
+    shape = (plan.E, plan.R_max + 1) if plan.n_src <= 1 else (plan.n_src, plan.E, plan.R_max + 1)
+    rep_begin = torch.empty(shape, dtype=torch.int32, device=dev)
     slot_count = torch.empty(max(plan.S, 1), dtype=torch.int32, device=dev)[: plan.S]
     slot_offset = torch.empty(plan.S + 1, dtype=torch.int32, device=dev)
     cp = plan.c_struct()

@@ -15,17 +15,21 @@ constexpr int kHistChunk = 512;
 constexpr int kHistThreads = 256;
 constexpr int kWsHeaderBytes = 256;
 
-inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+constexpr size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Workspace layout (fixed offsets, so that every call can find its part
-// from its own arguments):
+// from its own arguments). With a per-source plan the ranking keys are
+// (source, expert) pairs, key = s * E + e, and slots are split the same way
+// into virtual slots j * n_src + s; "keys" below is E or n_src * E.
 //   [0, 256)                 int32 status words
-//   [256, 256 + 64 KiB)      rep_slot[E * R_max]: local slot of replica (e, r) or -1
-//   [kWsPartialOff, ...)     per-block histogram partials [NB][E+1]; the rank
+//   [256, +64 KiB)           rep_slot[keys * R_max]: (virtual) slot of replica (key, r) or -1
+//   [kWsVSlotOff, +4 KiB+4)  vslot_offset[S * n_src + 1]: row offsets of the virtual slots
+//   [kWsPartialOff, ...)     per-block histogram partials [NB][keys+1]; the rank
 //                            kernel turns them into exclusive block bases
 constexpr size_t kWsRepSlotOff = kWsHeaderBytes;
-constexpr size_t kWsPartialOff =
+constexpr size_t kWsVSlotOff =
     kWsRepSlotOff + sizeof(int32_t) * (size_t)FOREMOE_MAX_EXPERTS * (size_t)FOREMOE_MAX_REPLICAS;
+constexpr size_t kWsPartialOff = kWsVSlotOff + align_up(sizeof(int32_t) * ((size_t)FOREMOE_MAX_SLOTS + 1), 256);
 
 inline int64_t hist_blocks(int64_t npairs) {
   int64_t nb = (npairs + kHistChunk - 1) / kHistChunk;

@@ -34,14 +34,49 @@ __device__ __forceinline__ uint64_t match_key(int key, int nbits, uint64_t activ
 // Key of a recorded id: the expert, -1 for padding, E for invalid ids.
 __device__ __forceinline__ int id_key(int v, int E) { return v == -1 ? -1 : ((v >= 0 && v < E) ? v : E); }
 
+// How a pair becomes its ranking key. With one source the key is the
+// expert; with a per-source split (Sec. 7.2: r_{s,e,j} per source rank) it
+// is s * E + e for the source s that owns the pair's token, so that ranks,
+// counts and replica blocks are per (source, expert). nkeys = n_src * E is
+// the invalid-id bucket.
+struct KeyMap {
+  int E, n_src, K;
+  const int32_t* tb;  // [n_src + 1] first token of each source (n_src >= 2)
+};
+
+// Source bounds into LDS (n_src + 1 <= FOREMOE_MAX_SOURCES + 1 entries).
+__device__ __forceinline__ void load_sources(const KeyMap& km, int* s_tb) {
+  if (km.n_src >= 2)
+    for (int i = threadIdx.x; i <= km.n_src; i += blockDim.x) s_tb[i] = km.tb[i];
+}
+
+__device__ __forceinline__ int pair_key(int v, int64_t p, const KeyMap& km, const int* s_tb) {
+  const int k = id_key(v, km.E);
+  if (km.n_src < 2 || k < 0) return k;
+  const int nkeys = km.n_src * km.E;
+  if (k == km.E) return nkeys;
+  const int t = (int)(p / km.K);
+  if (t < s_tb[0] || t >= s_tb[km.n_src]) return nkeys;  // token outside every source
+  int lo = 0, hi = km.n_src - 1;  // the last source starting at or before t
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (s_tb[mid] <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo * km.E + k;
+}
+
 // ---------------------------------------------------------------------------
-// Step 1a: per-block counts of each expert (bucket E counts invalid ids).
+// Step 1a: per-block counts of each key (bucket nkeys counts invalid ids).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kHistThreads) void hist_count_kernel(const int32_t* __restrict__ ids, int64_t npairs,
-                                                                  int E, int nbits, int32_t* __restrict__ partial) {
+                                                                  KeyMap km, int E, int nbits,
+                                                                  int32_t* __restrict__ partial) {
   __shared__ int s_cnt[FOREMOE_MAX_EXPERTS + 1];
+  __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
   const int tid = threadIdx.x;
   for (int e = tid; e <= E; e += kHistThreads) s_cnt[e] = 0;
+  load_sources(km, s_tb);
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * kHistChunk;
   const int lane = tid & 63;
@@ -49,7 +84,7 @@ __global__ __launch_bounds__(kHistThreads) void hist_count_kernel(const int32_t*
   for (int i = 0; i < kHistChunk / kHistThreads; ++i) {
     const int64_t p = base + (int64_t)i * kHistThreads + tid;
     int key = -1;
-    if (p < npairs) key = id_key(ids[p], E);
+    if (p < npairs) key = pair_key(ids[p], p, km, s_tb);
     const uint64_t active = __ballot(key >= 0);
     const uint64_t m = match_key(key, nbits, active);
     if (key >= 0 && lane == __builtin_ctzll(m)) atomicAdd(&s_cnt[key], __popcll(m));
@@ -108,11 +143,12 @@ __global__ __launch_bounds__(kHistThreads) void hist_scan_kernel(int32_t* __rest
 // Step 2: replica boundaries, slot counts and slot offsets (one workgroup).
 // ---------------------------------------------------------------------------
 struct PlanDev {
-  int E, S, R_max;
+  int E, S, R_max, n_src;  // n_src >= 1
   const int32_t* slot_expert;
   const int32_t* slot_replica;
   const int32_t* expert_nrep;
   const int32_t* expert_rep_weight;
+  const int32_t* src_rep_weight;  // [n_src * E * R_max] or NULL
 };
 
 __device__ __forceinline__ int clamp_nrep(const PlanDev& P, int e, int& err) {
@@ -124,82 +160,103 @@ __device__ __forceinline__ int clamp_nrep(const PlanDev& P, int e, int& err) {
   return R;
 }
 
+// Keys are (source, expert) pairs kk = s * E + e and the S slots are split
+// into virtual slots jj = j * n_src + s (one source: kk = e, jj = j).
+// Virtual slot jj takes replica r_j of key s * E + e_j; its rows follow
+// those of the same slot's earlier sources, so a slot's rows are its
+// sources' blocks in source order.
 __global__ __launch_bounds__(kHistThreads) void assign_kernel(const int32_t* __restrict__ counts, PlanDev P,
                                                               int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count,
-                                                              int32_t* __restrict__ slot_offset, int32_t* __restrict__ rep_slot,
-                                                              int32_t* __restrict__ status) {
+                                                              int32_t* __restrict__ slot_offset, int32_t* __restrict__ vslot_offset,
+                                                              int32_t* __restrict__ rep_slot, int32_t* __restrict__ status) {
   __shared__ int s_err;
   __shared__ int s_cnt[FOREMOE_MAX_SLOTS];
+  __shared__ int s_off[FOREMOE_MAX_SLOTS + 1];
   __shared__ int s_tmp[kWaves];
   const int tid = threadIdx.x;
   if (tid == 0) s_err = 0;
   const int RS = P.R_max + 1;
-  for (int i = tid; i < P.E * P.R_max; i += kHistThreads) rep_slot[i] = INT_MAX;
+  const int NK = P.n_src * P.E, NS = P.n_src * P.S;
+  for (int i = tid; i < NK * P.R_max; i += kHistThreads) rep_slot[i] = INT_MAX;
   __syncthreads();
   int err = 0;
-  for (int e = tid; e < P.E; e += kHistThreads) {
-    const int n = counts[e];
+  for (int kk = tid; kk < NK; kk += kHistThreads) {
+    const int e = kk % P.E;
+    const int n = counts[kk];
     const int R = clamp_nrep(P, e, err);
+    const int32_t* wt = P.src_rep_weight ? P.src_rep_weight + (int64_t)kk * P.R_max
+                                          : (P.expert_rep_weight ? P.expert_rep_weight + (int64_t)e * P.R_max : nullptr);
     long long total = 0;
     bool bad = false;
     for (int r = 0; r < R; ++r) {
-      const int w = P.expert_rep_weight ? P.expert_rep_weight[e * P.R_max + r] : 1;
+      const int w = wt ? wt[r] : 1;
       if (w < 0) bad = true;
       total += w;
     }
-    if (total <= 0) bad = true;
+    // all-zero per-source weights are fine for an empty block
+    if (total <= 0 && (n > 0 || !P.src_rep_weight)) bad = true;
     if (bad) ++err;
     long long pref = 0;
-    int32_t* rb = rep_begin + (int64_t)e * RS;
+    int32_t* rb = rep_begin + (int64_t)kk * RS;
     rb[0] = 0;
     for (int r = 0; r < R; ++r) {
-      const long long w = bad ? 1 : (P.expert_rep_weight ? P.expert_rep_weight[e * P.R_max + r] : 1);
+      const long long w = (bad || total <= 0) ? 1 : (wt ? wt[r] : 1);
       pref += w;
-      rb[r + 1] = (int)(((long long)n * pref) / (bad ? (long long)R : total));
+      rb[r + 1] = (int)(((long long)n * pref) / ((bad || total <= 0) ? (long long)R : total));
     }
     for (int r = R + 1; r < RS; ++r) rb[r] = n;
   }
-  // Slot j claims replica (e, r); with duplicates the lowest j wins.
-  for (int j = tid; j < P.S; j += kHistThreads) {
+  // Virtual slot jj claims replica (key, r); with duplicates the lowest slot wins.
+  for (int jj = tid; jj < NS; jj += kHistThreads) {
+    const int j = jj / P.n_src, src = jj % P.n_src;
     const int e = P.slot_expert[j], r = P.slot_replica[j];
-    if (e >= 0 && e < P.E && r >= 0 && r < P.R_max) atomicMin(&rep_slot[e * P.R_max + r], j);
+    if (e >= 0 && e < P.E && r >= 0 && r < P.R_max) atomicMin(&rep_slot[(src * P.E + e) * P.R_max + r], jj);
   }
   __syncthreads();
-  for (int j = tid; j < P.S; j += kHistThreads) {
+  for (int jj = tid; jj < NS; jj += kHistThreads) {
+    const int j = jj / P.n_src, src = jj % P.n_src;
     const int e = P.slot_expert[j], r = P.slot_replica[j];
     int c = 0;
+    bool ok = false;
     if (e >= 0 && e < P.E && r >= 0) {
       int dummy = 0;
       const int R = clamp_nrep(P, e, dummy);
-      if (r < R && rep_slot[e * P.R_max + r] == j) {
-        const int32_t* rb = rep_begin + (int64_t)e * RS;
+      const int kk = src * P.E + e;
+      if (r < R && rep_slot[kk * P.R_max + r] == jj) {
+        const int32_t* rb = rep_begin + (int64_t)kk * RS;
         c = rb[r + 1] - rb[r];
-      } else {
-        ++err;
+        ok = true;
       }
-    } else {
-      ++err;
     }
-    slot_count[j] = c;
-    s_cnt[j] = c;
+    if (!ok && src == 0) ++err;  // one error per bad slot
+    s_cnt[jj] = c;
   }
   if (err) atomicAdd(&s_err, err);
   __syncthreads();
-  for (int i = tid; i < P.E * P.R_max; i += kHistThreads) {
+  for (int i = tid; i < NK * P.R_max; i += kHistThreads) {
     // replicas beyond R_e, and replicas held by no (valid) slot, are remote
-    const int e = i / P.R_max, r = i % P.R_max;
+    const int e = (i / P.R_max) % P.E, r = i % P.R_max;
     int dummy = 0;
     const int R = clamp_nrep(P, e, dummy);
     if (rep_slot[i] == INT_MAX || r >= R) rep_slot[i] = -1;
   }
   int carry = 0;
-  for (int j0 = 0; j0 < P.S; j0 += kHistThreads) {
-    const int j = j0 + tid;
-    const int v = j < P.S ? s_cnt[j] : 0;
+  for (int j0 = 0; j0 < NS; j0 += kHistThreads) {
+    const int jj = j0 + tid;
+    const int v = jj < NS ? s_cnt[jj] : 0;
     int total;
     const int incl = block_inclusive_scan(v, s_tmp, total);
-    if (j < P.S) slot_offset[j] = carry + incl - v;
+    if (jj < NS) s_off[jj] = carry + incl - v;
     carry += total;
+  }
+  if (tid == 0) s_off[NS] = carry;
+  __syncthreads();
+  for (int jj = tid; jj <= NS; jj += kHistThreads) vslot_offset[jj] = s_off[jj];
+  for (int j = tid; j < P.S; j += kHistThreads) {
+    int c = 0;
+    for (int src = 0; src < P.n_src; ++src) c += s_cnt[j * P.n_src + src];
+    slot_count[j] = c;
+    slot_offset[j] = s_off[j * P.n_src];
   }
   if (tid == 0) {
     slot_offset[P.S] = carry;
@@ -213,20 +270,22 @@ __global__ __launch_bounds__(kHistThreads) void assign_kernel(const int32_t* __r
 // block's pairs in ascending order.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kHistThreads) void permute_rank_kernel(
-    const int32_t* __restrict__ ids, int64_t npairs, int E, int nbits, int R_max,
+    const int32_t* __restrict__ ids, int64_t npairs, KeyMap km, int E, int nbits, int R_max,
     const int32_t* __restrict__ block_base, const int32_t* __restrict__ rep_begin,
     const int32_t* __restrict__ rep_slot, const int32_t* __restrict__ slot_offset, int S, int64_t n_cap,
     int32_t* __restrict__ pair_to_row, int32_t* __restrict__ row_to_pair, int32_t* __restrict__ status) {
   __shared__ int s_w[kWaves][FOREMOE_MAX_EXPERTS + 1];
+  __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   for (int e = lane; e <= E; e += 64) s_w[w][e] = 0;
+  load_sources(km, s_tb);
   __syncthreads();
   const int64_t wbase = (int64_t)blockIdx.x * kHistChunk + (int64_t)w * kPairsPerWave;
   // pass 1: per-wave counts
   for (int i = 0; i < kPairsPerWave / 64; ++i) {
     const int64_t p = wbase + i * 64 + lane;
     int key = -1;
-    if (p < npairs) key = id_key(ids[p], E);
+    if (p < npairs) key = pair_key(ids[p], p, km, s_tb);
     if (key == E) key = -1;
     const uint64_t active = __ballot(key >= 0);
     const uint64_t m = match_key(key, nbits, active);
@@ -248,7 +307,7 @@ __global__ __launch_bounds__(kHistThreads) void permute_rank_kernel(
   for (int i = 0; i < kPairsPerWave / 64; ++i) {
     const int64_t p = wbase + i * 64 + lane;
     int key = -1;
-    if (p < npairs) key = id_key(ids[p], E);
+    if (p < npairs) key = pair_key(ids[p], p, km, s_tb);
     if (key == E) key = -1;
     const uint64_t active = __ballot(key >= 0);
     const uint64_t m = match_key(key, nbits, active);
@@ -598,25 +657,41 @@ using namespace foremoe;
 
 extern "C" {
 
-int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t* counts, void* ws,
-                      size_t ws_bytes, void* stream) {
-  REQUIRE(T >= 0, "histogram: T < 0");
-  REQUIRE(K >= 1 && K <= FOREMOE_MAX_TOPK, "histogram: K=%d outside [1, %d]", K, FOREMOE_MAX_TOPK);
-  REQUIRE(E >= 1 && E <= FOREMOE_MAX_EXPERTS, "histogram: E=%d outside [1, %d]", E, FOREMOE_MAX_EXPERTS);
-  REQUIRE(T * (int64_t)K < (int64_t)INT_MAX, "histogram: T*K must be below 2^31");
-  REQUIRE(ids || T == 0, "histogram: ids is NULL");
-  REQUIRE(counts && ws, "histogram: counts or ws is NULL");
-  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, E), "histogram: workspace too small (%zu < %zu)", ws_bytes,
+static int histogram_common(const char* who, const int32_t* ids, int64_t T, int32_t K, int32_t E, KeyMap km,
+                            int32_t* counts, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(T >= 0, "%s: T < 0", who);
+  REQUIRE(K >= 1 && K <= FOREMOE_MAX_TOPK, "%s: K=%d outside [1, %d]", who, K, FOREMOE_MAX_TOPK);
+  REQUIRE(E >= 1 && E <= FOREMOE_MAX_EXPERTS, "%s: %d keys outside [1, %d]", who, E, FOREMOE_MAX_EXPERTS);
+  REQUIRE(T * (int64_t)K < (int64_t)INT_MAX, "%s: T*K must be below 2^31", who);
+  REQUIRE(ids || T == 0, "%s: ids is NULL", who);
+  REQUIRE(counts && ws, "%s: counts or ws is NULL", who);
+  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, E), "%s: workspace too small (%zu < %zu)", who, ws_bytes,
           ws_bytes_needed(T, K, E));
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
   int32_t* status = (int32_t*)ws;
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
-  hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, E, key_bits(E),
-                     partial);
+  hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, E,
+                     key_bits(E), partial);
   hipLaunchKernelGGL(hist_scan_kernel, dim3(E + 1), dim3(kHistThreads), 0, st, partial, nb, E, counts, status);
-  return check_launch("foremoe_histogram");
+  return check_launch(who);
+}
+
+int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t* counts, void* ws,
+                      size_t ws_bytes, void* stream) {
+  return histogram_common("foremoe_histogram", ids, T, K, E, KeyMap{E, 1, K, nullptr}, counts, ws, ws_bytes, stream);
+}
+
+int foremoe_histogram_src(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t n_src,
+                          const int32_t* src_token_begin, int32_t* counts, void* ws, size_t ws_bytes, void* stream) {
+  REQUIRE(n_src >= 2 && n_src <= FOREMOE_MAX_SOURCES, "histogram_src: n_src=%d outside [2, %d]", n_src,
+          FOREMOE_MAX_SOURCES);
+  REQUIRE(E >= 1 && (int64_t)E * n_src <= FOREMOE_MAX_EXPERTS, "histogram_src: n_src * E must be in [1, %d]",
+          FOREMOE_MAX_EXPERTS);
+  REQUIRE(src_token_begin, "histogram_src: src_token_begin is NULL");
+  return histogram_common("foremoe_histogram_src", ids, T, K, E * n_src, KeyMap{E, n_src, K, src_token_begin},
+                          counts, ws, ws_bytes, stream);
 }
 
 int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
@@ -631,12 +706,20 @@ int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int
   REQUIRE(plan->S == 0 || (plan->slot_expert && plan->slot_replica && slot_count),
           "assign_replicas: NULL slot arrays");
   REQUIRE(ws_bytes >= kWsPartialOff, "assign_replicas: workspace too small");
-  PlanDev P{plan->E, plan->S, plan->R_max, plan->slot_expert, plan->slot_replica, plan->expert_nrep,
-            plan->expert_rep_weight};
+  const int n_src = plan->n_src < 1 ? 1 : plan->n_src;
+  if (n_src >= 2) {
+    REQUIRE(n_src <= FOREMOE_MAX_SOURCES, "assign_replicas: n_src=%d above %d", n_src, FOREMOE_MAX_SOURCES);
+    REQUIRE((int64_t)n_src * plan->E <= FOREMOE_MAX_EXPERTS && (int64_t)n_src * plan->S <= FOREMOE_MAX_SLOTS,
+            "assign_replicas: n_src * E or n_src * S above the limits");
+    REQUIRE(plan->src_token_begin, "assign_replicas: plan->src_token_begin is NULL");
+  }
+  PlanDev P{plan->E, plan->S, plan->R_max, n_src, plan->slot_expert, plan->slot_replica, plan->expert_nrep,
+            plan->expert_rep_weight, n_src >= 2 ? plan->src_rep_weight : nullptr};
   int32_t* status = (int32_t*)ws;
   int32_t* rep_slot = (int32_t*)((char*)ws + kWsRepSlotOff);
+  int32_t* vslot = (int32_t*)((char*)ws + kWsVSlotOff);
   hipLaunchKernelGGL(assign_kernel, dim3(1), dim3(kHistThreads), 0, (hipStream_t)stream, counts, P, rep_begin,
-                     slot_count, slot_offset, rep_slot, status);
+                     slot_count, slot_offset, vslot, rep_slot, status);
   return check_launch("foremoe_assign_replicas");
 }
 
@@ -658,15 +741,27 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, co
   const int esz = dtype == FOREMOE_BF16 ? 2 : 4;
   if ((int64_t)d * esz % 16 != 0)
     return set_error(FOREMOE_EUNSUPPORTED, "permute: row of %d elements is not a multiple of 16 bytes", d);
-  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, plan->E), "permute: workspace too small");
+  const int n_src = plan->n_src < 1 ? 1 : plan->n_src;
+  if (n_src >= 2) {
+    REQUIRE(n_src <= FOREMOE_MAX_SOURCES && (int64_t)n_src * plan->E <= FOREMOE_MAX_EXPERTS &&
+                (int64_t)n_src * plan->S <= FOREMOE_MAX_SLOTS,
+            "permute: n_src out of range");
+    REQUIRE(plan->src_token_begin, "permute: plan->src_token_begin is NULL");
+  }
+  const int nkeys = n_src * plan->E;
+  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, nkeys), "permute: workspace too small");
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
   int32_t* status = (int32_t*)ws;
   const int32_t* rep_slot = (const int32_t*)((char*)ws + kWsRepSlotOff);
   const int32_t* base = (const int32_t*)((char*)ws + kWsPartialOff);
-  hipLaunchKernelGGL(permute_rank_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, plan->E,
-                     key_bits(plan->E), plan->R_max, base, rep_begin, rep_slot, slot_offset, plan->S, n_cap,
+  // rows come from the virtual slots' offsets (the slot offsets themselves
+  // with one source)
+  const int32_t* row_off = n_src >= 2 ? (const int32_t*)((char*)ws + kWsVSlotOff) : slot_offset;
+  const KeyMap km{plan->E, n_src, K, n_src >= 2 ? plan->src_token_begin : nullptr};
+  hipLaunchKernelGGL(permute_rank_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, nkeys,
+                     key_bits(nkeys), plan->R_max, base, rep_begin, rep_slot, row_off, n_src * plan->S, n_cap,
                      pair_to_row, row_to_pair, status);
   const int64_t vpr = (int64_t)d * esz / 16;
   hipLaunchKernelGGL(gather_rows_kernel, dim3(gather_grid(n_cap)), dim3(256), 0, st, (const uint4*)x, vpr, K,

@@ -53,10 +53,12 @@ def test_workspace_size(lib):
     assert small > 0 and small % 256 == 0
     big = lib.foremoe_workspace_size(32768, 8, 256)
     assert big > small
-    # status words, the replica->slot table, then [blocks][E+1] partial counts
+    # status words, the replica->slot table, the virtual-slot offsets
+    # (1025 ints rounded to 256 bytes), then [blocks][E+1] partial counts
     # (one block per 512 pairs)
-    assert big >= 256 + 4 * 1024 * 16 + 512 * 257 * 4
-    assert big - (256 + 4 * 1024 * 16 + 512 * 257 * 4) < 256
+    fixed = 256 + 4 * 1024 * 16 + 4352
+    assert big >= fixed + 512 * 257 * 4
+    assert big - (fixed + 512 * 257 * 4) < 256
     assert lib.foremoe_workspace_size(-1, 2, 8) == 0
     assert lib.foremoe_workspace_size(10, 0, 8) == 0
     assert lib.foremoe_workspace_size(10, 2, 2000) == 0
