@@ -46,6 +46,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
+    ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three plain 1 GiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
@@ -292,10 +293,106 @@ def main() -> int:
         "kernels": kernels,
         "setup_s": round(setup_s, 1),
     }
+    if not args.no_planner:
+        out["planner"] = planner_report(w, api, dev, n_micro)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> dict:
+    """The placement planner on the same micro-steps (Sec. 8 Alg. 1; App. D
+    Alg. 3; host C++), and the per-source dispatch of the measured rank's
+    planned share on the GPU (Sec. 7.2 r_{s,e,j} as water-filled counts).
+
+    Reported: the planner's host time per micro-step, the compute imbalance
+    L_max / L_mean over the 8 ranks (natural placement e -> e / (E/P), Stage 1
+    base placement, after Stages 2-4; medians over the micro-steps, the
+    metric of Sec. 10.4), the planned share's local pairs, and the GPU time of
+    histogram_src + assign_replicas + permute for it.
+    """
+    import numpy as np
+    import torch
+    from workload import Plan
+
+    spec = w.spec
+    P, E, T, K = spec.P, spec.E, spec.T, spec.K
+    tb = (np.arange(P + 1) * (T // P)).astype(np.int32)
+
+    def src_loads(ids):
+        out = np.zeros((P, E), dtype=np.int64)
+        for s in range(P):
+            v = ids[tb[s]:tb[s + 1]].reshape(-1)
+            out[s] = np.bincount(v[v >= 0], minlength=E)
+        return out
+
+    loads = [src_loads(m.ids) for m in w.micro[:n_micro]]
+    base = api.plan_base(np.sum(loads, axis=0), 1, P, E // P)
+    natural = np.arange(E) // (E // P)
+    imb = {"natural": [], "base": [], "planned": []}
+    plans, host_s = [], 0.0
+    for i, W in enumerate(loads):
+        t0 = time.perf_counter()
+        copy_rank, counts, rank_load = api.plan_micro_step(W, base, 1, P, E // P, N_r, C_max)
+        sl = api.plan_rank_slots(copy_rank, w.rank)
+        host_s += time.perf_counter() - t0
+        we = W.sum(axis=0)
+        for name, pl in (("natural", natural), ("base", base)):
+            L = np.bincount(pl, weights=we, minlength=P)
+            imb[name].append(float(L.max() / L.mean()))
+        imb["planned"].append(float(rank_load.max() / rank_load.mean()))
+        plans.append(Plan(E=E, R_max=C_max, slot_expert=sl["slot_expert"], slot_replica=sl["slot_replica"],
+                          expert_nrep=sl["expert_nrep"], expert_rep_weight=None, slot_widx=sl["slot_widx"],
+                          slot_gidx=sl["slot_widx"].copy(), local_experts=sl["local_experts"],
+                          src_token_begin=tb, src_rep_weight=counts))
+    # GPU: per-source dispatch of the measured rank's planned share
+    bf = torch.bfloat16
+    d = spec.d
+    n_cap = T * K
+    ws = api.workspace(T, K, E * P, dev)
+    x_perm = torch.empty((n_cap, d), dtype=bf, device=dev)
+    r2p = torch.empty(n_cap, dtype=torch.int32, device=dev)
+    p2r = torch.empty(T * K, dtype=torch.int32, device=dev)
+    ms = []
+    for i, pl in enumerate(plans):
+        dp = api.DevicePlan.from_host(pl, dev)
+        ms.append(dict(ids=torch.from_numpy(w.micro[i].ids).to(dev),
+                       x=torch.from_numpy(np.ascontiguousarray(w.x(i), dtype=np.float32)).to(dev).to(bf),
+                       plan=dp, cplan=dp.c_struct()))
+    lib = api._lib.load()
+    sp = torch.cuda.current_stream(dev).cuda_stream
+    Ns = []
+
+    def dispatch(m):
+        counts = api.histogram_src(m["ids"], E, m["plan"].src_token_begin, ws)
+        rb, sc, so = api.assign_replicas(counts.reshape(-1), m["plan"], ws)
+        api.check(lib.foremoe_permute(m["x"].data_ptr(), api._lib.BF16, T, d, m["ids"].data_ptr(), K,
+                                      ctypes.byref(m["cplan"]), rb.data_ptr(), so.data_ptr(), n_cap,
+                                      x_perm.data_ptr(), r2p.data_ptr(), p2r.data_ptr(), ws.data_ptr(),
+                                      ws.numel(), sp), "foremoe_permute")
+        return so
+
+    for m in ms:
+        Ns.append(int(dispatch(m)[-1].item()))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rounds = 3
+    e0.record()
+    for _ in range(rounds):
+        for m in ms:
+            dispatch(m)
+    e1.record()
+    torch.cuda.synchronize()
+    dispatch_us = e0.elapsed_time(e1) * 1e3 / (rounds * len(ms))
+    med = {k: round(float(np.median(v)), 3) for k, v in imb.items()}
+    return {"plan_us_per_micro_step": round(host_s / len(loads) * 1e6, 1),
+            "imbalance_median": med,
+            "imbalance_max": {k: round(float(np.max(v)), 3) for k, v in imb.items()},
+            "planned_share": {"rank": int(w.rank), "n_pairs_mean": round(float(np.mean(Ns)), 1),
+                              "n_pairs_max": int(max(Ns)), "n_pairs_min": int(min(Ns)),
+                              "dispatch_us_per_micro_step": round(dispatch_us, 2),
+                              "note": "histogram_src + assign_replicas + permute, (source, expert) keys"}}
 
 
 def measured_traffic(phase: str):
