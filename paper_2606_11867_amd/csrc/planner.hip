@@ -167,7 +167,7 @@ int foremoe_plan_micro_step(const int32_t* w, int32_t E, const foremoe_machine* 
       return set_error(FOREMOE_EINVAL, "plan_micro_step: expert %d has %d copies > C_max=%d", e,
                        (int)copies[e].size(), C_max);
   std::fill(counts, counts + (int64_t)P * E * C_max, 0);
-  // Stage 4: water-filling per machine, each unit to the least-loaded copy
+  // Stage 4: water-filling per machine, each token unit to the least-loaded copy
   std::vector<int64_t> load(P, 0);
   for (int m = 0; m < M; ++m) {
     std::vector<int> reps;
@@ -182,15 +182,42 @@ int foremoe_plan_micro_step(const int32_t* w, int32_t E, const foremoe_machine* 
     }
     for (int e : desc_order(we, reps)) {
       const std::vector<int>& c = copies[e];
+      const int nc = (int)c.size();
       for (int s = 0; s < P; ++s) {
-        int32_t* out = counts + ((int64_t)s * E + e) * C_max;
-        for (int32_t u = 0; u < w[(int64_t)s * E + e]; ++u) {
-          int best = 0;
-          for (int i = 1; i < (int)c.size(); ++i)
-            if (load[c[i]] < load[c[best]]) best = i;
-          ++out[best];
-          ++load[c[best]];
+        // The n units of (s, e), each to the copy with the least load
+        // (lowest copy index among equals), in closed form: raise every copy
+        // below the level lam to lam, where lam is the highest level the n
+        // units reach, then give the rest one each to the copies now at lam,
+        // in copy order.
+        const int64_t n = w[(int64_t)s * E + e];
+        if (n == 0) continue;
+        int64_t lo = load[c[0]], hi = load[c[0]];
+        for (int i = 1; i < nc; ++i) {
+          lo = std::min(lo, load[c[i]]);
+          hi = std::max(hi, load[c[i]]);
         }
+        hi += n;
+        while (lo < hi) {  // largest lam with sum max(0, lam - load) <= n
+          const int64_t mid = lo + (hi - lo + 1) / 2;
+          int64_t need = 0;
+          for (int i = 0; i < nc; ++i) need += std::max<int64_t>(0, mid - load[c[i]]);
+          if (need <= n) lo = mid;
+          else hi = mid - 1;
+        }
+        int32_t* out = counts + ((int64_t)s * E + e) * C_max;
+        int64_t rest = n;
+        for (int i = 0; i < nc; ++i) {
+          const int64_t add = std::max<int64_t>(0, lo - load[c[i]]);
+          out[i] += (int32_t)add;
+          load[c[i]] += add;
+          rest -= add;
+        }
+        for (int i = 0; i < nc && rest > 0; ++i)
+          if (load[c[i]] == lo) {
+            ++out[i];
+            ++load[c[i]];
+            --rest;
+          }
       }
     }
   }
