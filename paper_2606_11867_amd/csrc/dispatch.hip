@@ -94,8 +94,9 @@ __global__ __launch_bounds__(kHistThreads) void hist_count_kernel(const int32_t*
   for (int e = tid; e <= E; e += kHistThreads) out[e] = s_cnt[e];
 }
 
-// Inclusive block-wide scan of one int per thread (256 threads).
-__device__ int block_inclusive_scan(int v, int* s_tmp /* [kWaves] */, int& total) {
+// Inclusive block-wide scan of one int per thread (NW wavefronts).
+template <int NW = kWaves>
+__device__ int block_inclusive_scan(int v, int* s_tmp /* [NW] */, int& total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -106,7 +107,7 @@ __device__ int block_inclusive_scan(int v, int* s_tmp /* [kWaves] */, int& total
   __syncthreads();
   int before = 0;
   total = 0;
-  for (int i = 0; i < kWaves; ++i) {
+  for (int i = 0; i < NW; ++i) {
     const int t = s_tmp[i];
     if (i < w) before += t;
     total += t;
@@ -164,67 +165,83 @@ __device__ __forceinline__ int clamp_nrep(const PlanDev& P, int e, int& err) {
 // into virtual slots jj = j * n_src + s (one source: kk = e, jj = j).
 // Virtual slot jj takes replica r_j of key s * E + e_j; its rows follow
 // those of the same slot's earlier sources, so a slot's rows are its
-// sources' blocks in source order.
-__global__ __launch_bounds__(kHistThreads) void assign_kernel(const int32_t* __restrict__ counts, PlanDev P,
-                                                              int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count,
-                                                              int32_t* __restrict__ slot_offset, int32_t* __restrict__ vslot_offset,
-                                                              int32_t* __restrict__ rep_slot, int32_t* __restrict__ status) {
+// sources' blocks in source order. One workgroup of 1024 threads keeps the
+// replica bounds and the replica -> slot table in LDS while it works, loads
+// each key's weights together, and writes both tables out at the end, so
+// the kernel costs a few memory round trips.
+// Two sizes: up to 256 keys with 256 threads (small LDS, quick to launch)
+// and up to FOREMOE_MAX_EXPERTS keys with 1024 threads.
+template <int kAssignThreads, int MAXK>
+__global__ __launch_bounds__(kAssignThreads) void assign_kernel(const int32_t* __restrict__ counts, PlanDev P,
+                                                                int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count,
+                                                                int32_t* __restrict__ slot_offset, int32_t* __restrict__ vslot_offset,
+                                                                int32_t* __restrict__ rep_slot, int32_t* __restrict__ status) {
+  constexpr int NW = kAssignThreads / 64;
   __shared__ int s_err;
+  __shared__ int s_nrep[FOREMOE_MAX_EXPERTS];
+  __shared__ int s_rs[MAXK * FOREMOE_MAX_REPLICAS];
+  __shared__ int s_rb[MAXK * (FOREMOE_MAX_REPLICAS + 1)];
   __shared__ int s_cnt[FOREMOE_MAX_SLOTS];
   __shared__ int s_off[FOREMOE_MAX_SLOTS + 1];
-  __shared__ int s_tmp[kWaves];
+  __shared__ int s_tmp[NW];
   const int tid = threadIdx.x;
   if (tid == 0) s_err = 0;
   const int RS = P.R_max + 1;
   const int NK = P.n_src * P.E, NS = P.n_src * P.S;
-  for (int i = tid; i < NK * P.R_max; i += kHistThreads) rep_slot[i] = INT_MAX;
-  __syncthreads();
   int err = 0;
-  for (int kk = tid; kk < NK; kk += kHistThreads) {
+  for (int e = tid; e < P.E; e += kAssignThreads) s_nrep[e] = clamp_nrep(P, e, err);
+  for (int i = tid; i < NK * P.R_max; i += kAssignThreads) s_rs[i] = INT_MAX;
+  __syncthreads();
+  for (int kk = tid; kk < NK; kk += kAssignThreads) {
     const int e = kk % P.E;
     const int n = counts[kk];
-    const int R = clamp_nrep(P, e, err);
+    const int R = s_nrep[e];
     const int32_t* wt = P.src_rep_weight ? P.src_rep_weight + (int64_t)kk * P.R_max
                                           : (P.expert_rep_weight ? P.expert_rep_weight + (int64_t)e * P.R_max : nullptr);
+    int wv[FOREMOE_MAX_REPLICAS];
+#pragma unroll
+    for (int r = 0; r < FOREMOE_MAX_REPLICAS; ++r) wv[r] = (r < R) ? (wt ? wt[r] : 1) : 0;
     long long total = 0;
     bool bad = false;
-    for (int r = 0; r < R; ++r) {
-      const int w = wt ? wt[r] : 1;
-      if (w < 0) bad = true;
-      total += w;
+#pragma unroll
+    for (int r = 0; r < FOREMOE_MAX_REPLICAS; ++r) {
+      if (wv[r] < 0) bad = true;
+      total += wv[r];
     }
     // all-zero per-source weights are fine for an empty block
     if (total <= 0 && (n > 0 || !P.src_rep_weight)) bad = true;
     if (bad) ++err;
+    const bool eq = bad || total <= 0;
+    const long long den = eq ? (long long)R : total;
     long long pref = 0;
-    int32_t* rb = rep_begin + (int64_t)kk * RS;
+    int* rb = s_rb + kk * RS;
     rb[0] = 0;
-    for (int r = 0; r < R; ++r) {
-      const long long w = (bad || total <= 0) ? 1 : (wt ? wt[r] : 1);
-      pref += w;
-      rb[r + 1] = (int)(((long long)n * pref) / ((bad || total <= 0) ? (long long)R : total));
+    for (int r = 0; r < P.R_max; ++r) {
+      if (r < R) {
+        pref += eq ? 1 : wv[r];
+        rb[r + 1] = (int)(((long long)n * pref) / den);
+      } else {
+        rb[r + 1] = n;
+      }
     }
-    for (int r = R + 1; r < RS; ++r) rb[r] = n;
   }
   // Virtual slot jj claims replica (key, r); with duplicates the lowest slot wins.
-  for (int jj = tid; jj < NS; jj += kHistThreads) {
+  for (int jj = tid; jj < NS; jj += kAssignThreads) {
     const int j = jj / P.n_src, src = jj % P.n_src;
     const int e = P.slot_expert[j], r = P.slot_replica[j];
-    if (e >= 0 && e < P.E && r >= 0 && r < P.R_max) atomicMin(&rep_slot[(src * P.E + e) * P.R_max + r], jj);
+    if (e >= 0 && e < P.E && r >= 0 && r < P.R_max) atomicMin(&s_rs[(src * P.E + e) * P.R_max + r], jj);
   }
   __syncthreads();
-  for (int jj = tid; jj < NS; jj += kHistThreads) {
+  for (int i = tid; i < NK * RS; i += kAssignThreads) rep_begin[i] = s_rb[i];
+  for (int jj = tid; jj < NS; jj += kAssignThreads) {
     const int j = jj / P.n_src, src = jj % P.n_src;
     const int e = P.slot_expert[j], r = P.slot_replica[j];
     int c = 0;
     bool ok = false;
-    if (e >= 0 && e < P.E && r >= 0) {
-      int dummy = 0;
-      const int R = clamp_nrep(P, e, dummy);
+    if (e >= 0 && e < P.E && r >= 0 && r < s_nrep[e]) {
       const int kk = src * P.E + e;
-      if (r < R && rep_slot[kk * P.R_max + r] == jj) {
-        const int32_t* rb = rep_begin + (int64_t)kk * RS;
-        c = rb[r + 1] - rb[r];
+      if (s_rs[kk * P.R_max + r] == jj) {
+        c = s_rb[kk * RS + r + 1] - s_rb[kk * RS + r];
         ok = true;
       }
     }
@@ -232,27 +249,26 @@ __global__ __launch_bounds__(kHistThreads) void assign_kernel(const int32_t* __r
     s_cnt[jj] = c;
   }
   if (err) atomicAdd(&s_err, err);
-  __syncthreads();
-  for (int i = tid; i < NK * P.R_max; i += kHistThreads) {
+  for (int i = tid; i < NK * P.R_max; i += kAssignThreads) {
     // replicas beyond R_e, and replicas held by no (valid) slot, are remote
     const int e = (i / P.R_max) % P.E, r = i % P.R_max;
-    int dummy = 0;
-    const int R = clamp_nrep(P, e, dummy);
-    if (rep_slot[i] == INT_MAX || r >= R) rep_slot[i] = -1;
+    const int v = s_rs[i];
+    rep_slot[i] = (v == INT_MAX || r >= s_nrep[e]) ? -1 : v;
   }
+  __syncthreads();
   int carry = 0;
-  for (int j0 = 0; j0 < NS; j0 += kHistThreads) {
+  for (int j0 = 0; j0 < NS; j0 += kAssignThreads) {
     const int jj = j0 + tid;
     const int v = jj < NS ? s_cnt[jj] : 0;
     int total;
-    const int incl = block_inclusive_scan(v, s_tmp, total);
+    const int incl = block_inclusive_scan<NW>(v, s_tmp, total);
     if (jj < NS) s_off[jj] = carry + incl - v;
     carry += total;
   }
   if (tid == 0) s_off[NS] = carry;
   __syncthreads();
-  for (int jj = tid; jj <= NS; jj += kHistThreads) vslot_offset[jj] = s_off[jj];
-  for (int j = tid; j < P.S; j += kHistThreads) {
+  for (int jj = tid; jj <= NS; jj += kAssignThreads) vslot_offset[jj] = s_off[jj];
+  for (int j = tid; j < P.S; j += kAssignThreads) {
     int c = 0;
     for (int src = 0; src < P.n_src; ++src) c += s_cnt[j * P.n_src + src];
     slot_count[j] = c;
@@ -718,8 +734,12 @@ int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int
   int32_t* status = (int32_t*)ws;
   int32_t* rep_slot = (int32_t*)((char*)ws + kWsRepSlotOff);
   int32_t* vslot = (int32_t*)((char*)ws + kWsVSlotOff);
-  hipLaunchKernelGGL(assign_kernel, dim3(1), dim3(kHistThreads), 0, (hipStream_t)stream, counts, P, rep_begin,
-                     slot_count, slot_offset, vslot, rep_slot, status);
+  if (n_src * plan->E <= 256)
+    hipLaunchKernelGGL((assign_kernel<256, 256>), dim3(1), dim3(256), 0, (hipStream_t)stream, counts, P, rep_begin,
+                       slot_count, slot_offset, vslot, rep_slot, status);
+  else
+    hipLaunchKernelGGL((assign_kernel<1024, FOREMOE_MAX_EXPERTS>), dim3(1), dim3(1024), 0, (hipStream_t)stream, counts,
+                       P, rep_begin, slot_count, slot_offset, vslot, rep_slot, status);
   return check_launch("foremoe_assign_replicas");
 }
 
