@@ -10,12 +10,18 @@ step = one micro-step through every step of the path:
   -> combine -> combine_bwd -> down dgrad (+SwiGLU') -> gate/up dgrad
   -> gate/up wgrad -> down wgrad -> permute_bwd
 
+The two weight-gradient GEMMs run on a second stream, each beside the
+data-gradient GEMM that does not feed it (down wgrad beside down dgrad,
+gate/up wgrad beside gate/up dgrad); --no-overlap runs all twelve phases on
+one stream.
+
 All inputs are resident in HBM before timing. Each ABI call is bracketed by
 HIP events on the stream it runs on; the dominant kernel's average duration
-gives the roofline line. The fp64 CPU oracle is timed on one micro-step as
-the CPU baseline.
+in the timed region gives the roofline line. The same steps are run once
+more one kernel after another, for every phase's own duration. The fp64 CPU
+oracle is timed on one micro-step as the CPU baseline.
 
-    python bench.py [--gpus 1] [--steps 32] [--warmup 16] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps 32] [--warmup 16] [--no-cpu-baseline] [--no-overlap]
 """
 from __future__ import annotations
 
@@ -47,6 +53,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="run the weight-gradient GEMMs on the main stream instead of beside the data gradients")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three plain 1 GiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
@@ -133,52 +141,72 @@ def main() -> int:
         if rc != 0:
             raise _lib.ForeMoEError(rc, what)
 
-    def run_step(i, ev=None):
+    side = torch.cuda.Stream(dev)  # default priority, like every stream here
+    ssp = side.cuda_stream
+
+    def run_step(i, ev=None, overlap=False):
+        """One micro-step. With overlap the two weight-gradient GEMMs run on
+        the side stream, each beside the data-gradient GEMM that does not
+        feed it: down wgrad (needs dy_perm) beside down dgrad, gate/up wgrad
+        (needs d_au) beside gate/up dgrad. Both share one workspace, so they
+        stay ordered on that one stream; the main stream waits for the side
+        stream before the step ends, so the next step's buffers are free.
+        ev maps each phase to a (begin, end) event pair recorded on the
+        stream the phase runs on."""
         ms = mss[i % n_micro]
         S = ms["S"]
         so = P["slot_offset"]
         widx, gidx = ms["plan"].slot_widx.data_ptr(), ms["plan"].slot_gidx.data_ptr()
         cp = ctypes.byref(ms["cplan"])
 
-        def mark(k):
+        def call(phase, st, rc_fn):
             if ev is not None:
-                ev[k].record(stream)
-        mark(0)
-        chk(lib.foremoe_histogram(ms["ids"].data_ptr(), T, K, E, P["counts"], P["ws"], wsz, sp), "histogram")
-        mark(1)
-        chk(lib.foremoe_assign_replicas(P["counts"], cp, P["rep_begin"], P["slot_count"], so, P["ws"], wsz, sp),
-            "assign")
-        mark(2)
-        chk(lib.foremoe_permute(ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so,
-                                n_cap, P["x_perm"], P["r2p"], P["p2r"], P["ws"], wsz, sp), "permute")
-        mark(3)
-        chk(lib.foremoe_ffn_gate_up_fwd(P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"],
-                                        P["au"], sp), "gate_up_fwd")
-        mark(4)
-        chk(lib.foremoe_ffn_down_fwd(P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], sp),
-            "down_fwd")
-        mark(5)
-        chk(lib.foremoe_combine(P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap, P["y"], BF16,
-                                sp), "combine")
-        mark(6)
-        chk(lib.foremoe_combine_bwd(ms["dy"].data_ptr(), P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K,
-                                    d, n_cap, P["dy_perm"], P["dgates"], sp), "combine_bwd")
-        mark(7)
-        chk(lib.foremoe_ffn_down_dgrad(P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap,
-                                       P["d_au"], sp), "down_dgrad")
-        mark(8)
-        chk(lib.foremoe_ffn_gate_up_dgrad(P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap,
-                                          P["dx_perm"], sp), "gate_up_dgrad")
-        mark(9)
-        chk(lib.foremoe_ffn_gate_up_wgrad(P["d_au"], P["x_perm"], BF16, d, F, S, so, gidx, G, n_cap, P["dwgu"],
-                                          P["wws"], wwsz, sp), "gate_up_wgrad")
-        mark(10)
-        chk(lib.foremoe_ffn_down_wgrad(P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"],
-                                       P["wws"], wwsz, sp), "down_wgrad")
-        mark(11)
-        chk(lib.foremoe_permute_bwd(P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], BF16, sp),
-            "permute_bwd")
-        mark(12)
+                ev[phase][0].record(st)
+            chk(rc_fn(st.cuda_stream), phase)
+            if ev is not None:
+                ev[phase][1].record(st)
+
+        def gate_up_wgrad(st):
+            call("gate_up_wgrad", st, lambda q: lib.foremoe_ffn_gate_up_wgrad(
+                P["d_au"], P["x_perm"], BF16, d, F, S, so, gidx, G, n_cap, P["dwgu"], P["wws"], wwsz, q))
+
+        def down_wgrad(st):
+            call("down_wgrad", st, lambda q: lib.foremoe_ffn_down_wgrad(
+                P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"], P["wws"], wwsz, q))
+
+        call("histogram", stream, lambda q: lib.foremoe_histogram(ms["ids"].data_ptr(), T, K, E, P["counts"],
+                                                                    P["ws"], wsz, q))
+        call("assign_replicas", stream, lambda q: lib.foremoe_assign_replicas(
+            P["counts"], cp, P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
+        call("permute", stream, lambda q: lib.foremoe_permute(
+            ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
+            P["r2p"], P["p2r"], P["ws"], wsz, q))
+        call("gate_up_fwd", stream, lambda q: lib.foremoe_ffn_gate_up_fwd(
+            P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"], P["au"], q))
+        call("down_fwd", stream, lambda q: lib.foremoe_ffn_down_fwd(
+            P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], q))
+        call("combine", stream, lambda q: lib.foremoe_combine(
+            P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap, P["y"], BF16, q))
+        call("combine_bwd", stream, lambda q: lib.foremoe_combine_bwd(
+            ms["dy"].data_ptr(), P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap,
+            P["dy_perm"], P["dgates"], q))
+        if overlap:
+            side.wait_stream(stream)
+            down_wgrad(side)
+        call("down_dgrad", stream, lambda q: lib.foremoe_ffn_down_dgrad(
+            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["d_au"], q))
+        if overlap:
+            side.wait_stream(stream)
+            gate_up_wgrad(side)
+        call("gate_up_dgrad", stream, lambda q: lib.foremoe_ffn_gate_up_dgrad(
+            P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["dx_perm"], q))
+        if not overlap:
+            gate_up_wgrad(stream)
+            down_wgrad(stream)
+        call("permute_bwd", stream, lambda q: lib.foremoe_permute_bwd(
+            P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], BF16, q))
+        if overlap:
+            stream.wait_stream(side)
 
     # ---- realised per-micro-step sizes (read back once, outside the timed region)
     Ns, Gs = [], []
@@ -191,25 +219,45 @@ def main() -> int:
         gidx = mss[i]["plan"].slot_gidx.cpu().numpy()
         Gs.append(int(len(set(gidx[sc > 0].tolist()))))
 
+    overlap = not args.no_overlap
     for i in range(args.warmup):
-        run_step(i)
+        run_step(i, overlap=overlap)
     torch.cuda.synchronize()
 
-    # ---- timed region
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(PHASES) + 1)] for _ in range(args.steps)]
+    def new_events():
+        return {p: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for p in PHASES}
+
+    def phase_sums(evs):
+        return {p: sum(ev[p][0].elapsed_time(ev[p][1]) for ev in evs) for p in PHASES}
+
+    # ---- timed region: the step as it runs (backward GEMMs overlapped)
+    evs = [new_events() for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for s in range(args.steps):
-        run_step(s, evs[s])
+        run_step(s, evs[s], overlap=overlap)
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
-    phase_ms = {p: 0.0 for p in PHASES}
-    for s in range(args.steps):
-        for k, p in enumerate(PHASES):
-            phase_ms[p] += evs[s][k].elapsed_time(evs[s][k + 1])
+    live_ms = phase_sums(evs)
+
+    # ---- the same steps once more, one kernel after another, so that every
+    # phase's duration is its own (the overlapped ones share the chip)
+    if overlap:
+        evs_seq = [new_events() for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        seq0, seq1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        seq0.record(stream)
+        for s in range(args.steps):
+            run_step(s, evs_seq[s])
+        seq1.record(stream)
+        torch.cuda.synchronize()
+        phase_ms = phase_sums(evs_seq)
+        seq_ms_per_step = seq0.elapsed_time(seq1) / args.steps
+    else:
+        phase_ms, seq_ms_per_step = live_ms, ms_per_step
 
     # ---- algorithmic work of the timed steps
     work = {p: {"flop": 0.0, "bytes": 0.0} for p in PHASES}
@@ -233,28 +281,32 @@ def main() -> int:
         work["down_wgrad"]["bytes"] += 2.0 * (N * d + N * F) + 2.0 * g * d * F * 4
         work["permute_bwd"]["bytes"] += acc.permute_bwd_bytes(N, T, K, d, 2, 2)
 
-    kernels = {}
-    for p in PHASES:
-        t_s = phase_ms[p] / 1e3
+    def rates(p, ms):
+        t_s = ms / 1e3
         fl, by = work[p]["flop"], work[p]["bytes"]
         t_mfma = fl / acc.PEAK_BF16_DENSE_FLOPS
         t_hbm = by / acc.PEAK_HBM_BYTES_PER_S
         if fl > 0 and t_mfma >= t_hbm:
-            bound, ach, peak, unit = "mfma", fl / t_s / 1e12, acc.PEAK_BF16_DENSE_FLOPS / 1e12, "TFLOP/s"
-        else:
-            bound, ach, peak, unit = "hbm", by / t_s / 1e9, acc.PEAK_HBM_BYTES_PER_S / 1e9, "GB/s"
-        kernels[p] = {"us_per_step": round(phase_ms[p] * 1e3 / args.steps, 2), "bound": bound,
+            return "mfma", fl / t_s / 1e12, acc.PEAK_BF16_DENSE_FLOPS / 1e12, "TFLOP/s"
+        return "hbm", by / t_s / 1e9, acc.PEAK_HBM_BYTES_PER_S / 1e9, "GB/s"
+
+    kernels = {}
+    for p in PHASES:
+        t_s = phase_ms[p] / 1e3
+        fl, by = work[p]["flop"], work[p]["bytes"]
+        bound, ach, peak, unit = rates(p, phase_ms[p])
+        kernels[p] = {"us_per_step": round(phase_ms[p] * 1e3 / args.steps, 2),
+                      "us_in_timed_step": round(live_ms[p] * 1e3 / args.steps, 2), "bound": bound,
                       "achieved": round(ach, 2), "unit": unit, "frac": round(ach / peak, 4),
                       "tflops": round(fl / t_s / 1e12, 2) if fl else None,
                       "gbs": round(by / t_s / 1e9, 1)}
+    # the dominant single-launch kernel, timed live in the timed region on
+    # the stream it runs on
     dom = max((p for p in PHASES if p in SINGLE_LAUNCH), key=lambda p: phase_ms[p])
-    kd = kernels[dom]
-    per_launch_us = phase_ms[dom] * 1e3 / args.steps
-    roofline = {"bound": kd["bound"], "achieved": kd["achieved"],
-                "peak": round((acc.PEAK_BF16_DENSE_FLOPS / 1e12) if kd["bound"] == "mfma"
-                              else acc.PEAK_HBM_BYTES_PER_S / 1e9, 1),
-                "unit": kd["unit"], "frac": kd["frac"], "traffic": measured_traffic(dom), "kernel": dom,
-                "avg_launch_us": round(per_launch_us, 2)}
+    bound, ach, peak, unit = rates(dom, live_ms[dom])
+    roofline = {"bound": bound, "achieved": round(ach, 2), "peak": round(peak, 1), "unit": unit,
+                "frac": round(ach / peak, 4), "traffic": measured_traffic(dom), "kernel": dom,
+                "avg_launch_us": round(live_ms[dom] * 1e3 / args.steps, 2)}
 
     ffn = ["gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad"]
     ffn_flop = sum(work[p]["flop"] for p in ffn)
@@ -282,7 +334,9 @@ def main() -> int:
         "config": {"workload": "qwen3-30b-a3b EP=8 rank share, policy-update micro-step (fwd+bwd)",
                    "T": T, "d": d, "F": F, "E": E, "K": K, "local_experts": G, "slots": S_max,
                    "micro_steps": n_micro, "n_pairs_mean": round(float(np.mean(Ns)), 1),
-                   "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns))},
+                   "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns)),
+                   "backward_overlap": overlap},
+        "ms_per_step_sequential": round(seq_ms_per_step, 4),
         "roofline": roofline,
         "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),
         "grouped_ffn_frac_bf16_peak": round(ffn_flop / ffn_s / acc.PEAK_BF16_DENSE_FLOPS, 4),
