@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
+    ap.add_argument("--no-split", action="store_true",
+                    help="run the row GEMMs without the workspace (no K split of a partial last round of tiles)")
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the weight-gradient GEMMs on the main stream instead of beside the data gradients")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -128,10 +130,12 @@ def main() -> int:
         y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d), dy_perm=z(n_cap, d), dgates=z(T, K, dt=torch.float32),
         d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d), dx=z(T, d),
         dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32),
-        wws=api.wgrad_workspace(d, F, dev))
+        wws=api.wgrad_workspace(d, F, dev), rws=api.ffn_workspace(dev))
     P = {k: v.data_ptr() for k, v in buf.items()}
     wsz = buf["ws"].numel()
     wwsz = buf["wws"].numel()
+    # row-GEMM workspace (tail split of a partial last round of tiles)
+    rws, rwsz = (None, 0) if args.no_split else (P["rws"], buf["rws"].numel())
     stream = torch.cuda.current_stream(dev)
     sp = stream.cuda_stream
     BF16 = _lib.BF16
@@ -182,9 +186,9 @@ def main() -> int:
             ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
             P["r2p"], P["p2r"], P["ws"], wsz, q))
         call("gate_up_fwd", stream, lambda q: lib.foremoe_ffn_gate_up_fwd(
-            P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"], P["au"], q))
+            P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"], P["au"], rws, rwsz, q))
         call("down_fwd", stream, lambda q: lib.foremoe_ffn_down_fwd(
-            P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], q))
+            P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], rws, rwsz, q))
         call("combine", stream, lambda q: lib.foremoe_combine(
             P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap, P["y"], BF16, q))
         call("combine_bwd", stream, lambda q: lib.foremoe_combine_bwd(
@@ -194,12 +198,12 @@ def main() -> int:
             side.wait_stream(stream)
             down_wgrad(side)
         call("down_dgrad", stream, lambda q: lib.foremoe_ffn_down_dgrad(
-            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["d_au"], q))
+            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["d_au"], rws, rwsz, q))
         if overlap:
             side.wait_stream(stream)
             gate_up_wgrad(side)
         call("gate_up_dgrad", stream, lambda q: lib.foremoe_ffn_gate_up_dgrad(
-            P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["dx_perm"], q))
+            P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["dx_perm"], rws, rwsz, q))
         if not overlap:
             gate_up_wgrad(stream)
             down_wgrad(stream)
@@ -335,7 +339,7 @@ def main() -> int:
                    "T": T, "d": d, "F": F, "E": E, "K": K, "local_experts": G, "slots": S_max,
                    "micro_steps": n_micro, "n_pairs_mean": round(float(np.mean(Ns)), 1),
                    "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns)),
-                   "backward_overlap": overlap},
+                   "backward_overlap": overlap, "tail_split": not args.no_split},
         "ms_per_step_sequential": round(seq_ms_per_step, 4),
         "roofline": roofline,
         "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),

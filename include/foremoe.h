@@ -212,18 +212,32 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
  * 0 <= S <= FOREMOE_MAX_SLOTS.
  * foremoe_grouped_ffn_fwd = foremoe_ffn_gate_up_fwd then foremoe_ffn_down_fwd;
  * each of these two is a single kernel launch.
+ *
+ * workspace (optional, these and the input-gradient calls below): NULL, or
+ * caller-owned device memory of at least foremoe_ffn_workspace_size()
+ * bytes, 256-byte aligned, zero-filled before its first use (the library
+ * leaves its counters at zero after every call). With it, a last round of
+ * output tiles that would occupy only part of the GPU is cut along K into
+ * up to 4 pieces, each computed by its own workgroup; the last piece to
+ * finish adds the pieces' fp32 partial sums in piece order and writes the
+ * tile. Results are deterministic either way and equal with and without the
+ * workspace up to the fp32 summation order. Calls that share a workspace
+ * must not overlap in time (same stream, or ordered by events). Too small or
+ * misaligned: FOREMOE_EINVAL, nothing launched. Ignored for f32.
  */
+size_t foremoe_ffn_workspace_size(void);
+
 int foremoe_grouped_ffn_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
                             int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
                             int32_t W, const void* w_gate_up, const void* w_down, int64_t n_cap,
-                            void* h, void* y_perm, void* save_au, void* stream);
+                            void* h, void* y_perm, void* save_au, void* workspace, size_t ws_bytes, void* stream);
 int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
                             int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
                             int32_t W, const void* w_gate_up, int64_t n_cap,
-                            void* h, void* save_au, void* stream);
+                            void* h, void* save_au, void* workspace, size_t ws_bytes, void* stream);
 int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t F,
                          int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
-                         int32_t W, const void* w_down, int64_t n_cap, void* y_perm, void* stream);
+                         int32_t W, const void* w_down, int64_t n_cap, void* y_perm, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Step 4, input gradient (chain rule of the forward above):
@@ -232,22 +246,23 @@ int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t 
  * with silu'(a) = s + a s (1 - s), s = 1 / (1 + exp(-a)).
  * dy_perm [n_cap, d]; save_au [n_cap, 2F] from the forward;
  * d_au    [n_cap, 2F] out: dA in columns [0, F), dU in [F, 2F);
- * dx_perm [n_cap, d] out. Same dtype and shape rules as the forward.
+ * dx_perm [n_cap, d] out. Same dtype, shape and workspace rules as the
+ * forward.
  * = foremoe_ffn_down_dgrad then foremoe_ffn_gate_up_dgrad (one launch each).
  */
 int foremoe_grouped_ffn_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype,
                               int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
                               const int32_t* slot_widx, int32_t W, const void* w_gate_up,
                               const void* w_down, int64_t n_cap, void* d_au, void* dx_perm,
-                              void* stream);
+                              void* workspace, size_t ws_bytes, void* stream);
 int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype,
                            int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
                            const int32_t* slot_widx, int32_t W, const void* w_down,
-                           int64_t n_cap, void* d_au, void* stream);
+                           int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes, void* stream);
 int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F,
                               int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
                               int32_t W, const void* w_gate_up, int64_t n_cap, void* dx_perm,
-                              void* stream);
+                              void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Step 4, weight gradient with main-expert accumulation (Sec. 6.2, Copy-in:

@@ -50,18 +50,19 @@ SIGNATURES = {
     "foremoe_assign_replicas": (ctypes.c_int, [c_p, PPlan, c_p, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_permute": (ctypes.c_int, [c_p, c_i32, c_i64, c_i32, c_p, c_i32, PPlan, c_p, c_p, c_i64,
                                        c_p, c_p, c_p, c_p, c_sz, c_p]),
+    "foremoe_ffn_workspace_size": (c_sz, []),
     "foremoe_grouped_ffn_fwd": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_p,
-                                               c_i64, c_p, c_p, c_p, c_p]),
+                                               c_i64, c_p, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_gate_up_fwd": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_i64,
-                                               c_p, c_p, c_p]),
+                                               c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_down_fwd": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_i64,
-                                            c_p, c_p]),
+                                            c_p, c_p, c_sz, c_p]),
     "foremoe_grouped_ffn_dgrad": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
-                                                 c_p, c_i64, c_p, c_p, c_p]),
+                                                 c_p, c_i64, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_down_dgrad": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
-                                              c_i64, c_p, c_p]),
+                                              c_i64, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_gate_up_dgrad": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
-                                                 c_i64, c_p, c_p]),
+                                                 c_i64, c_p, c_p, c_sz, c_p]),
     "foremoe_wgrad_workspace_size": (c_sz, [c_i32, c_i32]),
     "foremoe_grouped_ffn_wgrad": (ctypes.c_int, [c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p,
                                                  c_i32, c_i64, c_p, c_p, c_p, c_sz, c_p]),

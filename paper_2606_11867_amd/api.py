@@ -153,8 +153,22 @@ def permute(x: torch.Tensor, ids: torch.Tensor, plan: DevicePlan, rep_begin: tor
     return x_perm, row_to_pair, pair_to_row
 
 
+def ffn_workspace(device) -> torch.Tensor:
+    """Scratch that lets the row GEMMs cut a partial last round of tiles
+    along K (foremoe_ffn_workspace_size() bytes for the current device).
+    Zero-filled here, as its arrival counters must be before first use; each
+    call leaves them zero again."""
+    n = _lib.load().foremoe_ffn_workspace_size()
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def _ws(ws: Optional[torch.Tensor]):
+    return (None, 0) if ws is None else (ws.data_ptr(), ws.numel())
+
+
 def grouped_ffn_fwd(x_perm: torch.Tensor, slot_offset: torch.Tensor, slot_widx: torch.Tensor,
-                    w_gate_up: torch.Tensor, w_down: torch.Tensor, save: bool = True):
+                    w_gate_up: torch.Tensor, w_down: torch.Tensor, save: bool = True,
+                    ws: Optional[torch.Tensor] = None):
     n_cap, d = x_perm.shape
     W, F2, _ = w_gate_up.shape
     F = F2 // 2
@@ -166,13 +180,15 @@ def grouped_ffn_fwd(x_perm: torch.Tensor, slot_offset: torch.Tensor, slot_widx: 
     check(_lib.load().foremoe_grouped_ffn_fwd(_ptr(x_perm), _dt(x_perm), d, F, S, _ptr(slot_offset),
                                               _ptr(slot_widx), W, _ptr(w_gate_up), _ptr(w_down), n_cap,
                                               h.data_ptr(), y_perm.data_ptr(),
-                                              None if save_au is None else save_au.data_ptr(), _stream(dev)),
+                                              None if save_au is None else save_au.data_ptr(), *_ws(ws),
+                                              _stream(dev)),
           "foremoe_grouped_ffn_fwd")
     return h, y_perm, save_au
 
 
 def grouped_ffn_dgrad(dy_perm: torch.Tensor, save_au: torch.Tensor, slot_offset: torch.Tensor,
-                      slot_widx: torch.Tensor, w_gate_up: torch.Tensor, w_down: torch.Tensor):
+                      slot_widx: torch.Tensor, w_gate_up: torch.Tensor, w_down: torch.Tensor,
+                      ws: Optional[torch.Tensor] = None):
     n_cap, d = dy_perm.shape
     W, F2, _ = w_gate_up.shape
     F = F2 // 2
@@ -183,7 +199,7 @@ def grouped_ffn_dgrad(dy_perm: torch.Tensor, save_au: torch.Tensor, slot_offset:
     check(_lib.load().foremoe_grouped_ffn_dgrad(_ptr(dy_perm), _ptr(save_au), _dt(dy_perm), d, F, S,
                                                 _ptr(slot_offset), _ptr(slot_widx), W, _ptr(w_gate_up),
                                                 _ptr(w_down), n_cap, d_au.data_ptr(), dx_perm.data_ptr(),
-                                                _stream(dev)), "foremoe_grouped_ffn_dgrad")
+                                                *_ws(ws), _stream(dev)), "foremoe_grouped_ffn_dgrad")
     return d_au, dx_perm
 
 

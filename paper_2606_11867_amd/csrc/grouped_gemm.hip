@@ -464,6 +464,8 @@ struct RowsArgs {
   int64_t ldc2;
   const uint16_t* AU;  // input gradient: saved [A | U]
   int64_t ldau;
+  float* sk_part;      // split workspace: one partial tile per workgroup, or NULL
+  unsigned* sk_count;  // arrival count per tile of the split round (zero between calls)
 };
 
 // Per-slot m-tile prefix in LDS: s_mt[j] = m-tiles of slots before j.
@@ -682,6 +684,109 @@ __device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& co
   }
 }
 
+// Tail split of the row GEMM (the last, partial round of tiles cut along
+// K): the partial sums of a piece stay in the MFMA register layout, one
+// workspace slot per workgroup, then per wave, then per float4 index with
+// the 64 lanes consecutive, so every store and load moves a whole 1 KiB.
+//
+// The pieces of a tile may run on different XCDs, whose L2 caches are not
+// coherent with each other. The partial sums are therefore stored and loaded
+// with device-scope coherence (the SC1 cache-policy bit: the store writes
+// through to memory, the load does not take a stale L2 line), and a store is
+// complete once the wave's vector-memory counter has drained. No device-wide
+// fence is needed: such a fence would write back and invalidate the whole
+// L2 of the XCD, evicting the operand tiles that every other workgroup there
+// is using.
+#ifndef FM_SPLIT_MAX
+#define FM_SPLIT_MAX 4
+#endif
+#ifndef FM_SPLIT_MIN_K
+#define FM_SPLIT_MIN_K 32
+#endif
+constexpr int kSplitMax = FM_SPLIT_MAX;    // pieces per tile at most (2..4)
+constexpr int kSplitMinK = FM_SPLIT_MIN_K;  // k-steps a tile needs before it is split
+constexpr int kSplitRegionKiB = 16;  // LDS per wave for the pieces in flight
+constexpr int kCoherentDevice = 16;  // cache policy of buffer accesses: SC1
+
+template <class CoreT, int NW>
+__device__ __forceinline__ uint32_t split_offset(int slot, int wave, int e) {
+  constexpr int PER_WAVE = CoreT::MB * CoreT::NB * 4 * 64;  // float4 per wave
+  return (uint32_t)((((uint32_t)slot * NW + wave) * PER_WAVE + (uint32_t)e * 64 + lane64()) * 16u);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t split_rsrc(float* part, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(part, (short)0, (int)bytes, 0x00020000);
+}
+
+// One wavefront moves 64 x 16 bytes of the split workspace into LDS (lane l
+// to lds_wave_base + 16 l), device-coherently.
+__device__ __forceinline__ void split_dma16(__amdgpu_buffer_rsrc_t rs, uint32_t lds_wave_base, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(uintptr_t)lds_wave_base, 16,
+                                           voff, 0, 0, kCoherentDevice);
+}
+
+template <class CoreT, int NW>
+__device__ __forceinline__ void split_store(__amdgpu_buffer_rsrc_t rs, int slot, int wave, const CoreT& core) {
+#pragma unroll
+  for (int i = 0; i < CoreT::MB; ++i)
+#pragma unroll
+    for (int j = 0; j < CoreT::NB; ++j)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        i32x4 v;
+        v.x = __float_as_int(core.acc[i][j][4 * c]);
+        v.y = __float_as_int(core.acc[i][j][4 * c + 1]);
+        v.z = __float_as_int(core.acc[i][j][4 * c + 2]);
+        v.w = __float_as_int(core.acc[i][j][4 * c + 3]);
+        __builtin_amdgcn_raw_buffer_store_b128(v, rs, split_offset<CoreT, NW>(slot, wave, (i * CoreT::NB + j) * 4 + c),
+                                               0, kCoherentDevice);
+      }
+}
+
+// acc = piece 0 + piece 1 + ... + piece SPLIT-1, added in this order for
+// every element, all read back from the workspace (this workgroup's own
+// piece included), so the result does not depend on which piece arrived
+// last. The pieces travel workspace -> LDS by asynchronous loads that need
+// no registers (up to 16 KiB per wave in flight, in the wave's own part of
+// the free operand ring), then LDS -> registers for the additions. (Taking
+// the own piece from the registers instead saves one read but makes the
+// compiler spill the accumulators.) `rs` covers the tile's SPLIT slots;
+// `wl` is the wave's LDS region.
+template <int NW, int SPLIT, class CoreT>
+__device__ __forceinline__ void split_sum(__amdgpu_buffer_rsrc_t rs, int wave, char* wl, CoreT& core) {
+  constexpr int NE = CoreT::MB * CoreT::NB * 4;  // float4 groups per lane
+  constexpr int GR = kSplitRegionKiB / SPLIT;    // groups per round
+  const uint32_t wbase = lds_addr(wl);
+  static_for<0, (NE + GR - 1) / GR>([&](auto rc) {
+    constexpr int e0 = decltype(rc)::value * GR;
+    constexpr int ne = NE - e0 < GR ? NE - e0 : GR;
+#pragma unroll
+    for (int g = 0; g < ne; ++g)
+#pragma unroll
+      for (int pc = 0; pc < SPLIT; ++pc)
+        split_dma16(rs, wbase + (pc * GR + g) * 1024, split_offset<CoreT, NW>(pc, wave, e0 + g));
+    wait_vm<0>();  // this wave's loads have landed in its LDS region
+#pragma unroll
+    for (int g = 0; g < ne; ++g) {
+      const int e = e0 + g, c = e % 4, j = (e / 4) % CoreT::NB, i = e / 4 / CoreT::NB;
+      float4 t = *reinterpret_cast<const float4*>(wl + g * 1024 + lane64() * 16);
+#pragma unroll
+      for (int pc = 1; pc < SPLIT; ++pc) {
+        const float4 x = *reinterpret_cast<const float4*>(wl + (pc * GR + g) * 1024 + lane64() * 16);
+        t.x += x.x;
+        t.y += x.y;
+        t.z += x.z;
+        t.w += x.w;
+      }
+      core.acc[i][j][4 * c] = t.x;
+      core.acc[i][j][4 * c + 1] = t.y;
+      core.acc[i][j][4 * c + 2] = t.z;
+      core.acc[i][j][4 * c + 3] = t.w;
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): LDS reads done before the region is refilled
+  });
+}
+
 template <int BM, int BN, int BK, int NS, int WGM, int WGN, bool B_KMAJ, int EPI>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   constexpr bool SW = (EPI == kEpiSwigluFwd);
@@ -693,6 +798,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
   __shared__ int s_mt[FOREMOE_MAX_SLOTS + 1];
   __shared__ int s_tmp[16];
+  __shared__ int s_last;
 
   build_slot_tiles<BM>(a.slot_offset, a.S, a.n_cap, s_mt, s_tmp);
   const int n_tiles = a.N / BN;
@@ -705,7 +811,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   CoreT core;
   const typename CoreT::template Offsets<AT, BT, BK> offs(wm, wn);
 
-  for (int t = xcd_virtual_id(); t < total; t += gridDim.x) {
+  // Whole rounds of G tiles, one tile per workgroup per round. When the last
+  // round is partial (r < G tiles) and a workspace is given, its tiles are
+  // cut along K into `split` pieces each, so that r * split workgroups share
+  // it instead of r. Workgroups with consecutive virtual ids (one XCD) take
+  // the pieces of one tile.
+  const int G = gridDim.x;
+  const int v = xcd_virtual_id();
+  const int r = total % G;
+  int split = 1;
+  if (a.sk_part && r > 0 && KT >= kSplitMinK) {
+    split = G / r;
+    split = split < kSplitMax ? split : kSplitMax;
+  }
+  const int dp = split > 1 ? total - r : total;
+  // One output tile, k-steps [kb, kb + nk). With split > 1 this is piece q
+  // of a tile cut along K: the partial sums go to the workspace and the last
+  // piece to arrive adds all pieces in piece order and writes the tile.
+  auto run_tile = [&](int t, int kb, int nk, int q, int split) {
     const int mtg = t / n_tiles, nt = t % n_tiles;
     int lo = 0, hi = a.S - 1;
     while (lo < hi) {
@@ -720,7 +843,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     const int mrel = (mtg - s_mt[j]) * BM;  // first tile row relative to the slot
     const int64_t m0 = rbeg + mrel;
     const int w = a.slot_widx[j];
-    if (w < 0 || w >= a.W) continue;  // invalid weight index: rows left unwritten
+    if (w < 0 || w >= a.W) return;  // invalid weight index: rows left unwritten (every piece skips)
     const int n0 = nt * BN;           // first output column of the tile grid
     const int f0 = nt * (BN / 2);     // SwiGLU: first H column
 
@@ -755,9 +878,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     }
     auto issue = [&](int kt, int p) {
       // stages past the last load nothing (zero-size resources)
-      const bool live = kt < KT;
+      const bool live = kt < nk;
       const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
-      const uint32_t k0 = live ? (uint32_t)(kt * BK) : 0u;
+      const uint32_t k0 = live ? (uint32_t)((kb + kt) * BK) : 0u;
       if (p < AT::PER_WAVE) {
         AT::issue(buf_rsrc(abase + k0, live ? abytes - 2u * k0 : 0u), sa, va[p], p);
       } else if constexpr (B_KMAJ) {
@@ -770,12 +893,41 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     };
 
     core.zero();
-    pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, KT, offs, issue);
+    pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, nk, offs, issue);
+    if (split > 1) {
+      // piece q of tail tile t - dp is computed by workgroup v - q + q' for
+      // piece q'; each keeps its partial sums in its own workspace slot
+      const __amdgpu_buffer_rsrc_t rs = split_rsrc(a.sk_part, (uint32_t)G * (BM * BN * 4));
+      split_store<CoreT, NW>(rs, v, wave, core);
+      wait_vm<0>();  // this wave's partial sums have reached memory
+      __syncthreads();
+      if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[t - dp], 1u) == (unsigned)(split - 1);
+      __syncthreads();
+      if (!s_last) return;
+      // the tile's pieces: slots v - q .. v - q + split - 1
+      {
+        static_assert(NW * kSplitRegionKiB * 1024 <= NS * STAGE, "split pieces must fit in the ring");
+        const __amdgpu_buffer_rsrc_t ts =
+            split_rsrc(a.sk_part + (size_t)(v - q) * (BM * BN), (uint32_t)split * (BM * BN * 4));
+        char* wl = lds + wave * (kSplitRegionKiB * 1024);
+        if (split == 2) split_sum<NW, 2>(ts, wave, wl, core);
+        else if (split == 3) split_sum<NW, 3>(ts, wave, wl, core);
+        else split_sum<NW, 4>(ts, wave, wl, core);
+      }
+      if (threadIdx.x == 0) atomicExch(&a.sk_count[t - dp], 0u);  // ready for the next call
+    }
     static_assert(NW * EpiBytes<CoreT, EPI>::PER_WAVE <= NS * STAGE, "epilogue staging must fit in the ring");
     __syncthreads();  // every wave is done reading the ring: it now stages the epilogue
     rows_epilogue<CoreT, EPI>(a, core, lds + wave * EpiBytes<CoreT, EPI>::PER_WAVE, m0 + wm * CoreT::WM, rend, n0,
                               f0, wn);
     __syncthreads();  // staging reads done before the next tile's loads overwrite the ring
+  };
+
+  for (int t = v; t < dp; t += G) run_tile(t, 0, KT, 0, 1);
+  if (split > 1 && v < r * split) {
+    const int q = v % split;
+    const int kb = q * KT / split, ke = (q + 1) * KT / split;
+    run_tile(dp + v / split, kb, ke - kb, q, split);
   }
 }
 
@@ -1256,10 +1408,21 @@ __global__ __launch_bounds__(256) void f32_wgrad_kernel(const float* __restrict_
 // ---------------------------------------------------------------------------
 int persistent_grid() { return num_cus(); }
 
+// Row-GEMM workspace (optional): arrival counters of the split round, then
+// one fp32 partial tile of up to 256 x 256 per workgroup of the grid.
+constexpr size_t kRowsCountBytes = 4096;  // counters for up to 1024 tiles
+constexpr size_t kRowsSlotBytes = (size_t)256 * 256 * 4;
+
+size_t rows_workspace_bytes() { return kRowsCountBytes + (size_t)persistent_grid() * kRowsSlotBytes; }
+
 // Row-grouped launches: 256-row tiles; 256-wide output tiles with 2 LDS
 // stages of 64-deep K slices (128 KiB), or 128-wide with 3 stages (144 KiB).
 template <int BN, bool KMAJ, int EPI>
-void launch_rows(const RowsArgs& a, hipStream_t st) {
+void launch_rows(RowsArgs a, void* ws, hipStream_t st) {
+  if (ws && persistent_grid() <= (int)(kRowsCountBytes / 4)) {
+    a.sk_count = (unsigned*)ws;
+    a.sk_part = (float*)((char*)ws + kRowsCountBytes);
+  }
   if constexpr (BN == 256) {
     constexpr int WGM = FM_ROWS_WGM, WGN = FM_ROWS_WGN;
     hipLaunchKernelGGL((gemm_rows_kernel<256, 256, FM_ROWS_BK, FM_ROWS_NS, WGM, WGN, KMAJ, EPI>),
@@ -1301,6 +1464,14 @@ static int check_ffn(const char* who, foremoe_dtype dtype, int32_t d, int32_t F,
   return FOREMOE_OK;
 }
 
+static int check_rows_ws(const char* who, const void* workspace, size_t ws_bytes) {
+  if (!workspace) return FOREMOE_OK;
+  REQUIRE(((uintptr_t)workspace & 255) == 0, "%s: workspace must be 256-byte aligned", who);
+  REQUIRE(ws_bytes >= rows_workspace_bytes(), "%s: workspace of %zu bytes, %zu needed", who, ws_bytes,
+          rows_workspace_bytes());
+  return FOREMOE_OK;
+}
+
 static dim3 f32_grid(int cols, int64_t rows) {
   return dim3((unsigned)((cols + 15) / 16), (unsigned)((rows + 15) / 16 > 0 ? (rows + 15) / 16 : 1));
 }
@@ -1309,8 +1480,10 @@ extern "C" {
 
 int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                             const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
-                            int64_t n_cap, void* h, void* save_au, void* stream) {
+                            int64_t n_cap, void* h, void* save_au, void* workspace, size_t ws_bytes, void* stream) {
   int rc = check_ffn("gate_up_fwd", dtype, d, F, S, n_cap, slot_offset);
+  if (rc) return rc;
+  rc = check_rows_ws("gate_up_fwd", workspace, ws_bytes);
   if (rc) return rc;
   if (S == 0 || n_cap == 0) return FOREMOE_OK;
   REQUIRE(x_perm && slot_widx && w_gate_up && h && W >= 1, "gate_up_fwd: NULL buffer or W < 1");
@@ -1334,7 +1507,7 @@ int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, 
     a.ldc = F;
     a.C2 = (uint16_t*)save_au;
     a.ldc2 = 2 * (int64_t)F;
-    launch_rows<256, true, kEpiSwigluFwd>(a, st);
+    launch_rows<256, true, kEpiSwigluFwd>(a, workspace, st);
   } else {
     hipLaunchKernelGGL(f32_rows_kernel<kF32GateUpFwd>, f32_grid(F, n_cap), dim3(256), 0, st, (const float*)x_perm,
                        (const float*)w_gate_up, nullptr, d, F, W, slot_offset, slot_widx, S, n_cap, (float*)h,
@@ -1345,8 +1518,10 @@ int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, 
 
 int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                          const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_down,
-                         int64_t n_cap, void* y_perm, void* stream) {
+                         int64_t n_cap, void* y_perm, void* workspace, size_t ws_bytes, void* stream) {
   int rc = check_ffn("down_fwd", dtype, d, F, S, n_cap, slot_offset);
+  if (rc) return rc;
+  rc = check_rows_ws("down_fwd", workspace, ws_bytes);
   if (rc) return rc;
   if (S == 0 || n_cap == 0) return FOREMOE_OK;
   REQUIRE(h && slot_widx && w_down && y_perm && W >= 1, "down_fwd: NULL buffer or W < 1");
@@ -1368,8 +1543,8 @@ int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t 
     a.n_cap = n_cap;
     a.C = (uint16_t*)y_perm;
     a.ldc = d;
-    if (d % 256 == 0) launch_rows<256, true, kEpiStore>(a, st);
-    else launch_rows<128, true, kEpiStore>(a, st);
+    if (d % 256 == 0) launch_rows<256, true, kEpiStore>(a, workspace, st);
+    else launch_rows<128, true, kEpiStore>(a, workspace, st);
   } else {
     hipLaunchKernelGGL(f32_rows_kernel<kF32DownFwd>, f32_grid(d, n_cap), dim3(256), 0, st, (const float*)h,
                        (const float*)w_down, nullptr, d, F, W, slot_offset, slot_widx, S, n_cap, (float*)y_perm,
@@ -1380,17 +1555,20 @@ int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t 
 
 int foremoe_grouped_ffn_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                             const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
-                            const void* w_down, int64_t n_cap, void* h, void* y_perm, void* save_au, void* stream) {
+                            const void* w_down, int64_t n_cap, void* h, void* y_perm, void* save_au, void* workspace, size_t ws_bytes, void* stream) {
   int rc = foremoe_ffn_gate_up_fwd(x_perm, dtype, d, F, S, slot_offset, slot_widx, W, w_gate_up, n_cap, h, save_au,
-                                   stream);
+                                   workspace, ws_bytes, stream);
   if (rc) return rc;
-  return foremoe_ffn_down_fwd(h, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, y_perm, stream);
+  return foremoe_ffn_down_fwd(h, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, y_perm, workspace, ws_bytes,
+                              stream);
 }
 
 int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,
                            int32_t S, const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
-                           const void* w_down, int64_t n_cap, void* d_au, void* stream) {
+                           const void* w_down, int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes, void* stream) {
   int rc = check_ffn("down_dgrad", dtype, d, F, S, n_cap, slot_offset);
+  if (rc) return rc;
+  rc = check_rows_ws("down_dgrad", workspace, ws_bytes);
   if (rc) return rc;
   if (S == 0 || n_cap == 0) return FOREMOE_OK;
   REQUIRE(dy_perm && save_au && slot_widx && w_down && d_au && W >= 1, "down_dgrad: NULL buffer or W < 1");
@@ -1414,8 +1592,8 @@ int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dty
     a.ldc = 2 * (int64_t)F;
     a.AU = (const uint16_t*)save_au;
     a.ldau = 2 * (int64_t)F;
-    if (F % 256 == 0) launch_rows<256, false, kEpiSwigluBwd>(a, st);
-    else launch_rows<128, false, kEpiSwigluBwd>(a, st);
+    if (F % 256 == 0) launch_rows<256, false, kEpiSwigluBwd>(a, workspace, st);
+    else launch_rows<128, false, kEpiSwigluBwd>(a, workspace, st);
   } else {
     hipLaunchKernelGGL(f32_rows_kernel<kF32DownDgrad>, f32_grid(F, n_cap), dim3(256), 0, st, (const float*)dy_perm,
                        (const float*)w_down, (const float*)save_au, d, F, W, slot_offset, slot_widx, S, n_cap,
@@ -1426,8 +1604,10 @@ int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dty
 
 int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                               const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
-                              int64_t n_cap, void* dx_perm, void* stream) {
+                              int64_t n_cap, void* dx_perm, void* workspace, size_t ws_bytes, void* stream) {
   int rc = check_ffn("gate_up_dgrad", dtype, d, F, S, n_cap, slot_offset);
+  if (rc) return rc;
+  rc = check_rows_ws("gate_up_dgrad", workspace, ws_bytes);
   if (rc) return rc;
   if (S == 0 || n_cap == 0) return FOREMOE_OK;
   REQUIRE(d_au && slot_widx && w_gate_up && dx_perm && W >= 1, "gate_up_dgrad: NULL buffer or W < 1");
@@ -1449,8 +1629,8 @@ int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, 
     a.n_cap = n_cap;
     a.C = (uint16_t*)dx_perm;
     a.ldc = d;
-    if (d % 256 == 0) launch_rows<256, false, kEpiStore>(a, st);
-    else launch_rows<128, false, kEpiStore>(a, st);
+    if (d % 256 == 0) launch_rows<256, false, kEpiStore>(a, workspace, st);
+    else launch_rows<128, false, kEpiStore>(a, workspace, st);
   } else {
     hipLaunchKernelGGL(f32_rows_kernel<kF32GateUpDgrad>, f32_grid(d, n_cap), dim3(256), 0, st, (const float*)d_au,
                        (const float*)w_gate_up, nullptr, d, F, W, slot_offset, slot_widx, S, n_cap, (float*)dx_perm,
@@ -1462,12 +1642,12 @@ int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, 
 int foremoe_grouped_ffn_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,
                               int32_t S, const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
                               const void* w_gate_up, const void* w_down, int64_t n_cap, void* d_au, void* dx_perm,
-                              void* stream) {
+                              void* workspace, size_t ws_bytes, void* stream) {
   int rc = foremoe_ffn_down_dgrad(dy_perm, save_au, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, d_au,
-                                  stream);
+                                  workspace, ws_bytes, stream);
   if (rc) return rc;
   return foremoe_ffn_gate_up_dgrad(d_au, dtype, d, F, S, slot_offset, slot_widx, W, w_gate_up, n_cap, dx_perm,
-                                   stream);
+                                   workspace, ws_bytes, stream);
 }
 
 static int wgrad_common(const char* who, const void* A, int lda, const void* B, int ldb, int M, int N,
@@ -1517,6 +1697,8 @@ static int wgrad_common(const char* who, const void* A, int lda, const void* B, 
   }
   return check_launch(who);
 }
+
+size_t foremoe_ffn_workspace_size(void) { return rows_workspace_bytes(); }
 
 size_t foremoe_wgrad_workspace_size(int32_t d, int32_t F) {
   if (d < 1 || F < 1) return 0;

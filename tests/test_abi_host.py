@@ -94,11 +94,11 @@ def test_permute_rejects_misaligned_rows(lib):
 
 
 def test_ffn_rejects_unsupported_bf16_shapes(lib):
-    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 96, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None)
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 96, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None, 0, None)
     assert rc == -2
-    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 128, 200, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None)
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 128, 200, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None, 0, None)
     assert rc == -2
-    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 7, 128, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None)
+    rc = lib.foremoe_grouped_ffn_fwd(FAKE, 7, 128, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None, None, 0, None)
     assert rc == -1
     rc = lib.foremoe_grouped_ffn_wgrad(FAKE, FAKE, FAKE, FAKE, 1, 128, 128, 4, FAKE, FAKE, 0, 64, FAKE, FAKE,
                                        None, 0, None)
@@ -108,9 +108,22 @@ def test_ffn_rejects_unsupported_bf16_shapes(lib):
     assert rc == -1  # ws NULL with ws_bytes > 0
     # (n_cap + 256) * row bytes must stay below 4 GiB for 32-bit buffer offsets
     rc = lib.foremoe_grouped_ffn_fwd(FAKE, 1, 8192, 1024, 4, FAKE, FAKE, 3, FAKE, FAKE, 1 << 18, FAKE, FAKE, None,
-                                     None)
+                                     None, 0, None)
     assert rc == -2
     assert lib.foremoe_wgrad_workspace_size(2048, 768) > 0
+
+
+def test_ffn_workspace_checks(lib):
+    # counters (4 KiB) + one 256 x 256 fp32 partial tile per workgroup of the
+    # persistent grid (one per CU; 256 when no device is visible)
+    n = lib.foremoe_ffn_workspace_size()
+    assert n >= 4096 + 256 * 256 * 4 and (n - 4096) % (256 * 256 * 4) == 0
+    args = (FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE, None)
+    # too small, then misaligned: rejected before any launch
+    assert lib.foremoe_grouped_ffn_fwd(FAKE, 1, 128, 256, 4, *args, 1 << 28, n - 1, None) == -1
+    assert lib.foremoe_grouped_ffn_fwd(FAKE, 1, 128, 256, 4, *args, (1 << 28) + 16, n, None) == -1
+    assert lib.foremoe_grouped_ffn_dgrad(FAKE, FAKE, 1, 128, 256, 4, FAKE, FAKE, 3, FAKE, FAKE, 64, FAKE, FAKE,
+                                         1 << 28, 1024, None) == -1
 
 
 def test_gathers_reject_bad_args(lib):
@@ -127,4 +140,4 @@ def test_empty_calls_launch_nothing(lib):
     assert lib.foremoe_permute_bwd(None, 1, None, 0, 2, 16, 0, None, 0, None) == 0
     # zero slots: the FFN returns before any launch
     assert lib.foremoe_grouped_ffn_fwd(None, 1, 128, 128, 0, FAKE, None, 1, None, None, 0, None, None, None,
-                                       None) == 0
+                                       None, 0, None) == 0

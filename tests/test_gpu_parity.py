@@ -155,8 +155,20 @@ def _ffn_inputs(w, m):
     return ref, N, gu, dn, x_perm
 
 
+def _ffn_ws(gpu, split):
+    """The row-GEMM workspace (a partial last round of tiles cut along K), or None."""
+    from paper_2606_11867_amd import api
+    return api.ffn_workspace(gpu) if split else None
+
+
+def _check_ws_reset(ws):
+    if ws is not None:
+        assert not ws[:4096].any().item(), "split arrival counters not reset"
+
+
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
-def test_ffn_forward(gpu, name):
+def test_ffn_forward(gpu, name, split):
     from paper_2606_11867_amd import api
     w = _wl(name)
     m = _ms(w)
@@ -166,12 +178,15 @@ def test_ffn_forward(gpu, name):
     dt = tdtype(w)
     so = torch.from_numpy(ref["slot_offset"]).to(gpu)
     widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
-    h, y, au = api.grouped_ffn_fwd(to_dev(x_perm, dt, gpu), so, widx, to_dev(gu, dt, gpu), to_dev(dn, dt, gpu))
+    ws = _ffn_ws(gpu, split)
+    h, y, au = api.grouped_ffn_fwd(to_dev(x_perm, dt, gpu), so, widx, to_dev(gu, dt, gpu), to_dev(dn, dt, gpu),
+                                   ws=ws)
     torch.cuda.synchronize()
     check_close("H", to_np(h), f["H"])
     check_close("Y", to_np(y), f["Y"])
     check_close("A", to_np(au[:, : w.spec.F]), f["A"])
     check_close("U", to_np(au[:, w.spec.F:]), f["U"])
+    _check_ws_reset(ws)
 
 
 def _sampled_rows(ref, m, rng, per_slot=6):
@@ -200,9 +215,11 @@ def test_ffn_forward_sampled_rows_full_size(gpu, name):
     gu, dn = w.weights(m.plan)
     dt = tdtype(w)
     widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+    ws = _ffn_ws(gpu, True)  # as the benchmark launches it
     h, y, au = api.grouped_ffn_fwd(got["x_perm"], got["slot_offset"], widx, to_dev(gu, dt, gpu),
-                                   to_dev(dn, dt, gpu))
+                                   to_dev(dn, dt, gpu), ws=ws)
     torch.cuda.synchronize()
+    _check_ws_reset(ws)
     ref = oracle_dispatch(w, m)
     rows, sub_off, sub_widx = _sampled_rows(ref, m, np.random.default_rng(0))
     f = O.ffn_forward(ref["x_perm"][rows], sub_off, sub_widx, gu, dn)
@@ -210,8 +227,9 @@ def test_ffn_forward_sampled_rows_full_size(gpu, name):
     check_close("Y", to_np(y[torch.from_numpy(rows).to(gpu)]), f["Y"])
 
 
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
-def test_ffn_backward(gpu, name):
+def test_ffn_backward(gpu, name, split):
     from paper_2606_11867_amd import api
     w = _wl(name)
     m = _ms(w)
@@ -228,12 +246,16 @@ def test_ffn_backward(gpu, name):
     so = torch.from_numpy(ref["slot_offset"]).to(gpu)
     widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
     gidx = torch.from_numpy(m.plan.slot_gidx).to(gpu)
+    ws = _ffn_ws(gpu, split)
     d_au, dx = api.grouped_ffn_dgrad(to_dev(dy_perm, dt, gpu), to_dev(au, dt, gpu), so, widx, to_dev(gu, dt, gpu),
-                                     to_dev(dn, dt, gpu))
+                                     to_dev(dn, dt, gpu), ws=ws)
     torch.cuda.synchronize()
     check_close("dA", to_np(d_au[:, :F]), g["dA"])
     check_close("dU", to_np(d_au[:, F:]), g["dU"])
     check_close("dX", to_np(dx), g["dX"])
+    _check_ws_reset(ws)
+    if split:
+        return  # the weight gradient does not use the row-GEMM workspace
     # weight gradient from the same (rounded) operands, accumulated onto a non-zero start
     dau_q = rnd(w, np.concatenate([g["dA"], g["dU"]], axis=1))
     G = m.plan.G
@@ -309,10 +331,11 @@ def run_gpu_layer(w, m, gpu, dy, dw_gate_up=None, dw_down=None):
     widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
     gidx = torch.from_numpy(m.plan.slot_gidx).to(gpu)
     gates = torch.from_numpy(m.gates).to(gpu)
-    h, y_perm, au = api.grouped_ffn_fwd(got["x_perm"], got["slot_offset"], widx, gud, dnd)
+    ws = api.ffn_workspace(gpu)  # as the benchmark launches the row GEMMs
+    h, y_perm, au = api.grouped_ffn_fwd(got["x_perm"], got["slot_offset"], widx, gud, dnd, ws=ws)
     y = api.combine(y_perm, got["pair_to_row"], gates, out_dtype=torch.float32)
     dyp, dg = api.combine_bwd(to_dev(dy, dt, gpu), y_perm, got["pair_to_row"], gates)
-    d_au, dxp = api.grouped_ffn_dgrad(dyp, au, got["slot_offset"], widx, gud, dnd)
+    d_au, dxp = api.grouped_ffn_dgrad(dyp, au, got["slot_offset"], widx, gud, dnd, ws=ws)
     if dw_gate_up is None:
         dw_gate_up = torch.zeros((m.plan.G, 2 * w.spec.F, d), dtype=torch.float32, device=gpu)
         dw_down = torch.zeros((m.plan.G, d, w.spec.F), dtype=torch.float32, device=gpu)
