@@ -398,3 +398,81 @@ def test_determinism(gpu):
     torch.cuda.synchronize()
     for k in a:
         assert torch.equal(a[k], b[k]), k
+
+
+def _backward_two_ways(w, gpu, n_micro):
+    """The benchmark's backward schedule (weight gradients on a second stream
+    beside the data gradients, sharing one workspace) against the same calls
+    on one stream, over consecutive micro-steps accumulating into dW."""
+    from paper_2606_11867_amd import _lib, api
+    lib = _lib.load()
+    d, F = w.spec.d, w.spec.F
+    dt = tdtype(w)
+    BF = _lib.BF16 if dt == torch.bfloat16 else _lib.F32
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    res = []
+    for overlap in (False, True):
+        G = w.micro[0].plan.G
+        dwgu = torch.zeros((G, 2 * F, d), dtype=torch.float32, device=gpu)
+        dwdn = torch.zeros((G, d, F), dtype=torch.float32, device=gpu)
+        wws, rws = api.wgrad_workspace(d, F, gpu), api.ffn_workspace(gpu)
+        outs = []
+        for m in w.micro[:n_micro]:
+            got = gpu_dispatch(w, m, gpu)
+            gu, dn = w.weights(m.plan)
+            gud, dnd = to_dev(gu, dt, gpu), to_dev(dn, dt, gpu)
+            widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+            gidx = torch.from_numpy(m.plan.slot_gidx).to(gpu)
+            gates = torch.from_numpy(m.gates).to(gpu)
+            h, y_perm, au = api.grouped_ffn_fwd(got["x_perm"], got["slot_offset"], widx, gud, dnd, ws=rws)
+            dyp, dg = api.combine_bwd(to_dev(w.dy(m.index), dt, gpu), y_perm, got["pair_to_row"], gates)
+            n_cap, S = got["x_perm"].shape[0], m.plan.S
+            so = got["slot_offset"].data_ptr()
+            d_au = torch.empty((n_cap, 2 * F), dtype=dt, device=gpu)
+            dxp = torch.empty((n_cap, d), dtype=dt, device=gpu)
+
+            def down_wgrad(st):
+                assert lib.foremoe_ffn_down_wgrad(dyp.data_ptr(), h.data_ptr(), BF, d, F, S, so, gidx.data_ptr(), G,
+                                                  n_cap, dwdn.data_ptr(), wws.data_ptr(), wws.numel(),
+                                                  st.cuda_stream) == 0
+
+            def gate_up_wgrad(st):
+                assert lib.foremoe_ffn_gate_up_wgrad(d_au.data_ptr(), got["x_perm"].data_ptr(), BF, d, F, S, so,
+                                                     gidx.data_ptr(), G, n_cap, dwgu.data_ptr(), wws.data_ptr(),
+                                                     wws.numel(), st.cuda_stream) == 0
+
+            if overlap:
+                side.wait_stream(main)
+                down_wgrad(side)
+            assert lib.foremoe_ffn_down_dgrad(dyp.data_ptr(), au.data_ptr(), BF, d, F, S, so, widx.data_ptr(), G,
+                                              dnd.data_ptr(), n_cap, d_au.data_ptr(), rws.data_ptr(), rws.numel(),
+                                              main.cuda_stream) == 0
+            if overlap:
+                side.wait_stream(main)
+                gate_up_wgrad(side)
+            assert lib.foremoe_ffn_gate_up_dgrad(d_au.data_ptr(), BF, d, F, S, so, widx.data_ptr(), G,
+                                                 gud.data_ptr(), n_cap, dxp.data_ptr(), rws.data_ptr(), rws.numel(),
+                                                 main.cuda_stream) == 0
+            if not overlap:
+                gate_up_wgrad(main)
+                down_wgrad(main)
+            dx = api.permute_bwd(dxp, got["pair_to_row"], m.ids.shape[0], m.ids.shape[1], out_dtype=torch.float32)
+            if overlap:
+                main.wait_stream(side)
+            N = int(got["slot_offset"][-1].item())  # rows past N are not written
+            outs.append(dict(dx=dx, d_au=d_au[:N], dgates=dg))
+        torch.cuda.synchronize()
+        assert not wws[:256].any().item() and not rws[:4096].any().item(), "workspace counters not reset"
+        res.append(dict(outs=outs, dwgu=dwgu, dwdn=dwdn))
+    return res
+
+
+@pytest.mark.parametrize("name,n_micro", [("share", 3), ("cfg3", 2)])
+def test_backward_overlap_matches_one_stream(gpu, name, n_micro):
+    w = _wl(name)
+    _print_case(name, w, w.micro[0])
+    seq, ovl = _backward_two_ways(w, gpu, n_micro)
+    for i, (a, b) in enumerate(zip(seq["outs"], ovl["outs"])):
+        for k in a:
+            assert torch.equal(a[k], b[k]), f"micro-step {i}: {k} differs with the overlapped schedule"
+    assert torch.equal(seq["dwgu"], ovl["dwgu"]) and torch.equal(seq["dwdn"], ovl["dwdn"])
