@@ -6,7 +6,7 @@ stage (T=16384 tokens, d=2048, F=768, E=128, top-8, 16 hosted experts + 4
 replica slots, 16 micro-steps with independently jittered routing). One
 step = one micro-step through every step of the path:
 
-  histogram -> assign_replicas -> permute -> gate/up (+SwiGLU) -> down
+  histogram + assign_replicas (one call) -> permute -> gate/up (+SwiGLU) -> down
   -> combine -> combine_bwd -> down dgrad (+SwiGLU') -> gate/up dgrad
   -> gate/up wgrad -> down wgrad -> permute_bwd
 
@@ -40,10 +40,10 @@ if ROOT not in sys.path:
 
 METRIC = "grouped-FFN TFLOP/s & % bf16 MFMA peak; permute+combine GB/s; tokens/s per micro-step"
 
-PHASES = ["histogram", "assign_replicas", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
+PHASES = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
           "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
 # phases that are exactly one kernel launch (candidates for the roofline line)
-SINGLE_LAUNCH = {"assign_replicas", "gate_up_fwd", "down_fwd", "combine", "combine_bwd", "down_dgrad",
+SINGLE_LAUNCH = {"gate_up_fwd", "down_fwd", "combine", "combine_bwd", "down_dgrad",
                  "gate_up_dgrad", "permute_bwd"}
 
 
@@ -189,10 +189,8 @@ def main() -> int:
             call("down_wgrad", st, lambda q: lib.foremoe_ffn_down_wgrad(
                 P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"], P["wws"], wwsz, q))
 
-        call("histogram", main, lambda q: lib.foremoe_histogram(ms["ids"].data_ptr(), T, K, E, P["counts"],
-                                                                  P["ws"], wsz, q))
-        call("assign_replicas", main, lambda q: lib.foremoe_assign_replicas(
-            P["counts"], cp, P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
+        call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
+            ms["ids"].data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
         call("permute", main, lambda q: lib.foremoe_permute(
             ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
             P["r2p"], P["p2r"], P["ws"], wsz, q))
@@ -293,7 +291,7 @@ def main() -> int:
     work = {p: {"flop": 0.0, "bytes": 0.0} for p in PHASES}
     for s in range(args.steps):
         N, g = Ns[s % n_micro], Gs[s % n_micro]
-        work["histogram"]["bytes"] += 4.0 * T * K
+        work["histogram_assign"]["bytes"] += 4.0 * T * K
         work["permute"]["bytes"] += acc.permute_bytes(N, T, K, d, 2)
         work["gate_up_fwd"]["flop"] += acc.gate_up_flops(N, d, F)
         work["gate_up_fwd"]["bytes"] += 2.0 * (N * d + g * 2 * F * d + N * F + N * 2 * F)
@@ -339,7 +337,7 @@ def main() -> int:
     ffn = ["gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad"]
     ffn_flop = sum(work[p]["flop"] for p in ffn)
     ffn_s = sum(phase_ms[p] for p in ffn) / 1e3
-    fwd_ph = ["histogram", "assign_replicas", "permute", "gate_up_fwd", "down_fwd", "combine"]
+    fwd_ph = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine"]
     fwd_s = sum(phase_ms[p] for p in fwd_ph) / 1e3
     ffn_fwd_s = (phase_ms["gate_up_fwd"] + phase_ms["down_fwd"]) / 1e3
     ffn_fwd_flop = work["gate_up_fwd"]["flop"] + work["down_fwd"]["flop"]

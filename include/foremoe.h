@@ -123,6 +123,9 @@ typedef struct foremoe_plan {
 #define FOREMOE_WS_INVALID_IDS 0  /* ids outside [-1, E): skipped, written by histogram */
 #define FOREMOE_WS_DROPPED 1      /* local pairs beyond n_cap, written by permute       */
 #define FOREMOE_WS_PLAN_ERRORS 2  /* device-side plan errors, written by assign         */
+/* Word 63 is the arrival ticket of foremoe_histogram_assign: it must be zero
+ * before that call is first made on a workspace (zero-fill the workspace once)
+ * and every such call leaves it zero. */
 size_t foremoe_workspace_size(int64_t T, int32_t K, int32_t E);
 
 /*
@@ -167,6 +170,22 @@ int foremoe_histogram_src(const int32_t* ids, int64_t T, int32_t K, int32_t E, i
 int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan,
                             int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset,
                             void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Steps 1 and 2 in one call (Sec. 5 Routing Collector counts; Sec. 7.2
+ * replica split): the same outputs as foremoe_histogram (plan->n_src < 2)
+ * or foremoe_histogram_src (plan->n_src >= 2, sources from
+ * plan->src_token_begin) into counts [n_src * E], followed by
+ * foremoe_assign_replicas with the same plan, workspace and stream. With up
+ * to 256 keys this is two launches instead of three: the per-key column
+ * scan and the replica split share one, where the last workgroup to finish
+ * the scan does the split (a ticket in workspace status word 63, see
+ * above). Larger key sets run the three launches. Same argument rules and
+ * errors as the two calls it replaces.
+ */
+int foremoe_histogram_assign(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan,
+                             int32_t* counts, int32_t* rep_begin, int32_t* slot_count,
+                             int32_t* slot_offset, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Step 3 (Sec. 9, replica-aware token dispatch; one GPU's half of it).

@@ -48,6 +48,7 @@ SIGNATURES = {
     "foremoe_histogram": (ctypes.c_int, [c_p, c_i64, c_i32, c_i32, c_p, c_p, c_sz, c_p]),
     "foremoe_histogram_src": (ctypes.c_int, [c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_assign_replicas": (ctypes.c_int, [c_p, PPlan, c_p, c_p, c_p, c_p, c_sz, c_p]),
+    "foremoe_histogram_assign": (ctypes.c_int, [c_p, c_i64, c_i32, PPlan, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_permute": (ctypes.c_int, [c_p, c_i32, c_i64, c_i32, c_p, c_i32, PPlan, c_p, c_p, c_i64,
                                        c_p, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_workspace_size": (c_sz, []),

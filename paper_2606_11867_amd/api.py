@@ -95,7 +95,9 @@ def workspace(T: int, K: int, E: int, device) -> torch.Tensor:
     n = _lib.load().foremoe_workspace_size(T, K, E)
     if n == 0:
         raise ValueError("invalid workspace sizes")
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    # zero-filled: foremoe_histogram_assign's arrival ticket (a header word)
+    # must start at zero; every call leaves it zero again
+    return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def ws_status(ws: torch.Tensor) -> np.ndarray:
@@ -135,6 +137,25 @@ def assign_replicas(counts: torch.Tensor, plan: DevicePlan, ws: torch.Tensor):
                                               slot_count.data_ptr(), _ptr(slot_offset), _ptr(ws), ws.numel(),
                                               _stream(dev)), "foremoe_assign_replicas")
     return rep_begin, slot_count, slot_offset
+
+
+def histogram_assign(ids: torch.Tensor, plan: DevicePlan, ws: torch.Tensor):
+    """Steps 1 and 2 in one call (two launches for up to 256 keys): the
+    per-key counts (n_src * E keys for a per-source plan) and the replica
+    split, as histogram(_src) followed by assign_replicas."""
+    T, K = ids.shape
+    dev = ids.device
+    nkeys = plan.E * max(plan.n_src, 1)
+    counts = torch.empty(nkeys, dtype=torch.int32, device=dev)
+    shape = (plan.E, plan.R_max + 1) if plan.n_src <= 1 else (plan.n_src, plan.E, plan.R_max + 1)
+    rep_begin = torch.empty(shape, dtype=torch.int32, device=dev)
+    slot_count = torch.empty(max(plan.S, 1), dtype=torch.int32, device=dev)[: plan.S]
+    slot_offset = torch.empty(plan.S + 1, dtype=torch.int32, device=dev)
+    cp = plan.c_struct()
+    check(_lib.load().foremoe_histogram_assign(_ptr(ids), T, K, ctypes.byref(cp), _ptr(counts), _ptr(rep_begin),
+                                               slot_count.data_ptr(), _ptr(slot_offset), _ptr(ws), ws.numel(),
+                                               _stream(dev)), "foremoe_histogram_assign")
+    return counts, rep_begin, slot_count, slot_offset
 
 
 def permute(x: torch.Tensor, ids: torch.Tensor, plan: DevicePlan, rep_begin: torch.Tensor,

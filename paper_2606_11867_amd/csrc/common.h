@@ -14,6 +14,8 @@ namespace foremoe {
 constexpr int kHistChunk = 512;
 constexpr int kHistThreads = 256;
 constexpr int kWsHeaderBytes = 256;
+// status word used internally as the arrival ticket of foremoe_histogram_assign
+constexpr int kWsTicketWord = 63;
 
 constexpr size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

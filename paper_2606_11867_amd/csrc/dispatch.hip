@@ -171,11 +171,12 @@ __device__ __forceinline__ int clamp_nrep(const PlanDev& P, int e, int& err) {
 // the kernel costs a few memory round trips.
 // Two sizes: up to 256 keys with 256 threads (small LDS, quick to launch)
 // and up to FOREMOE_MAX_EXPERTS keys with 1024 threads.
+// `counts` may point to global memory or to LDS.
 template <int kAssignThreads, int MAXK>
-__global__ __launch_bounds__(kAssignThreads) void assign_kernel(const int32_t* __restrict__ counts, PlanDev P,
-                                                                int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count,
-                                                                int32_t* __restrict__ slot_offset, int32_t* __restrict__ vslot_offset,
-                                                                int32_t* __restrict__ rep_slot, int32_t* __restrict__ status) {
+__device__ __forceinline__ void assign_block(const int32_t* counts, const PlanDev& P, int32_t* __restrict__ rep_begin,
+                                             int32_t* __restrict__ slot_count, int32_t* __restrict__ slot_offset,
+                                             int32_t* __restrict__ vslot_offset, int32_t* __restrict__ rep_slot,
+                                             int32_t* __restrict__ status) {
   constexpr int NW = kAssignThreads / 64;
   __shared__ int s_err;
   __shared__ int s_nrep[FOREMOE_MAX_EXPERTS];
@@ -278,6 +279,57 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(const int32_t* _
     slot_offset[P.S] = carry;
     status[FOREMOE_WS_PLAN_ERRORS] = s_err;
   }
+}
+
+template <int kAssignThreads, int MAXK>
+__global__ __launch_bounds__(kAssignThreads) void assign_kernel(const int32_t* __restrict__ counts, PlanDev P,
+                                                                int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count,
+                                                                int32_t* __restrict__ slot_offset, int32_t* __restrict__ vslot_offset,
+                                                                int32_t* __restrict__ rep_slot, int32_t* __restrict__ status) {
+  assign_block<kAssignThreads, MAXK>(counts, P, rep_begin, slot_count, slot_offset, vslot_offset, rep_slot, status);
+}
+
+// ---------------------------------------------------------------------------
+// Step 1b and step 2 in one launch (up to 256 keys): one workgroup per key
+// column turns the per-block counts into block bases and the key's total,
+// as hist_scan_kernel does; the last workgroup to finish (a ticket in the
+// workspace header) then splits the keys over the replicas, as
+// assign_kernel does. Workgroups may run on different XCDs, whose L2
+// caches are not coherent with each other: the totals are stored and loaded
+// with device scope (SC1 cache policy: written through, never read from a
+// stale line), and each workgroup drains its stores before it takes its
+// ticket. No workgroup waits for another.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kHistThreads) void hist_scan_assign_kernel(
+    int32_t* __restrict__ partial, int64_t nblocks, int nkeys, int32_t* __restrict__ counts, uint32_t* ticket,
+    PlanDev P, int32_t* __restrict__ rep_begin, int32_t* __restrict__ slot_count, int32_t* __restrict__ slot_offset,
+    int32_t* __restrict__ vslot_offset, int32_t* __restrict__ rep_slot, int32_t* __restrict__ status) {
+  __shared__ int s_tmp[kWaves];
+  __shared__ int s_cnt[257];
+  __shared__ int s_last;
+  const int e = blockIdx.x;
+  int carry = 0;
+  for (int64_t b0 = 0; b0 < nblocks; b0 += kHistThreads) {
+    const int64_t b = b0 + threadIdx.x;
+    const int v = b < nblocks ? partial[b * (nkeys + 1) + e] : 0;
+    int total;
+    const int incl = block_inclusive_scan(v, s_tmp, total);
+    if (b < nblocks) partial[b * (nkeys + 1) + e] = carry + incl - v;
+    carry += total;
+  }
+  if (threadIdx.x == 0) {
+    if (e < nkeys) __hip_atomic_store(counts + e, carry, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else status[FOREMOE_WS_INVALID_IDS] = carry;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the total has reached memory
+    s_last = atomicAdd(ticket, 1u) == gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  for (int k = threadIdx.x; k < nkeys; k += kHistThreads)
+    s_cnt[k] = __hip_atomic_load(counts + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  assign_block<kHistThreads, 256>(s_cnt, P, rep_begin, slot_count, slot_offset, vslot_offset, rep_slot, status);
+  if (threadIdx.x == 0) atomicExch(ticket, 0u);  // ready for the next call
 }
 
 // ---------------------------------------------------------------------------
@@ -673,8 +725,8 @@ using namespace foremoe;
 
 extern "C" {
 
-static int histogram_common(const char* who, const int32_t* ids, int64_t T, int32_t K, int32_t E, KeyMap km,
-                            int32_t* counts, void* ws, size_t ws_bytes, void* stream) {
+static int check_hist(const char* who, const int32_t* ids, int64_t T, int32_t K, int32_t E, const int32_t* counts,
+                      const void* ws, size_t ws_bytes) {
   REQUIRE(T >= 0, "%s: T < 0", who);
   REQUIRE(K >= 1 && K <= FOREMOE_MAX_TOPK, "%s: K=%d outside [1, %d]", who, K, FOREMOE_MAX_TOPK);
   REQUIRE(E >= 1 && E <= FOREMOE_MAX_EXPERTS, "%s: %d keys outside [1, %d]", who, E, FOREMOE_MAX_EXPERTS);
@@ -683,6 +735,13 @@ static int histogram_common(const char* who, const int32_t* ids, int64_t T, int3
   REQUIRE(counts && ws, "%s: counts or ws is NULL", who);
   REQUIRE(ws_bytes >= ws_bytes_needed(T, K, E), "%s: workspace too small (%zu < %zu)", who, ws_bytes,
           ws_bytes_needed(T, K, E));
+  return FOREMOE_OK;
+}
+
+static int histogram_common(const char* who, const int32_t* ids, int64_t T, int32_t K, int32_t E, KeyMap km,
+                            int32_t* counts, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_hist(who, ids, T, K, E, counts, ws, ws_bytes);
+  if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
@@ -710,8 +769,8 @@ int foremoe_histogram_src(const int32_t* ids, int64_t T, int32_t K, int32_t E, i
                           counts, ws, ws_bytes, stream);
 }
 
-int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
-                            int32_t* slot_offset, void* ws, size_t ws_bytes, void* stream) {
+static int check_plan(const foremoe_plan* plan, const int32_t* counts, const int32_t* rep_begin,
+                      const int32_t* slot_count, const int32_t* slot_offset, const void* ws, size_t ws_bytes) {
   REQUIRE(plan, "assign_replicas: plan is NULL");
   REQUIRE(plan->E >= 1 && plan->E <= FOREMOE_MAX_EXPERTS, "assign_replicas: E=%d out of range", plan->E);
   REQUIRE(plan->S >= 0 && plan->S <= FOREMOE_MAX_SLOTS, "assign_replicas: S=%d out of range", plan->S);
@@ -729,8 +788,21 @@ int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int
             "assign_replicas: n_src * E or n_src * S above the limits");
     REQUIRE(plan->src_token_begin, "assign_replicas: plan->src_token_begin is NULL");
   }
-  PlanDev P{plan->E, plan->S, plan->R_max, n_src, plan->slot_expert, plan->slot_replica, plan->expert_nrep,
-            plan->expert_rep_weight, n_src >= 2 ? plan->src_rep_weight : nullptr};
+  return FOREMOE_OK;
+}
+
+static PlanDev plan_dev(const foremoe_plan* plan) {
+  const int n_src = plan->n_src < 1 ? 1 : plan->n_src;
+  return PlanDev{plan->E, plan->S, plan->R_max, n_src, plan->slot_expert, plan->slot_replica, plan->expert_nrep,
+                 plan->expert_rep_weight, n_src >= 2 ? plan->src_rep_weight : nullptr};
+}
+
+int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
+                            int32_t* slot_offset, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_plan(plan, counts, rep_begin, slot_count, slot_offset, ws, ws_bytes);
+  if (rc) return rc;
+  const PlanDev P = plan_dev(plan);
+  const int n_src = P.n_src;
   int32_t* status = (int32_t*)ws;
   int32_t* rep_slot = (int32_t*)((char*)ws + kWsRepSlotOff);
   int32_t* vslot = (int32_t*)((char*)ws + kWsVSlotOff);
@@ -741,6 +813,34 @@ int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int
     hipLaunchKernelGGL((assign_kernel<1024, FOREMOE_MAX_EXPERTS>), dim3(1), dim3(1024), 0, (hipStream_t)stream, counts,
                        P, rep_begin, slot_count, slot_offset, vslot, rep_slot, status);
   return check_launch("foremoe_assign_replicas");
+}
+
+int foremoe_histogram_assign(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan, int32_t* counts,
+                             int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset, void* ws, size_t ws_bytes,
+                             void* stream) {
+  int rc = check_plan(plan, counts, rep_begin, slot_count, slot_offset, ws, ws_bytes);
+  if (rc) return rc;
+  const PlanDev P = plan_dev(plan);
+  const int nkeys = P.n_src * P.E;
+  const KeyMap km{P.E, P.n_src, K, P.n_src >= 2 ? plan->src_token_begin : nullptr};
+  if (nkeys > 256) {  // large key sets: the three separate launches
+    rc = histogram_common("foremoe_histogram_assign", ids, T, K, nkeys, km, counts, ws, ws_bytes, stream);
+    if (rc) return rc;
+    return foremoe_assign_replicas(counts, plan, rep_begin, slot_count, slot_offset, ws, ws_bytes, stream);
+  }
+  rc = check_hist("foremoe_histogram_assign", ids, T, K, nkeys, counts, ws, ws_bytes);
+  if (rc) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t npairs = T * (int64_t)K;
+  const int64_t nb = hist_blocks(npairs);
+  int32_t* status = (int32_t*)ws;
+  int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
+  hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, nkeys,
+                     key_bits(nkeys), partial);
+  hipLaunchKernelGGL(hist_scan_assign_kernel, dim3(nkeys + 1), dim3(kHistThreads), 0, st, partial, nb, nkeys, counts,
+                     (uint32_t*)(status + kWsTicketWord), P, rep_begin, slot_count, slot_offset,
+                     (int32_t*)((char*)ws + kWsVSlotOff), (int32_t*)((char*)ws + kWsRepSlotOff), status);
+  return check_launch("foremoe_histogram_assign");
 }
 
 int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, const int32_t* ids, int32_t K,

@@ -61,8 +61,10 @@ def custom_workload(name: str):
     return make_custom(**shapes[name])
 
 
-def gpu_dispatch(w, m, dev, n_cap=None, x=None):
-    """Steps 1-3 on the GPU; returns device tensors and the workspace."""
+def gpu_dispatch(w, m, dev, n_cap=None, x=None, fused=True):
+    """Steps 1-3 on the GPU; returns device tensors and the workspace.
+    fused: steps 1-2 through foremoe_histogram_assign (as the benchmark runs
+    them), else through foremoe_histogram and foremoe_assign_replicas."""
     from paper_2606_11867_amd import api
     T, K = m.ids.shape
     if n_cap is None:
@@ -72,8 +74,11 @@ def gpu_dispatch(w, m, dev, n_cap=None, x=None):
     ids = torch.from_numpy(m.ids).to(dev)
     plan = api.DevicePlan.from_host(m.plan, dev)
     ws = api.workspace(T, K, m.plan.E, dev)
-    counts = api.histogram(ids, m.plan.E, ws)
-    rep_begin, slot_count, slot_offset = api.assign_replicas(counts, plan, ws)
+    if fused:
+        counts, rep_begin, slot_count, slot_offset = api.histogram_assign(ids, plan, ws)
+    else:
+        counts = api.histogram(ids, m.plan.E, ws)
+        rep_begin, slot_count, slot_offset = api.assign_replicas(counts, plan, ws)
     xd = to_dev(x, tdtype(w), dev)
     x_perm, r2p, p2r = api.permute(xd, ids, plan, rep_begin, slot_offset, n_cap, ws)
     return dict(ids=ids, plan=plan, ws=ws, counts=counts, rep_begin=rep_begin, slot_count=slot_count,

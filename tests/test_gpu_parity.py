@@ -36,8 +36,9 @@ def _print_case(name, w, m):
 # ---------------------------------------------------------------------------
 # Steps 1-3: bit-exact dispatch
 # ---------------------------------------------------------------------------
+@pytest.mark.parametrize("fused", [True, False], ids=["histogram_assign", "separate"])
 @pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg2", "cfg3", "cfg4"])
-def test_dispatch_bit_exact(gpu, name):
+def test_dispatch_bit_exact(gpu, name, fused):
     w = _wl(name)
     m = _ms(w)
     _print_case(name, w, m)
@@ -45,7 +46,7 @@ def test_dispatch_bit_exact(gpu, name):
     N = int(ref["slot_offset"][-1])
     n_cap = N + 37
     ref = oracle_dispatch(w, m, n_cap=n_cap)
-    got = gpu_dispatch(w, m, gpu, n_cap=n_cap)
+    got = gpu_dispatch(w, m, gpu, n_cap=n_cap, fused=fused)
     torch.cuda.synchronize()
     assert np.array_equal(got["counts"].cpu().numpy(), ref["counts"])
     assert np.array_equal(got["rep_begin"].cpu().numpy(), ref["rep_begin"])
@@ -56,6 +57,26 @@ def test_dispatch_bit_exact(gpu, name):
     assert np.array_equal(to_np(got["x_perm"][:N]), ref["x_perm"][:N])  # bitwise: bf16/f32 -> f64 is exact
     status = got["ws"][:256].view(torch.int32).cpu().numpy()
     assert status[0] == ref["invalid"] and status[1] == 0 and status[2] == 0
+    assert status[63] == 0, "histogram_assign ticket not reset"
+
+
+def test_histogram_assign_repeated_calls(gpu):
+    """One workspace, consecutive micro-steps through the fused steps 1-2:
+    every call matches the oracle (the arrival ticket is reset each time)."""
+    from paper_2606_11867_amd import api
+    w = _wl("share")
+    m0 = w.micro[0]
+    T, K = m0.ids.shape
+    ws = api.workspace(T, K, m0.plan.E, gpu)
+    for m in w.micro:
+        ids = torch.from_numpy(m.ids).to(gpu)
+        plan = api.DevicePlan.from_host(m.plan, gpu)
+        counts, rb, sc, so = api.histogram_assign(ids, plan, ws)
+        rc, _ = O.histogram(m.ids, m.plan.E)
+        rrb, rsc, rso = O.assign_replicas(rc, m.plan)
+        assert np.array_equal(counts.cpu().numpy(), rc) and np.array_equal(rb.cpu().numpy(), rrb)
+        assert np.array_equal(sc.cpu().numpy(), rsc) and np.array_equal(so.cpu().numpy(), rso)
+    assert ws[:256].view(torch.int32)[63].item() == 0
 
 
 def test_dispatch_edge_cases(gpu):

@@ -46,7 +46,7 @@ def planned_share(w, m, rank, N_r=4, C_max=8):
     return plan, mp
 
 
-def run_both(ids, plan, x, n_cap, dtype, gpu):
+def run_both(ids, plan, x, n_cap, dtype, gpu, fused=False):
     from paper_2606_11867_amd import api
     T, K = ids.shape
     tb = plan.src_token_begin
@@ -58,8 +58,12 @@ def run_both(ids, plan, x, n_cap, dtype, gpu):
     idd = torch.from_numpy(ids).to(gpu)
     dp = api.DevicePlan.from_host(plan, gpu)
     ws = api.workspace(T, K, plan.E * plan.n_src, gpu)
-    counts = api.histogram_src(idd, plan.E, dp.src_token_begin, ws)
-    rep_begin, slot_count, slot_offset = api.assign_replicas(counts.reshape(-1), dp, ws)
+    if fused:  # foremoe_histogram_assign: two launches up to 256 keys, else three
+        counts, rep_begin, slot_count, slot_offset = api.histogram_assign(idd, dp, ws)
+        counts = counts.reshape(plan.n_src, plan.E)
+    else:
+        counts = api.histogram_src(idd, plan.E, dp.src_token_begin, ws)
+        rep_begin, slot_count, slot_offset = api.assign_replicas(counts.reshape(-1), dp, ws)
     xd = to_dev(x, dtype, gpu)
     x_perm, g_r2p, g_p2r = api.permute(xd, idd, dp, rep_begin, slot_offset, n_cap, ws)
     torch.cuda.synchronize()
@@ -87,7 +91,7 @@ def test_planned_share_bit_exact_and_ffn(gpu):
     print(f"planned share: rank {w.rank}, S={plan.S}, copies {[len(c) for c in mp.copies if len(c) > 1]}",
           flush=True)
     x = w.x(m.index)
-    got = run_both(m.ids, plan, x, T * K, tdtype(w), gpu)
+    got = run_both(m.ids, plan, x, T * K, tdtype(w), gpu, fused=True)  # 1024 keys: three launches
     # the grouped FFN consumes the planned slot table as any other
     N = int(got["ref"]["so"][-1])
     gu, dn = w.weights(plan)
@@ -130,4 +134,5 @@ def test_random_sources_bit_exact(gpu, seed):
     x = rng.standard_normal((T, d)).astype(np.float32)
     N = int(O.assign_replicas_src(cs, plan)[2][-1])
     for n_cap in (N + 3, max(N - 50, 1)):
-        run_both(ids, plan, x, n_cap, torch.float32, gpu)
+        for fused in (False, True):
+            run_both(ids, plan, x, n_cap, torch.float32, gpu, fused=fused)
