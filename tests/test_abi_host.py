@@ -85,6 +85,21 @@ def test_assign_rejects_bad_plan(lib):
     assert lib.foremoe_assign_replicas(FAKE, None, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
 
 
+def test_histogram_assign_rejects_bad_args(lib):
+    from paper_2606_11867_amd._lib import Plan
+    p = Plan(8, 4, 2, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE)
+    f = lib.foremoe_histogram_assign
+    assert f(FAKE, 10, 2, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1   # no plan
+    assert f(None, 10, 2, ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1  # no ids
+    assert f(FAKE, 10, 0, ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1  # K = 0
+    assert f(FAKE, 10, 2, ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == -1       # small ws
+    bad = Plan(8, 4, 0, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE)                                # R_max = 0
+    assert f(FAKE, 10, 2, ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    # per-source plan without its source boundaries
+    src = Plan(8, 4, 2, 4, FAKE, FAKE, FAKE, None, FAKE, FAKE)
+    assert f(FAKE, 10, 2, ctypes.byref(src), FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+
+
 def test_permute_rejects_misaligned_rows(lib):
     from paper_2606_11867_amd._lib import Plan
     p = Plan(8, 4, 2, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE)
