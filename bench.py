@@ -12,8 +12,11 @@ step = one micro-step through every step of the path:
 
 The two weight-gradient GEMMs run on a second stream, each beside the
 data-gradient GEMM that does not feed it (down wgrad beside down dgrad,
-gate/up wgrad beside gate/up dgrad); --no-overlap runs all twelve phases on
-one stream.
+gate/up wgrad beside gate/up dgrad), and the streams are not joined at the
+end of a micro-step: the next micro-step's dispatch and forward (which do
+not depend on this one's weight gradients) start while they run, on a
+second set of activation buffers. --no-pipeline joins the streams after
+every micro-step; --no-overlap runs all phases on one stream.
 
 All inputs are resident in HBM before timing. A first pass brackets every
 ABI call with HIP events on the stream it runs on, one kernel after
@@ -23,7 +26,7 @@ events (events around every call would add about 80 us per step); their
 average duration gives the roofline line. The fp64 CPU oracle is timed on
 one micro-step as the CPU baseline.
 
-    python bench.py [--gpus 1] [--steps 32] [--warmup 16] [--no-cpu-baseline] [--no-overlap] [--no-split]
+    python bench.py [--gpus 1] [--steps 32] [--warmup 16] [--no-cpu-baseline] [--no-overlap] [--no-pipeline] [--no-split]
 """
 from __future__ import annotations
 
@@ -57,6 +60,9 @@ def parse():
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
     ap.add_argument("--no-split", action="store_true",
                     help="run the row GEMMs without the workspace (no K split of a partial last round of tiles)")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="join the two streams at the end of every micro-step instead of letting the next "
+                         "micro-step's forward start while this one's weight gradients run")
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the weight-gradient GEMMs on the main stream instead of beside the data gradients")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -125,15 +131,21 @@ def main() -> int:
     S_max = max(ms["S"] for ms in mss)
     n_cap = T * K
     z = lambda *s, dt=bf: torch.zeros(s, dtype=dt, device=dev)  # noqa: E731
-    buf = dict(
-        counts=z(E, dt=torch.int32), rep_begin=z(E, 3, dt=torch.int32), slot_count=z(S_max, dt=torch.int32),
-        slot_offset=z(S_max + 1, dt=torch.int32), ws=api.workspace(T, K, E, dev),
-        x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
-        y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d), dy_perm=z(n_cap, d), dgates=z(T, K, dt=torch.float32),
-        d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d), dx=z(T, d),
-        dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32),
-        wws=api.wgrad_workspace(d, F, dev), rws=api.ffn_workspace(dev))
+    def step_buffers():
+        return dict(
+            counts=z(E, dt=torch.int32), rep_begin=z(E, 3, dt=torch.int32), slot_count=z(S_max, dt=torch.int32),
+            slot_offset=z(S_max + 1, dt=torch.int32), ws=api.workspace(T, K, E, dev),
+            x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
+            y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d), dy_perm=z(n_cap, d),
+            dgates=z(T, K, dt=torch.float32), d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d), dx=z(T, d))
+
+    # activations of one micro-step; a second set lets the next micro-step's
+    # forward start while this one's weight gradients still read its set
+    sets = [step_buffers(), step_buffers()]
+    buf = dict(sets[0], dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32),
+               wws=api.wgrad_workspace(d, F, dev), rws=api.ffn_workspace(dev))
     P = {k: v.data_ptr() for k, v in buf.items()}
+    PS = [dict(P, **{k: v.data_ptr() for k, v in st.items()}) for st in sets]
     wsz = buf["ws"].numel()
     wwsz = buf["wws"].numel()
     # row-GEMM workspace (tail split of a partial last round of tiles)
@@ -150,7 +162,9 @@ def main() -> int:
     side = torch.cuda.Stream(dev)  # default priority, like every stream here
     ssp = side.cuda_stream
 
-    def step_ops(i, ev=None, overlap=False):
+    done = [torch.cuda.Event(), torch.cuda.Event()]  # side-stream work of the micro-step using set b
+
+    def step_ops(i, ev=None, overlap=False, pipelined=False):
         """The operations of one micro-step, in order, as (phase, thunk)
         pairs (phase None: a stream dependency). With overlap the two
         weight-gradient GEMMs run on the side stream, each beside the
@@ -158,9 +172,14 @@ def main() -> int:
         beside down dgrad, gate/up wgrad (needs d_au) beside gate/up dgrad.
         Both share one workspace, so they stay ordered on that one stream;
         the main stream waits for the side stream before the step ends, so
-        the next step's buffers are free. ev maps phases to (begin, end)
-        event pairs recorded on the stream the phase runs on."""
+        the next step's buffers are free. Pipelined, the streams are not
+        joined: micro-step i uses buffer set i % 2, and before reusing it
+        the main stream waits for the side-stream work of micro-step i - 2.
+        ev maps phases to (begin, end) event pairs recorded on the stream
+        the phase runs on."""
         main = stream
+        bset = i % 2 if pipelined else 0
+        P = PS[bset]
         ms = mss[i % n_micro]
         S = ms["S"]
         so = P["slot_offset"]
@@ -189,6 +208,8 @@ def main() -> int:
             call("down_wgrad", st, lambda q: lib.foremoe_ffn_down_wgrad(
                 P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"], P["wws"], wwsz, q))
 
+        if pipelined:  # set bset was last used two micro-steps ago: its weight gradients must be done
+            ops.append((None, lambda: main.wait_event(done[bset])))
         call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
             ms["ids"].data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
         call("permute", main, lambda q: lib.foremoe_permute(
@@ -218,12 +239,14 @@ def main() -> int:
             down_wgrad(main)
         call("permute_bwd", main, lambda q: lib.foremoe_permute_bwd(
             P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], BF16, q))
-        if overlap:
+        if pipelined:
+            ops.append((None, lambda: done[bset].record(side)))
+        elif overlap:
             dep(main, side)
         return ops
 
-    def run_step(i, ev=None, overlap=False):
-        for _, op in step_ops(i, ev, overlap):
+    def run_step(i, ev=None, overlap=False, pipelined=False):
+        for _, op in step_ops(i, ev, overlap or pipelined, pipelined):
             op()
 
     # ---- realised per-micro-step sizes (read back once, outside the timed region)
@@ -271,16 +294,22 @@ def main() -> int:
     # 0.83 ms per step), so the calls are launched one by one.
     evs = [new_events([dom]) for _ in range(args.steps)]
 
+    pipelined = overlap and not args.no_pipeline
+
     def timed_step(i, ev):
-        run_step(i, ev, overlap=overlap)
+        run_step(i, ev, overlap=overlap, pipelined=pipelined)
 
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for e in done:
+        e.record(side)
     for i in range(2):
         timed_step(i, None)
+    stream.wait_stream(side)
     torch.cuda.synchronize()
     start.record(stream)
     for s in range(args.steps):
         timed_step(s, evs[s])
+    stream.wait_stream(side)
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
@@ -361,7 +390,8 @@ def main() -> int:
                    "T": T, "d": d, "F": F, "E": E, "K": K, "local_experts": G, "slots": S_max,
                    "micro_steps": n_micro, "n_pairs_mean": round(float(np.mean(Ns)), 1),
                    "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns)),
-                   "backward_overlap": overlap, "tail_split": not args.no_split},
+                   "backward_overlap": overlap, "tail_split": not args.no_split,
+                   "pipelined_micro_steps": pipelined},
         "ms_per_step_sequential": round(seq_ms_per_step, 4),
         "roofline": roofline,
         "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),

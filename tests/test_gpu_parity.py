@@ -421,10 +421,13 @@ def test_determinism(gpu):
         assert torch.equal(a[k], b[k]), k
 
 
-def _backward_two_ways(w, gpu, n_micro):
-    """The benchmark's backward schedule (weight gradients on a second stream
-    beside the data gradients, sharing one workspace) against the same calls
-    on one stream, over consecutive micro-steps accumulating into dW."""
+def _backward_schedules(w, gpu, n_micro):
+    """The benchmark's schedules against one stream, over consecutive
+    micro-steps accumulating into dW: "overlap" runs the weight gradients on
+    a second stream beside the data gradients (sharing one workspace) and
+    joins the streams at the end of each micro-step; "pipelined" never joins
+    them, so the next micro-step's dispatch and forward start while this
+    one's weight gradients run (each micro-step keeps its own activations)."""
     from paper_2606_11867_amd import _lib, api
     lib = _lib.load()
     d, F = w.spec.d, w.spec.F
@@ -432,7 +435,8 @@ def _backward_two_ways(w, gpu, n_micro):
     BF = _lib.BF16 if dt == torch.bfloat16 else _lib.F32
     main, side = torch.cuda.current_stream(), torch.cuda.Stream()
     res = []
-    for overlap in (False, True):
+    for mode in ("seq", "overlap", "pipelined"):
+        overlap = mode != "seq"
         G = w.micro[0].plan.G
         dwgu = torch.zeros((G, 2 * F, d), dtype=torch.float32, device=gpu)
         dwdn = torch.zeros((G, d, F), dtype=torch.float32, device=gpu)
@@ -478,22 +482,28 @@ def _backward_two_ways(w, gpu, n_micro):
                 gate_up_wgrad(main)
                 down_wgrad(main)
             dx = api.permute_bwd(dxp, got["pair_to_row"], m.ids.shape[0], m.ids.shape[1], out_dtype=torch.float32)
-            if overlap:
+            if mode == "overlap":
                 main.wait_stream(side)
-            N = int(got["slot_offset"][-1].item())  # rows past N are not written
-            outs.append(dict(dx=dx, d_au=d_au[:N], dgates=dg))
+            outs.append(dict(dx=dx, d_au=d_au, dgates=dg, keep=(got, h, dyp, au, gidx, widx, gud, dnd, gates),
+                             so=got["slot_offset"]))
+        main.wait_stream(side)
         torch.cuda.synchronize()
+        for o in outs:
+            N = int(o.pop("so")[-1].item())  # rows past N are not written
+            o["d_au"] = o["d_au"][:N]
+            o.pop("keep")
         assert not wws[:256].any().item() and not rws[:4096].any().item(), "workspace counters not reset"
         res.append(dict(outs=outs, dwgu=dwgu, dwdn=dwdn))
     return res
 
 
-@pytest.mark.parametrize("name,n_micro", [("share", 3), ("cfg3", 2)])
-def test_backward_overlap_matches_one_stream(gpu, name, n_micro):
+@pytest.mark.parametrize("name,n_micro", [("share", 4), ("cfg3", 3)])
+def test_backward_schedules_match_one_stream(gpu, name, n_micro):
     w = _wl(name)
     _print_case(name, w, w.micro[0])
-    seq, ovl = _backward_two_ways(w, gpu, n_micro)
-    for i, (a, b) in enumerate(zip(seq["outs"], ovl["outs"])):
-        for k in a:
-            assert torch.equal(a[k], b[k]), f"micro-step {i}: {k} differs with the overlapped schedule"
-    assert torch.equal(seq["dwgu"], ovl["dwgu"]) and torch.equal(seq["dwdn"], ovl["dwdn"])
+    seq, *others = _backward_schedules(w, gpu, n_micro)
+    for tag, o in zip(("overlap", "pipelined"), others):
+        for i, (a, b) in enumerate(zip(seq["outs"], o["outs"])):
+            for k in a:
+                assert torch.equal(a[k], b[k]), f"micro-step {i}: {k} differs with the {tag} schedule"
+        assert torch.equal(seq["dwgu"], o["dwgu"]) and torch.equal(seq["dwdn"], o["dwdn"]), tag
