@@ -241,7 +241,8 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
  * finish adds the pieces' fp32 partial sums in piece order and writes the
  * tile. Results are deterministic either way and equal with and without the
  * workspace up to the fp32 summation order. Calls that share a workspace
- * must not overlap in time (same stream, or ordered by events). Too small or
+ * must not overlap in time (same stream, or ordered by events); after a
+ * call that did not complete, zero the workspace again. Too small or
  * misaligned: FOREMOE_EINVAL, nothing launched. Ignored for f32.
  */
 size_t foremoe_ffn_workspace_size(void);

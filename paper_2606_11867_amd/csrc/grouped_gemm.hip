@@ -828,7 +828,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   // One output tile, k-steps [kb, kb + nk). With split > 1 this is piece q
   // of a tile cut along K: the partial sums go to the workspace and the last
   // piece to arrive adds all pieces in piece order and writes the tile.
-  auto run_tile = [&](int t, int kb, int nk, int q, int split) {
+  auto run_tile = [&](int t, int kb, int nk, int q, int pieces) {
     const int mtg = t / n_tiles, nt = t % n_tiles;
     int lo = 0, hi = a.S - 1;
     while (lo < hi) {
@@ -894,24 +894,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
 
     core.zero();
     pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, nk, offs, issue);
-    if (split > 1) {
+    if (pieces > 1) {
       // piece q of tail tile t - dp is computed by workgroup v - q + q' for
       // piece q'; each keeps its partial sums in its own workspace slot
       const __amdgpu_buffer_rsrc_t rs = split_rsrc(a.sk_part, (uint32_t)G * (BM * BN * 4));
       split_store<CoreT, NW>(rs, v, wave, core);
       wait_vm<0>();  // this wave's partial sums have reached memory
       __syncthreads();
-      if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[t - dp], 1u) == (unsigned)(split - 1);
+      if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[t - dp], 1u) == (unsigned)(pieces - 1);
       __syncthreads();
       if (!s_last) return;
-      // the tile's pieces: slots v - q .. v - q + split - 1
+      // the tile's pieces: slots v - q .. v - q + pieces - 1
       {
         static_assert(NW * kSplitRegionKiB * 1024 <= NS * STAGE, "split pieces must fit in the ring");
         const __amdgpu_buffer_rsrc_t ts =
-            split_rsrc(a.sk_part + (size_t)(v - q) * (BM * BN), (uint32_t)split * (BM * BN * 4));
+            split_rsrc(a.sk_part + (size_t)(v - q) * (BM * BN), (uint32_t)pieces * (BM * BN * 4));
         char* wl = lds + wave * (kSplitRegionKiB * 1024);
-        if (split == 2) split_sum<NW, 2>(ts, wave, wl, core);
-        else if (split == 3) split_sum<NW, 3>(ts, wave, wl, core);
+        if (pieces == 2) split_sum<NW, 2>(ts, wave, wl, core);
+        else if (pieces == 3) split_sum<NW, 3>(ts, wave, wl, core);
         else split_sum<NW, 4>(ts, wave, wl, core);
       }
       if (threadIdx.x == 0) atomicExch(&a.sk_count[t - dp], 0u);  // ready for the next call
