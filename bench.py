@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
+    ap.add_argument("--no-reference-peaks", action="store_true",
+                    help="skip the measured square-GEMM and copy peaks reported beside the nominal ones")
     ap.add_argument("--no-split", action="store_true",
                     help="run the row GEMMs without the workspace (no K split of a partial last round of tiles)")
     ap.add_argument("--no-pipeline", action="store_true",
@@ -403,12 +405,56 @@ def main() -> int:
         "kernels": kernels,
         "setup_s": round(setup_s, 1),
     }
+    if not args.no_reference_peaks:
+        ref = reference_peaks(dev)
+        ref["dominant_kernel_frac"] = round(roofline["achieved"] / ref["bf16_gemm_tflops"], 4) \
+            if roofline["unit"] == "TFLOP/s" else None
+        ref["grouped_ffn_frac"] = round(out["grouped_ffn_tflops"] / ref["bf16_gemm_tflops"], 4)
+        ref["permute_frac"] = round(out["permute_gbs"] / ref["copy_gbs"], 4)
+        ref["combine_frac"] = round(out["combine_gbs"] / ref["copy_gbs"], 4)
+        out["measured_peaks"] = ref
     if not args.no_planner:
         out["planner"] = planner_report(w, api, dev, n_micro)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def reference_peaks(dev) -> dict:
+    """Context for the rooflines, measured outside the timed region: a large
+    square bf16 GEMM through torch (hipBLASLt) and a 1 GiB device copy (far
+    larger than the caches). Neither is part of the path."""
+    import torch
+    n = 8192
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        torch.matmul(a, b, out=c)
+    e1.record()
+    torch.cuda.synchronize()
+    gemm = 2.0 * n ** 3 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e12
+    del a, b, c
+    x = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    x.fill_(1)
+    y = torch.empty_like(x)
+    for _ in range(2):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    copy = 2.0 * (1 << 30) * 5 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    return {"bf16_gemm_tflops": round(gemm, 1), "bf16_gemm": "torch.matmul 8192^3 (hipBLASLt)",
+            "copy_gbs": round(copy, 1), "copy": "1 GiB device copy, bytes read + written"}
 
 
 def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> dict:
