@@ -153,7 +153,6 @@ def main() -> int:
     # row-GEMM workspace (tail split of a partial last round of tiles)
     rws, rwsz = (None, 0) if args.no_split else (P["rws"], buf["rws"].numel())
     stream = torch.cuda.current_stream(dev)
-    sp = stream.cuda_stream
     BF16 = _lib.BF16
     setup_s = time.time() - t0
 
@@ -162,7 +161,6 @@ def main() -> int:
             raise _lib.ForeMoEError(rc, what)
 
     side = torch.cuda.Stream(dev)  # default priority, like every stream here
-    ssp = side.cuda_stream
 
     done = [torch.cuda.Event(), torch.cuda.Event()]  # side-stream work of the micro-step using set b
 
