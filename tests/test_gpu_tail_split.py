@@ -6,7 +6,8 @@ split only changes the fp32 summation order of the Step-4 products).
 Row layouts are chosen so that the split really happens (the expected
 piece count per GEMM is computed here from the tile counts and asserted
 non-trivial): one with whole rounds of tiles plus a split tail, one with
-fewer tiles than workgroups (every tile split). Checked: sampled rows
+fewer tiles than workgroups (every tile split), one where the down dgrad
+runs on 128-wide output tiles (F not a multiple of 256). Checked: sampled rows
 against the fp64 oracle, split against unsplit within the tolerance, two
 split runs bit for bit equal, and the arrival counters left at zero.
 """
@@ -20,13 +21,15 @@ from workload import bf16_round
 
 pytestmark = pytest.mark.gpu
 
-D, F, W = 2048, 256, 3
+D, W = 2048, 3
 SPLIT_MAX, SPLIT_MIN_K = 4, 32
 
 
 def expected_split(rows, n_cols, k, grid):
-    """Pieces per tile of the last round (1: no split), as the kernel picks them."""
-    tiles = sum((r + 255) // 256 for r in rows) * (n_cols // 256)
+    """Pieces per tile of the last round (1: no split), as the kernel picks them
+    (256-wide output tiles when n_cols allows, else 128-wide)."""
+    bn = 256 if n_cols % 256 == 0 else 128
+    tiles = sum((r + 255) // 256 for r in rows) * (n_cols // bn)
     rem = tiles % grid
     if rem == 0 or k // 64 < SPLIT_MIN_K:
         return 1
@@ -46,13 +49,15 @@ def sampled(off, rng, per_slot=5):
     return np.array(rows), np.array(sub), np.array(widx)
 
 
-@pytest.mark.parametrize("rows", [[9000, 20000, 9400], [5000, 12000, 3000]], ids=["rounds+tail", "all-split"])
-def test_tail_split_parity_and_determinism(gpu, rows):
+@pytest.mark.parametrize("F,rows", [(256, [9000, 20000, 9400]), (256, [5000, 12000, 3000]),
+                                    (384, [3000, 6000, 1500])],
+                         ids=["rounds+tail", "all-split", "128-wide-tiles"])
+def test_tail_split_parity_and_determinism(gpu, F, rows):
     from paper_2606_11867_amd import api
     grid = torch.cuda.get_device_properties(gpu).multi_processor_count
     s_fwd = expected_split(rows, 2 * F, D, grid)   # gate/up forward: N = 2F, K = d
     s_dgr = expected_split(rows, F, D, grid)       # down dgrad: N = F, K = d
-    print(f"rows {rows}: pieces gate/up fwd {s_fwd}, down dgrad {s_dgr}", flush=True)
+    print(f"F={F} rows {rows}: pieces gate/up fwd {s_fwd}, down dgrad {s_dgr}", flush=True)
     assert max(s_fwd, s_dgr) >= 2, "layout no longer exercises the split"
     rng = np.random.default_rng(5)
     off = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
