@@ -69,9 +69,12 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 // Virtual workgroup id: workgroups are dispatched round-robin over the 8 XCDs,
 // so give the workgroups of one XCD consecutive ids (they then share tiles
 // that reuse the same operand rows in that XCD's L2).
+#ifndef FM_XCD_MAP
+#define FM_XCD_MAP 1
+#endif
 __device__ __forceinline__ int xcd_virtual_id() {
   const int b = blockIdx.x, n = gridDim.x;
-  if (n % 8 != 0) return b;
+  if (!FM_XCD_MAP || n % 8 != 0) return b;
   return (b % 8) * (n / 8) + b / 8;
 }
 
@@ -121,6 +124,19 @@ __device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds_wave_base, uint32_t
                : "memory");
 }
 
+// The same with lane offset voff0 + soff (soff wave-uniform): the add sits
+// in the asm so that one temporary serves every load instead of one
+// precomputed offset register per load.
+__device__ __forceinline__ void dma16s(i32x4 rs, uint32_t lds_wave_base, uint32_t voff0, uint32_t soff) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_wave_base);
+  uint32_t t;
+  asm volatile(
+      "v_add_u32 %0, %1, %2\n\ts_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %4, 0 offen lds"
+      : "=&v"(t)
+      : "s"(soff), "v"(voff0), "s"(m0v), "s"(rs)
+      : "memory");
+}
+
 // Wait until at most N vector-memory operations of this wavefront are in flight.
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -163,6 +179,11 @@ struct KTile {
   __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, uint32_t voff, int i) {
     dma16(rs, lds + (wave_id() + NW * i) * 1024, voff);
   }
+  // load i with lane offset voff(0) + soff_i, soff_i = voff(i) - voff(0) (the
+  // same for every lane: the swizzle of a row or k row does not change by i)
+  __device__ __forceinline__ static void issue_s(i32x4 rs, uint32_t lds, uint32_t voff0, uint32_t soff, int i) {
+    dma16s(rs, lds + (wave_id() + NW * i) * 1024, voff0, soff);
+  }
   // MFMA operand for rows mn0..mn0+31 of the tile, k-step kk (16 k values):
   // lane l gets row mn0 + l % 32, k = 16 kk + 8 (l / 32) + 0..7. The swizzle
   // only depends on l % 32 (mn0 is a multiple of 32), so the address splits
@@ -200,6 +221,11 @@ struct MTile {
   }
   __device__ __forceinline__ static void issue(i32x4 rs, uint32_t lds, uint32_t voff, int i) {
     dma16(rs, lds + (wave_id() + NW * i) * 1024, voff);
+  }
+  // load i with lane offset voff(0) + soff_i, soff_i = voff(i) - voff(0) (the
+  // same for every lane: the swizzle of a row or k row does not change by i)
+  __device__ __forceinline__ static void issue_s(i32x4 rs, uint32_t lds, uint32_t voff0, uint32_t soff, int i) {
+    dma16s(rs, lds + (wave_id() + NW * i) * 1024, voff0, soff);
   }
   // Same operand layout as KTile::frag, assembled from two transpose reads:
   // in each 16-lane group g, lane i addresses 4 consecutive m/n of one k row
@@ -697,6 +723,9 @@ __device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& co
 // fence is needed: such a fence would write back and invalidate the whole
 // L2 of the XCD, evicting the operand tiles that every other workgroup there
 // is using.
+#ifndef FM_TAIL_SPREAD
+#define FM_TAIL_SPREAD 1
+#endif
 #ifndef FM_SPLIT_MAX
 #define FM_SPLIT_MAX 4
 #endif
@@ -705,7 +734,10 @@ __device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& co
 #endif
 constexpr int kSplitMax = FM_SPLIT_MAX;    // pieces per tile at most (2..4)
 constexpr int kSplitMinK = FM_SPLIT_MIN_K;  // k-steps a tile needs before it is split
-constexpr int kSplitRegionKiB = 16;  // LDS per wave for the pieces in flight
+#ifndef FM_SPLIT_REGION_KIB
+#define FM_SPLIT_REGION_KIB 16
+#endif
+constexpr int kSplitRegionKiB = FM_SPLIT_REGION_KIB;  // LDS per wave for the pieces in flight
 constexpr int kCoherentDevice = 16;  // cache policy of buffer accesses: SC1
 
 template <class CoreT, int NW>
@@ -824,11 +856,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     split = G / r;
     split = split < kSplitMax ? split : kSplitMax;
   }
-  const int dp = split > 1 ? total - r : total;
+  const int full = total - r;  // tiles of the whole rounds
   // One output tile, k-steps [kb, kb + nk). With split > 1 this is piece q
   // of a tile cut along K: the partial sums go to the workspace and the last
   // piece to arrive adds all pieces in piece order and writes the tile.
-  auto run_tile = [&](int t, int kb, int nk, int q, int pieces) {
+  auto run_tile = [&](int t, int kb, int nk, int q, int pieces, int slot) {
     const int mtg = t / n_tiles, nt = t % n_tiles;
     int lo = 0, hi = a.S - 1;
     while (lo < hi) {
@@ -856,65 +888,64 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     const uint32_t abytes = (uint32_t)((rend - rbeg) * a.lda * 2);
     const uint16_t* bbase = a.B + (int64_t)w * a.wstride;
     const uint32_t bbytes = (uint32_t)(a.wstride * 2);
-    uint32_t va[AT::PER_WAVE], vb[BT::PER_WAVE];
-#pragma unroll
-    for (int i = 0; i < AT::PER_WAVE; ++i)
-      va[i] = AT::voff([&](int r) -> uint32_t { return (uint32_t)(mrel + r) * lda2; }, i);
-#pragma unroll
-    for (int i = 0; i < BT::PER_WAVE; ++i) {
+    auto arow = [&](int r) -> uint32_t { return (uint32_t)(mrel + r) * lda2; };
+    auto brow = [&](int r) -> uint32_t {
       if constexpr (B_KMAJ) {
-        vb[i] = BT::voff(
-            [&](int r) -> uint32_t {
-              int wr;
-              if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
-              else wr = n0 + r;
-              return (uint32_t)wr * ldb2;
-            },
-            i);
+        int wr;
+        if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
+        else wr = n0 + r;
+        return (uint32_t)wr * ldb2;
       } else {
         // K-major weights: element (n, k) at (k * ldb + n) * 2
-        vb[i] = BT::voff([&](int k) -> uint32_t { return (uint32_t)k * ldb2 + (uint32_t)n0 * 2u; }, i);
+        return (uint32_t)r * ldb2 + (uint32_t)n0 * 2u;
       }
-    }
+    };
+    const uint32_t va0 = AT::voff(arow, 0), vb0 = BT::voff(brow, 0);
+    uint32_t sa_[AT::PER_WAVE], sb_[BT::PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < AT::PER_WAVE; ++i) sa_[i] = __builtin_amdgcn_readfirstlane(AT::voff(arow, i) - va0);
+#pragma unroll
+    for (int i = 0; i < BT::PER_WAVE; ++i) sb_[i] = __builtin_amdgcn_readfirstlane(BT::voff(brow, i) - vb0);
     auto issue = [&](int kt, int p) {
       // stages past the last load nothing (zero-size resources)
       const bool live = kt < nk;
       const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
       const uint32_t k0 = live ? (uint32_t)((kb + kt) * BK) : 0u;
       if (p < AT::PER_WAVE) {
-        AT::issue(buf_rsrc(abase + k0, live ? abytes - 2u * k0 : 0u), sa, va[p], p);
+        AT::issue_s(buf_rsrc(abase + k0, live ? abytes - 2u * k0 : 0u), sa, va0, sa_[p], p);
       } else if constexpr (B_KMAJ) {
-        BT::issue(buf_rsrc(bbase + k0, live ? bbytes - 2u * k0 : 0u), sa + AT::BYTES, vb[p - AT::PER_WAVE],
-                  p - AT::PER_WAVE);
+        BT::issue_s(buf_rsrc(bbase + k0, live ? bbytes - 2u * k0 : 0u), sa + AT::BYTES, vb0, sb_[p - AT::PER_WAVE],
+                    p - AT::PER_WAVE);
       } else {
-        BT::issue(buf_rsrc(bbase + (int64_t)k0 * a.ldb, live ? bbytes - k0 * ldb2 : 0u), sa + AT::BYTES,
-                  vb[p - AT::PER_WAVE], p - AT::PER_WAVE);
+        BT::issue_s(buf_rsrc(bbase + (int64_t)k0 * a.ldb, live ? bbytes - k0 * ldb2 : 0u), sa + AT::BYTES, vb0,
+                    sb_[p - AT::PER_WAVE], p - AT::PER_WAVE);
       }
     };
 
     core.zero();
     pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, nk, offs, issue);
     if (pieces > 1) {
-      // piece q of tail tile t - dp is computed by workgroup v - q + q' for
-      // piece q'; each keeps its partial sums in its own workspace slot
+      // piece q' of tail tile t - full is computed by the workgroup with
+      // slot slot - q + q'; each keeps its partial sums in its own
+      // workspace slot
       const __amdgpu_buffer_rsrc_t rs = split_rsrc(a.sk_part, (uint32_t)G * (BM * BN * 4));
-      split_store<CoreT, NW>(rs, v, wave, core);
+      split_store<CoreT, NW>(rs, slot, wave, core);
       wait_vm<0>();  // this wave's partial sums have reached memory
       __syncthreads();
-      if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[t - dp], 1u) == (unsigned)(pieces - 1);
+      if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[t - full], 1u) == (unsigned)(pieces - 1);
       __syncthreads();
       if (!s_last) return;
-      // the tile's pieces: slots v - q .. v - q + pieces - 1
+      // the tile's pieces: slots slot - q .. slot - q + pieces - 1
       {
         static_assert(NW * kSplitRegionKiB * 1024 <= NS * STAGE, "split pieces must fit in the ring");
         const __amdgpu_buffer_rsrc_t ts =
-            split_rsrc(a.sk_part + (size_t)(v - q) * (BM * BN), (uint32_t)pieces * (BM * BN * 4));
+            split_rsrc(a.sk_part + (size_t)(slot - q) * (BM * BN), (uint32_t)pieces * (BM * BN * 4));
         char* wl = lds + wave * (kSplitRegionKiB * 1024);
         if (pieces == 2) split_sum<NW, 2>(ts, wave, wl, core);
         else if (pieces == 3) split_sum<NW, 3>(ts, wave, wl, core);
         else split_sum<NW, 4>(ts, wave, wl, core);
       }
-      if (threadIdx.x == 0) atomicExch(&a.sk_count[t - dp], 0u);  // ready for the next call
+      if (threadIdx.x == 0) atomicExch(&a.sk_count[t - full], 0u);  // ready for the next call
     }
     static_assert(NW * EpiBytes<CoreT, EPI>::PER_WAVE <= NS * STAGE, "epilogue staging must fit in the ring");
     __syncthreads();  // every wave is done reading the ring: it now stages the epilogue
@@ -923,11 +954,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     __syncthreads();  // staging reads done before the next tile's loads overwrite the ring
   };
 
-  for (int t = v; t < dp; t += G) run_tile(t, 0, KT, 0, 1);
-  if (split > 1 && v < r * split) {
-    const int q = v % split;
+  // Whole rounds take the XCD-grouped ids. A partial last round that keeps
+  // at most 7/8 of the workgroups busy spreads its tiles evenly over the
+  // XCDs instead (tile i on XCD i % 8): the XCDs share only memory, so such
+  // a round runs faster on eight partly busy XCDs than on fewer full ones.
+  // Unsplit, that is the hardware id; split, the pieces of a tile stay on
+  // one XCD (workgroups c * 8 + x, c = j * split + q for piece q of the
+  // XCD's j-th tile) when every XCD can hold its tiles' pieces.
+  for (int t = v; t < full; t += G) run_tile(t, 0, KT, 0, 1, v);
+  const int busy = r * split;
+  int u = v;
+  if (FM_TAIL_SPREAD && G % 8 == 0 && 8 * busy <= 7 * G) {
+    const int b = blockIdx.x, tpx = (G / 8) / split;  // tiles per XCD
+    if (split == 1) {
+      u = b;
+    } else if (r <= 8 * tpx) {
+      const int c = b / 8, j = c / split;
+      u = j < tpx ? (j * 8 + b % 8) * split + c % split : busy;  // busy: idle workgroup
+    }
+  }
+  if (u < busy) {
+    const int q = u % split;
     const int kb = q * KT / split, ke = (q + 1) * KT / split;
-    run_tile(dp + v / split, kb, ke - kb, q, split);
+    run_tile(full + u / split, kb, ke - kb, q, split, u);
   }
 }
 
