@@ -955,22 +955,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   };
 
   // Whole rounds take the XCD-grouped ids. A partial last round that keeps
-  // at most 7/8 of the workgroups busy spreads its tiles evenly over the
-  // XCDs instead (tile i on XCD i % 8): the XCDs share only memory, so such
-  // a round runs faster on eight partly busy XCDs than on fewer full ones.
-  // Unsplit, that is the hardware id; split, the pieces of a tile stay on
-  // one XCD (workgroups c * 8 + x, c = j * split + q for piece q of the
-  // XCD's j-th tile) when every XCD can hold its tiles' pieces.
+  // at most 7/8 of the workgroups busy is spread over all eight XCDs
+  // instead, in blocks: XCD x takes tiles [x * tpx, (x + 1) * tpx), so that
+  // neighbouring tiles (which share operand rows or weights) still share an
+  // L2, with the pieces of a split tile on consecutive workgroups of that
+  // XCD. The XCDs share only memory, so such a round runs faster on eight
+  // partly busy XCDs than on fewer full ones.
   for (int t = v; t < full; t += G) run_tile(t, 0, KT, 0, 1, v);
   const int busy = r * split;
   int u = v;
   if (FM_TAIL_SPREAD && G % 8 == 0 && 8 * busy <= 7 * G) {
-    const int b = blockIdx.x, tpx = (G / 8) / split;  // tiles per XCD
-    if (split == 1) {
-      u = b;
-    } else if (r <= 8 * tpx) {
-      const int c = b / 8, j = c / split;
-      u = j < tpx ? (j * 8 + b % 8) * split + c % split : busy;  // busy: idle workgroup
+    const int b = blockIdx.x, tpx = (r + 7) / 8;  // tiles per XCD
+    if (tpx * split <= G / 8) {
+      const int x = b % 8, c = b / 8, j = c / split, i = x * tpx + j;
+      u = (j < tpx && i < r) ? i * split + c % split : busy;  // busy: idle workgroup
     }
   }
   if (u < busy) {
