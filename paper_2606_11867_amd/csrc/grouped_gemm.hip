@@ -1185,13 +1185,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
     for (KCursor cc = cursor_begin(P, S, g, s0, s1); !cc.done; cursor_next_slot(P, S, g, s1, cc))
       KT += (cc.hi - cc.lo + BK - 1) / BK;
     KCursor ic = cursor_begin(P, S, g, s0, s1);
-    uint32_t va[AT::PER_WAVE], vb[BT::PER_WAVE];
+    auto koa = [&](int k) -> uint32_t { return (uint32_t)k * lda2 + (uint32_t)m0 * 2u; };
+    auto kob = [&](int k) -> uint32_t { return (uint32_t)k * ldb2 + (uint32_t)n0 * 2u; };
+    const uint32_t va0 = AT::voff(koa, 0), vb0 = BT::voff(kob, 0);
+    uint32_t sa_[AT::PER_WAVE], sb_[BT::PER_WAVE];
 #pragma unroll
-    for (int i = 0; i < AT::PER_WAVE; ++i)
-      va[i] = AT::voff([&](int k) -> uint32_t { return (uint32_t)k * lda2 + (uint32_t)m0 * 2u; }, i);
+    for (int i = 0; i < AT::PER_WAVE; ++i) sa_[i] = __builtin_amdgcn_readfirstlane(AT::voff(koa, i) - va0);
 #pragma unroll
-    for (int i = 0; i < BT::PER_WAVE; ++i)
-      vb[i] = BT::voff([&](int k) -> uint32_t { return (uint32_t)k * ldb2 + (uint32_t)n0 * 2u; }, i);
+    for (int i = 0; i < BT::PER_WAVE; ++i) sb_[i] = __builtin_amdgcn_readfirstlane(BT::voff(kob, i) - vb0);
     auto issue = [&](int kt, int p) {
       // the loads of one k-tile are issued in order p = 0 .. PER-1, k-tiles
       // in order: load the cursor's k-tile, advance after its last load. The
@@ -1203,10 +1204,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
       const int k = live ? ic.k : 0;
       const uint32_t nrow = live ? (uint32_t)(ic.hi - ic.k) : 0u;
       if (p < AT::PER_WAVE) {
-        AT::issue(buf_rsrc(a.A + (int64_t)k * a.lda, nrow * lda2), sa, va[p], p);
+        AT::issue_s(buf_rsrc(a.A + (int64_t)k * a.lda, nrow * lda2), sa, va0, sa_[p], p);
       } else {
-        BT::issue(buf_rsrc(a.B + (int64_t)k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb[p - AT::PER_WAVE],
-                  p - AT::PER_WAVE);
+        BT::issue_s(buf_rsrc(a.B + (int64_t)k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb0, sb_[p - AT::PER_WAVE],
+                    p - AT::PER_WAVE);
       }
       if (p == AT::PER_WAVE + BT::PER_WAVE - 1 && live) cursor_advance<BK>(P, S, g, s1, ic);
     };
@@ -1247,24 +1248,43 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
           }
         }
         wait_vm<0>();
+        // add the accumulators in place (LDS row r, chunk pc holds the
+        // global chunk pc ^ (r % CH) of row r)...
 #pragma unroll
         for (int ii = 0; ii < 2; ++ii) {
           const int i = ph * 2 + ii;
           if (i >= CoreT::MB) break;
-          const int64_t m = m0 + wm * CoreT::WM + i * 32 + l32;
 #pragma unroll
           for (int jj = 0; jj < CoreT::NB; ++jj) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int nl = jj * 32 + q * 8 + c4;
               const int pc = (nl / 4) ^ (l32 & (CH - 1));
-              float4 o = *reinterpret_cast<const float4*>(wl + ii * (32 * RB) + l32 * RB + pc * 16);
+              float4* lp = reinterpret_cast<float4*>(wl + ii * (32 * RB) + l32 * RB + pc * 16);
+              float4 o = *lp;
               o.x += core.acc[i][jj][q * 4 + 0];
               o.y += core.acc[i][jj][q * 4 + 1];
               o.z += core.acc[i][jj][q * 4 + 2];
               o.w += core.acc[i][jj][q * 4 + 3];
-              *reinterpret_cast<float4*>(Cg + m * a.ldc + nb + nl) = o;
+              *lp = o;
             }
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the sums are in LDS
+        // ...then store them from the lanes that loaded them: each store
+        // instruction writes whole row segments (full 128-byte lines)
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii) {
+          const int i = ph * 2 + ii;
+          if (i >= CoreT::MB) break;
+          const int mb = m0 + wm * CoreT::WM + i * 32;
+#pragma unroll
+          for (int q = 0; q < 32 * RB / 1024; ++q) {
+            const int r = q * (1024 / RB) + (lane * 16) / RB;
+            const int pc = ((lane * 16) % RB) / 16;
+            const int lc = pc ^ (r & (CH - 1));
+            const float4 o = *reinterpret_cast<const float4*>(wl + ii * (32 * RB) + q * 1024 + lane * 16);
+            *reinterpret_cast<float4*>(Cg + (int64_t)(mb + r) * a.ldc + nb + lc * 4) = o;
           }
         }
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): LDS reads done before the region is refilled
