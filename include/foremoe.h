@@ -236,9 +236,10 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
  * caller-owned device memory of at least foremoe_ffn_workspace_size()
  * bytes, 256-byte aligned, zero-filled before its first use (the library
  * leaves its counters at zero after every call). With it, a last round of
- * output tiles that would occupy at most half of the GPU's CUs is cut
- * along K (in GEMMs whose K is at least 2048) into up to 4 pieces, each
- * computed by its own workgroup; the last piece to
+ * output tiles that would occupy at most 7/16 of the GPU's CUs is cut
+ * along K (in GEMMs whose K is at least 2048) into up to 4 pieces (as many
+ * as keep at most 7/8 of the CUs busy), each computed by its own
+ * workgroup; the last piece to
  * finish adds the pieces' fp32 partial sums in piece order and writes the
  * tile. Results are deterministic either way and equal with and without the
  * workspace up to the fp32 summation order. Calls that share a workspace

@@ -853,8 +853,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   const int r = total % G;
   int split = 1;
   if (a.sk_part && r > 0 && KT >= kSplitMinK) {
-    split = G / r;
+    // as many pieces as keep at most 7/8 of the workgroups busy, so that
+    // the round is also spread over the XCDs (below); a split that fills
+    // the GPU measured slower than the unsplit round spread out
+    split = (7 * G / 8) / r;
     split = split < kSplitMax ? split : kSplitMax;
+    if (split < 2) split = 1;
   }
   const int full = total - r;  // tiles of the whole rounds
   // One output tile, k-steps [kb, kb + nk). With split > 1 this is piece q

@@ -27,13 +27,15 @@ SPLIT_MAX, SPLIT_MIN_K = 4, 32
 
 def expected_split(rows, n_cols, k, grid):
     """Pieces per tile of the last round (1: no split), as the kernel picks them
-    (256-wide output tiles when n_cols allows, else 128-wide)."""
+    (256-wide output tiles when n_cols allows, else 128-wide): as many as keep
+    at most 7/8 of the workgroups busy, at most SPLIT_MAX."""
     bn = 256 if n_cols % 256 == 0 else 128
     tiles = sum((r + 255) // 256 for r in rows) * (n_cols // bn)
     rem = tiles % grid
     if rem == 0 or k // 64 < SPLIT_MIN_K:
         return 1
-    return min(grid // rem, SPLIT_MAX)
+    s = min((7 * grid // 8) // rem, SPLIT_MAX)
+    return s if s >= 2 else 1
 
 
 def sampled(off, rng, per_slot=5):
@@ -50,7 +52,7 @@ def sampled(off, rng, per_slot=5):
 
 
 @pytest.mark.parametrize("F,rows", [(256, [9000, 20000, 9400]), (256, [5000, 12000, 3000]),
-                                    (384, [3000, 6000, 1500])],
+                                    (384, [2000, 5000, 1500])],
                          ids=["rounds+tail", "all-split", "128-wide-tiles"])
 def test_tail_split_parity_and_determinism(gpu, F, rows):
     from paper_2606_11867_amd import api
