@@ -48,6 +48,8 @@ PHASES = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine", "
 # phases that are exactly one kernel launch (candidates for the roofline line)
 SINGLE_LAUNCH = {"gate_up_fwd", "down_fwd", "combine", "combine_bwd", "down_dgrad",
                  "gate_up_dgrad", "permute_bwd"}
+# row-GEMM phases: one kernel each, timed by events attached to the launch
+ROW_GEMMS = {"gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad"}
 
 
 def parse():
@@ -190,10 +192,16 @@ def main() -> int:
         def call(phase, st, rc_fn):
             def run():
                 timed = ev is not None and phase in ev
-                if timed:
+                # row GEMMs carry their events on the kernel dispatch itself
+                # (no event commands between the kernels); the other phases
+                # are bracketed by event records on their stream
+                on_launch = timed and phase in ROW_GEMMS
+                if on_launch:
+                    lib.foremoe_set_launch_events(ev[phase][0].cuda_event, ev[phase][1].cuda_event)
+                elif timed:
                     ev[phase][0].record(st)
                 chk(rc_fn(st.cuda_stream), phase)
-                if timed:
+                if timed and not on_launch:
                     ev[phase][1].record(st)
             ops.append((phase, run))
 
@@ -266,13 +274,19 @@ def main() -> int:
     torch.cuda.synchronize()
 
     def new_events(phases=PHASES):
-        return {p: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for p in phases}
+        evp = {p: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for p in phases}
+        for a, b in evp.values():  # create the HIP events now (a launch can only update existing ones)
+            a.record(stream)
+            b.record(stream)
+        return evp
 
     def phase_sums(evs, phases=PHASES):
         return {p: sum(ev[p][0].elapsed_time(ev[p][1]) for ev in evs) for p in phases}
 
-    # ---- per-kernel pass: every phase bracketed by HIP events, one kernel
-    # after another, so that every phase's duration is its own
+    # ---- per-kernel pass: every phase timed by HIP events, one kernel after
+    # another, so that every phase's duration is its own (row GEMMs: events
+    # attached to the kernel launch, i.e. the kernel's start and end; other
+    # phases: event records around the call)
     evs_seq = [new_events() for _ in range(args.steps)]
     torch.cuda.synchronize()
     seq0, seq1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -284,12 +298,14 @@ def main() -> int:
     phase_ms = phase_sums(evs_seq)
     seq_ms_per_step = seq0.elapsed_time(seq1) / args.steps
     # the dominant single-launch kernel; in the timed region only its calls
-    # are bracketed by events (on the stream it runs on)
+    # carry events (on the stream it runs on)
     dom = max((p for p in PHASES if p in SINGLE_LAUNCH), key=lambda p: phase_ms[p])
 
     # ---- timed region: the step as it runs (backward GEMMs overlapped);
-    # only the dominant kernel's calls are bracketed by HIP events (events
-    # around every call cost about 80 us per step). Replaying the step from
+    # only the dominant kernel's calls carry HIP events, attached to its
+    # launches so that no event command sits between kernels (event records
+    # around every call cost about 80 us per step; a record pair around one
+    # kernel left two gaps of about 6 us). Replaying the step from
     # HIP graphs was measured slower than launching the calls (0.87 vs
     # 0.83 ms per step), so the calls are launched one by one.
     evs = [new_events([dom]) for _ in range(args.steps)]

@@ -428,6 +428,21 @@ int foremoe_plan_rank_slots(const int32_t* copy_rank, int32_t E, int32_t C_max, 
                             int32_t* slot_widx, int32_t* expert_nrep, int32_t* local_experts,
                             int32_t* S_out, int32_t* W_out);
 
+/*
+ * Kernel timing (a measurement hook, not an operation of the method).
+ * start, stop: hipEvent_t handles owned by the caller, created beforehand
+ * with timing enabled, or NULL. They are attached to the next bf16 row-GEMM
+ * kernel this host thread launches (foremoe_ffn_gate_up_fwd,
+ * foremoe_ffn_down_fwd, foremoe_ffn_down_dgrad, foremoe_ffn_gate_up_dgrad;
+ * in foremoe_grouped_ffn_fwd and foremoe_grouped_ffn_dgrad the first of their
+ * two launches) and then dropped: the events are set when that kernel
+ * starts and when it ends, with no separate event command in the stream, so
+ * hipEventElapsedTime(start, stop) is the kernel's own duration. A call that
+ * fails before launching leaves them attached; NULL, NULL detaches them.
+ * Always returns FOREMOE_OK.
+ */
+int foremoe_set_launch_events(void* start, void* stop);
+
 /* Utilities (host only, no GPU work). */
 const char* foremoe_status_string(int status);
 const char* foremoe_last_error(void); /* message of this thread's last failed call */

@@ -1494,13 +1494,16 @@ void launch_rows(RowsArgs a, void* ws, hipStream_t st) {
     a.sk_count = (unsigned*)ws;
     a.sk_part = (float*)((char*)ws + kRowsCountBytes);
   }
+  // events attached by foremoe_set_launch_events ride on the dispatch itself
+  hipEvent_t e0, e1;
+  take_launch_events(&e0, &e1);
   if constexpr (BN == 256) {
     constexpr int WGM = FM_ROWS_WGM, WGN = FM_ROWS_WGN;
-    hipLaunchKernelGGL((gemm_rows_kernel<256, 256, FM_ROWS_BK, FM_ROWS_NS, WGM, WGN, KMAJ, EPI>),
-                       dim3(persistent_grid()), dim3(64 * WGM * WGN), 0, st, a);
+    hipExtLaunchKernelGGL(gemm_rows_kernel<256, 256, FM_ROWS_BK, FM_ROWS_NS, WGM, WGN, KMAJ, EPI>,
+                          dim3(persistent_grid()), dim3(64 * WGM * WGN), 0, st, e0, e1, 0, a);
   } else {
-    hipLaunchKernelGGL((gemm_rows_kernel<256, 128, 64, 3, 2, 2, KMAJ, EPI>), dim3(persistent_grid()), dim3(256), 0,
-                       st, a);
+    hipExtLaunchKernelGGL(gemm_rows_kernel<256, 128, 64, 3, 2, 2, KMAJ, EPI>, dim3(persistent_grid()), dim3(256), 0,
+                          st, e0, e1, 0, a);
   }
 }
 

@@ -48,6 +48,13 @@ def test_version_and_status_strings(lib):
     assert lib.foremoe_status_string(-2) == b"unsupported shape or dtype"
 
 
+def test_set_launch_events_is_host_only(lib):
+    # attaching and detaching events touches no GPU state (no HIP call)
+    assert lib.foremoe_set_launch_events(None, None) == 0
+    assert lib.foremoe_set_launch_events(ctypes.c_void_p(0x1000), None) == 0
+    assert lib.foremoe_set_launch_events(None, None) == 0
+
+
 def test_workspace_size(lib):
     small = lib.foremoe_workspace_size(256, 2, 8)
     assert small > 0 and small % 256 == 0
