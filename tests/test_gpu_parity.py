@@ -248,6 +248,52 @@ def test_ffn_forward_sampled_rows_full_size(gpu, name):
     check_close("Y", to_np(y[torch.from_numpy(rows).to(gpu)]), f["Y"])
 
 
+@pytest.mark.parametrize("name", ["cfg2", "cfg4"])
+def test_ffn_backward_sampled_full_size(gpu, name):
+    """Full-size input and weight gradients (the row-GEMM and weight-gradient
+    workspaces as the benchmark uses them) from seeded inputs: the oracle
+    recomputes sampled rows of every slot for dA, dU, dX, and sampled
+    columns of every group's dW (the weight gradient is separable by
+    column, so the oracle runs on those columns only)."""
+    from paper_2606_11867_amd import api
+    w = _wl(name)
+    m = _ms(w)
+    _print_case(name, w, m)
+    ref, N, gu, dn, x_perm = _ffn_inputs(w, m)
+    d, F, G = w.spec.d, w.spec.F, m.plan.G
+    rng = np.random.default_rng(2024)
+    dy_perm = rnd(w, rng.standard_normal((N, d), dtype=np.float32))
+    au = rnd(w, 2.0 * rng.standard_normal((N, 2 * F), dtype=np.float32))   # saved [A | U]
+    hq = rnd(w, rng.standard_normal((N, F), dtype=np.float32))             # saved H
+    dau = rnd(w, rng.standard_normal((N, 2 * F), dtype=np.float32))        # [dA | dU] for dW
+    dt = tdtype(w)
+    so = torch.from_numpy(ref["slot_offset"]).to(gpu)
+    widx = torch.from_numpy(m.plan.slot_widx).to(gpu)
+    gidx = torch.from_numpy(m.plan.slot_gidx).to(gpu)
+    xd, dyd, gud, dnd = to_dev(x_perm, dt, gpu), to_dev(dy_perm, dt, gpu), to_dev(gu, dt, gpu), to_dev(dn, dt, gpu)
+    ws = _ffn_ws(gpu, True)
+    d_au, dx = api.grouped_ffn_dgrad(dyd, to_dev(au, dt, gpu), so, widx, gud, dnd, ws=ws)
+    dwgu = torch.zeros((G, 2 * F, d), dtype=torch.float32, device=gpu)
+    dwdn = torch.zeros((G, d, F), dtype=torch.float32, device=gpu)
+    api.grouped_ffn_wgrad(xd, to_dev(hq, dt, gpu), dyd, to_dev(dau, dt, gpu), so, gidx, dwgu, dwdn,
+                          ws=api.wgrad_workspace(d, F, gpu))
+    torch.cuda.synchronize()
+    _check_ws_reset(ws)
+    rows, sub_off, sub_widx = _sampled_rows(ref, m, np.random.default_rng(0))
+    g = O.ffn_dgrad(dy_perm[rows], au[rows, :F], au[rows, F:], sub_off, sub_widx, gu, dn)
+    rt = torch.from_numpy(rows).to(gpu)
+    check_close("dA", to_np(d_au[rt][:, :F]), g["dA"])
+    check_close("dU", to_np(d_au[rt][:, F:]), g["dU"])
+    check_close("dX", to_np(dx[rt]), g["dX"])
+    cx, cy, cf = (np.sort(rng.choice(n, size=4, replace=False)) for n in (d, d, F))
+    rgu, rdn = O.ffn_wgrad(x_perm[:, cx], hq[:, cf], dy_perm[:, cy], dau[:, cf], dau[:, F + cf], ref["slot_offset"],
+                           m.plan.slot_gidx, G)
+    rows_gu = torch.from_numpy(np.concatenate([cf, F + cf])).to(gpu)
+    check_close("dW_gate_up (sampled)", to_np(dwgu[:, rows_gu][:, :, torch.from_numpy(cx).to(gpu)]), rgu)
+    check_close("dW_down (sampled)",
+                to_np(dwdn[:, torch.from_numpy(cy).to(gpu)][:, :, torch.from_numpy(cf).to(gpu)]), rdn)
+
+
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
 def test_ffn_backward(gpu, name, split):

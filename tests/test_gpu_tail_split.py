@@ -68,10 +68,13 @@ def test_tail_split_parity_and_determinism(gpu, F, rows):
     dy = bf16_round(rng.standard_normal((N, D)).astype(np.float32))
     gu = bf16_round((rng.standard_normal((W, 2 * F, D)) / np.sqrt(D)).astype(np.float32))
     dn = bf16_round((rng.standard_normal((W, D, F)) / np.sqrt(F)).astype(np.float32))
+    # saved [A | U] for the input gradient: seeded inputs of their own (the
+    # forward's are checked against the oracle separately)
+    au_in = bf16_round((2.0 * rng.standard_normal((N, 2 * F))).astype(np.float32))
     widx = (np.arange(len(rows)) % W).astype(np.int32)
     bf = torch.bfloat16
     dev = lambda a: torch.from_numpy(a).to(gpu).to(bf)  # noqa: E731
-    xd, dyd, gud, dnd = dev(x), dev(dy), dev(gu), dev(dn)
+    xd, dyd, gud, dnd, aud = dev(x), dev(dy), dev(gu), dev(dn), dev(au_in)
     so = torch.from_numpy(off).to(gpu)
     wi = torch.from_numpy(widx).to(gpu)
     ws = api.ffn_workspace(gpu)
@@ -79,7 +82,7 @@ def test_tail_split_parity_and_determinism(gpu, F, rows):
     runs = []
     for w_ in (ws, ws, None):
         h, y, au = api.grouped_ffn_fwd(xd, so, wi, gud, dnd, ws=w_)
-        d_au, dx = api.grouped_ffn_dgrad(dyd, au, so, wi, gud, dnd, ws=w_)
+        d_au, dx = api.grouped_ffn_dgrad(dyd, aud, so, wi, gud, dnd, ws=w_)
         runs.append(dict(h=h, y=y, au=au, d_au=d_au, dx=dx))
     torch.cuda.synchronize()
     assert not ws[:4096].any().item(), "split arrival counters not reset"
@@ -87,15 +90,15 @@ def test_tail_split_parity_and_determinism(gpu, F, rows):
         assert torch.equal(runs[0][k], runs[1][k]), f"{k}: split result not deterministic"
         check_close(f"{k} split vs unsplit", to_np(runs[0][k]), to_np(runs[2][k]))
 
-    # sampled rows of every slot against the oracle (forward from x; input
-    # gradient from the kernel's own rounded A and U, as the backward uses)
+    # sampled rows of every slot against the oracle
     r, sub, sw = sampled(off, rng)
     f = O.ffn_forward(x[r].astype(np.float64), sub, sw, gu, dn)
     rt = torch.from_numpy(r).to(gpu)
     check_close("H", to_np(runs[0]["h"][rt]), f["H"])
     check_close("Y", to_np(runs[0]["y"][rt]), f["Y"])
-    au = to_np(runs[0]["au"][rt])
-    g = O.ffn_dgrad(dy[r].astype(np.float64), au[:, :F], au[:, F:], sub, sw, gu, dn)
+    check_close("A", to_np(runs[0]["au"][rt][:, :F]), f["A"])
+    check_close("U", to_np(runs[0]["au"][rt][:, F:]), f["U"])
+    g = O.ffn_dgrad(dy[r].astype(np.float64), au_in[r, :F], au_in[r, F:], sub, sw, gu, dn)
     check_close("dA", to_np(runs[0]["d_au"][rt][:, :F]), g["dA"])
     check_close("dU", to_np(runs[0]["d_au"][rt][:, F:]), g["dU"])
     check_close("dX", to_np(runs[0]["dx"][rt]), g["dX"])
