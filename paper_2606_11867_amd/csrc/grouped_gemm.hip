@@ -846,8 +846,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   // Whole rounds of G tiles, one tile per workgroup per round. When the last
   // round is partial (r < G tiles) and a workspace is given, its tiles are
   // cut along K into `split` pieces each, so that r * split workgroups share
-  // it instead of r. Workgroups with consecutive virtual ids (one XCD) take
-  // the pieces of one tile.
+  // it instead of r. The pieces of one tile run on workgroups of one XCD.
   const int G = gridDim.x;
   const int v = xcd_virtual_id();
   const int r = total % G;
