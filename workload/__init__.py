@@ -10,6 +10,7 @@ from .bf16 import bf16_round, f32_to_bf16_bits, bf16_bits_to_f32
 from .synth import (
     ConfigSpec,
     CONFIGS,
+    CONFIG_IDS,
     Plan,
     MicroStep,
     Workload,
@@ -24,6 +25,7 @@ __all__ = [
     "bf16_bits_to_f32",
     "ConfigSpec",
     "CONFIGS",
+    "CONFIG_IDS",
     "Plan",
     "MicroStep",
     "Workload",

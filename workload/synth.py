@@ -80,6 +80,9 @@ CONFIGS: Dict[int, ConfigSpec] = {
                   micro_steps=16, backward=True, seed=1003),
 }
 
+# workload id by name
+CONFIG_IDS: Dict[str, int] = {spec.name: i for i, spec in CONFIGS.items()}
+
 
 @dataclass
 class Plan:
