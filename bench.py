@@ -110,10 +110,9 @@ def main() -> int:
     lib = _lib.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    wid = CONFIG_IDS["qwen3-30b-a3b-ep8-policy-update"]
-    spec = CONFIGS[wid]
+    spec = CONFIGS[CONFIG_IDS["qwen3-30b-a3b-ep8-policy-update"]]
     t0 = time.time()
-    w = make_workload(wid)
+    w = make_workload(spec)
     n_micro = min(args.micro_steps, len(w.micro))
     T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
     bf = torch.bfloat16

@@ -43,8 +43,8 @@ def rnd(w, a):
 
 
 @functools.lru_cache(maxsize=None)
-def config_workload(c: int):
-    return make_workload(c)
+def config_workload(name: str):
+    return make_workload(name)
 
 
 @functools.lru_cache(maxsize=None)

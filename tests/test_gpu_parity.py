@@ -16,11 +16,14 @@ from tests.gpu_helpers import (check_close, config_workload, custom_workload, gp
 pytestmark = pytest.mark.gpu
 
 SMALL = ["tinyf32", "small", "odd128", "share"]
+# the paper-shaped workloads, by short id
+NAMED = {"tiny": "tiny-fp32", "mixtral": "mixtral-8x7b-share", "qwen3": "qwen3-30b-a3b-ep8-share",
+         "dsv3": "deepseek-v3-ep32-share"}
 
 
 def _wl(name):
-    if name.startswith("cfg"):
-        return config_workload(int(name[3:]))
+    if name in NAMED:
+        return config_workload(NAMED[name])
     return custom_workload(name)
 
 
@@ -37,7 +40,7 @@ def _print_case(name, w, m):
 # Steps 1-3: bit-exact dispatch
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("fused", [True, False], ids=["histogram_assign", "separate"])
-@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg2", "cfg3", "cfg4"])
+@pytest.mark.parametrize("name", SMALL + ["tiny", "mixtral", "qwen3", "dsv3"])
 def test_dispatch_bit_exact(gpu, name, fused):
     w = _wl(name)
     m = _ms(w)
@@ -188,7 +191,7 @@ def _check_ws_reset(ws):
 
 
 @pytest.mark.parametrize("split", [False, True])
-@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
+@pytest.mark.parametrize("name", SMALL + ["tiny", "qwen3"])
 def test_ffn_forward(gpu, name, split):
     from paper_2606_11867_amd import api
     w = _wl(name)
@@ -225,7 +228,7 @@ def _sampled_rows(ref, m, rng, per_slot=6):
     return np.array(rows), np.array(sub_off), np.array(widx)
 
 
-@pytest.mark.parametrize("name", ["cfg2", "cfg4"])
+@pytest.mark.parametrize("name", ["mixtral", "dsv3"])
 def test_ffn_forward_sampled_rows_full_size(gpu, name):
     """Full-size forward; the oracle recomputes sampled rows of every slot."""
     from paper_2606_11867_amd import api
@@ -248,7 +251,7 @@ def test_ffn_forward_sampled_rows_full_size(gpu, name):
     check_close("Y", to_np(y[torch.from_numpy(rows).to(gpu)]), f["Y"])
 
 
-@pytest.mark.parametrize("name", ["cfg2", "cfg4"])
+@pytest.mark.parametrize("name", ["mixtral", "dsv3"])
 def test_ffn_backward_sampled_full_size(gpu, name):
     """Full-size input and weight gradients (the row-GEMM and weight-gradient
     workspaces as the benchmark uses them) from seeded inputs: the oracle
@@ -295,7 +298,7 @@ def test_ffn_backward_sampled_full_size(gpu, name):
 
 
 @pytest.mark.parametrize("split", [False, True])
-@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
+@pytest.mark.parametrize("name", SMALL + ["tiny", "qwen3"])
 def test_ffn_backward(gpu, name, split):
     from paper_2606_11867_amd import api
     w = _wl(name)
@@ -350,7 +353,7 @@ def test_ffn_backward(gpu, name, split):
 # ---------------------------------------------------------------------------
 # Step 5 and the backward gathers
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3", "cfg4"])
+@pytest.mark.parametrize("name", SMALL + ["tiny", "qwen3", "dsv3"])
 def test_gathers(gpu, name):
     from paper_2606_11867_amd import api
     w = _wl(name)
@@ -412,7 +415,7 @@ def run_gpu_layer(w, m, gpu, dy, dw_gate_up=None, dw_down=None):
     return dict(y=y, dgates=dg, dx=dx, dw_gate_up=dw_gate_up, dw_down=dw_down)
 
 
-@pytest.mark.parametrize("name", SMALL + ["cfg1", "cfg3"])
+@pytest.mark.parametrize("name", SMALL + ["tiny", "qwen3"])
 def test_layer_chain(gpu, name):
     w = _wl(name)
     m = _ms(w)
@@ -543,7 +546,7 @@ def _backward_schedules(w, gpu, n_micro):
     return res
 
 
-@pytest.mark.parametrize("name,n_micro", [("share", 4), ("cfg3", 3)])
+@pytest.mark.parametrize("name,n_micro", [("share", 4), ("qwen3", 3)])
 def test_backward_schedules_match_one_stream(gpu, name, n_micro):
     w = _wl(name)
     _print_case(name, w, w.micro[0])

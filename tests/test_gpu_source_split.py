@@ -84,7 +84,7 @@ def run_both(ids, plan, x, n_cap, dtype, gpu, fused=False):
 
 def test_planned_share_bit_exact_and_ffn(gpu):
     from paper_2606_11867_amd import api
-    w = config_workload(3)
+    w = config_workload("qwen3-30b-a3b-ep8-share")
     m = w.micro[w.measured]
     plan, mp = planned_share(w, m, rank=w.rank)
     T, K = m.ids.shape

@@ -53,7 +53,7 @@ def test_histogram_brute_force():
 
 
 def test_histogram_sum_equals_pairs():
-    w = make_workload(1)
+    w = make_workload("tiny-fp32")
     m = w.micro[0]
     ids = m.ids.copy()
     ids[::7, 1] = -1
@@ -101,7 +101,7 @@ def test_replica_bounds_cover_and_balance():
 
 
 def test_assign_offsets_are_prefix_sums():
-    w = make_workload(1)
+    w = make_workload("tiny-fp32")
     m = w.micro[0]
     counts, _ = O.histogram(m.ids, w.spec.E)
     rep_begin, slot_count, slot_offset = O.assign_replicas(counts, m.plan)
@@ -188,8 +188,8 @@ def test_permute_brute_force():
     assert check_permute_brute_force()
 
 
-def test_permute_invariants_cfg1():
-    w = make_workload(1)
+def test_permute_invariants_tiny():
+    w = make_workload("tiny-fp32")
     m = w.micro[0]
     T, K = m.ids.shape
     x = w.x(0)
@@ -278,8 +278,8 @@ def test_dense_reference():
     assert check_dense_reference() <= 1e-12
 
 
-def test_dense_reference_cfg1():
-    w = make_workload(1)
+def test_dense_reference_tiny():
+    w = make_workload("tiny-fp32")
     m = w.micro[0]
     gu, dn = w.weights(m.plan)
     x = w.x(0)

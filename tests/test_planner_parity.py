@@ -70,7 +70,7 @@ def source_loads(w, m):
 def test_policy_update_workload(api):
     # the Qwen3 EP=8 share: one machine of 8 ranks, 16 base + 4 redundant
     # slots per rank; every micro-step planned by both and compared
-    w = make_workload(5)
+    w = make_workload("qwen3-30b-a3b-ep8-policy-update")
     P, E = w.spec.P, w.spec.E
     loads = [source_loads(w, m) for m in w.micro]
     agg = np.sum(loads, axis=0)

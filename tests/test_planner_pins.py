@@ -183,7 +183,7 @@ def test_policy_update_lowers_imbalance_on_generated_routing():
     # balanced than the base placement's in the median (the paper reports
     # the same direction, Sec. 10.4)
     from workload import make_workload
-    w = make_workload(5)
+    w = make_workload("qwen3-30b-a3b-ep8-policy-update")
     P, E, T = w.spec.P, w.spec.E, w.spec.T
     loads = []
     for m in w.micro[:6]:

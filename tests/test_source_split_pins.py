@@ -47,7 +47,7 @@ def test_hand_worked():
 
 
 def test_single_source_reduces_to_the_plain_split():
-    w = make_workload(1)
+    w = make_workload("tiny-fp32")
     m = w.micro[0]
     T, K = m.ids.shape
     tb = [0, T]

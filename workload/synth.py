@@ -56,7 +56,7 @@ class ConfigSpec:
     permute_popularity: bool
     P: int              # EP ranks the base placement is planned over
     n_rep: int          # redundant slots on the measured rank (paper: N_r)
-    micro_steps: int    # micro-steps generated (for planning and cfg5)
+    micro_steps: int    # micro-steps generated (for planning and the policy update)
     backward: bool
     seed: int
 
@@ -291,7 +291,10 @@ def _share_plan(spec: ConfigSpec, hosted: np.ndarray, load: np.ndarray) -> Plan:
 
 
 def make_workload(spec_or_id, micro_steps: Optional[int] = None) -> Workload:
-    """Generate the routing, plans and lazily-drawn values of a config."""
+    """Generate the routing, plans and lazily-drawn values of a workload, given
+    by its spec, its name or its id in the table."""
+    if isinstance(spec_or_id, str):
+        spec_or_id = CONFIG_IDS[spec_or_id]
     spec = CONFIGS[spec_or_id] if isinstance(spec_or_id, int) else spec_or_id
     n_micro = spec.micro_steps if micro_steps is None else micro_steps
     z = _popularity(spec)
