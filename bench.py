@@ -480,7 +480,12 @@ def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> d
     L_max / L_mean over the 8 ranks (natural placement e -> e / (E/P), Stage 1
     base placement, after Stages 2-4; medians over the micro-steps, the
     metric of Sec. 10.4), the planned share's local pairs, and the GPU time of
-    histogram_src + assign_replicas + permute for it.
+    histogram_src + assign_replicas + permute for it. Then the whole layer
+    (dispatch, expert FFN forward and backward, combine and the backward
+    gathers, one stream) on the share of each micro-step's slowest rank,
+    under the natural placement and under the plan: all ranks wait for the
+    slowest one (Sec. 7.1, Eq. 1), so these are the layer times per
+    micro-step that the two placements give on this GPU.
     """
     import numpy as np
     import torch
@@ -502,20 +507,34 @@ def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> d
     natural = np.arange(E) // (E // P)
     imb = {"natural": [], "base": [], "planned": []}
     plans, host_s = [], 0.0
+
+    def share_plan(copy_rank, counts, rank):
+        sl = api.plan_rank_slots(copy_rank, rank)
+        return Plan(E=E, R_max=C_max, slot_expert=sl["slot_expert"], slot_replica=sl["slot_replica"],
+                    expert_nrep=sl["expert_nrep"], expert_rep_weight=None, slot_widx=sl["slot_widx"],
+                    slot_gidx=sl["slot_widx"].copy(), local_experts=sl["local_experts"],
+                    src_token_begin=tb, src_rep_weight=counts)
+
+    # the natural placement as a plan: one copy per expert, on rank e / (E/P)
+    nat_rank = np.full((E, C_max), -1, dtype=np.int32)
+    nat_rank[:, 0] = natural
+    slowest = {"natural": [], "planned": []}  # (plan, expected local pairs) per micro-step
     for i, W in enumerate(loads):
         t0 = time.perf_counter()
         copy_rank, counts, rank_load = api.plan_micro_step(W, base, 1, P, E // P, N_r, C_max)
-        sl = api.plan_rank_slots(copy_rank, w.rank)
+        plans.append(share_plan(copy_rank, counts, w.rank))
         host_s += time.perf_counter() - t0
         we = W.sum(axis=0)
         for name, pl in (("natural", natural), ("base", base)):
             L = np.bincount(pl, weights=we, minlength=P)
             imb[name].append(float(L.max() / L.mean()))
         imb["planned"].append(float(rank_load.max() / rank_load.mean()))
-        plans.append(Plan(E=E, R_max=C_max, slot_expert=sl["slot_expert"], slot_replica=sl["slot_replica"],
-                          expert_nrep=sl["expert_nrep"], expert_rep_weight=None, slot_widx=sl["slot_widx"],
-                          slot_gidx=sl["slot_widx"].copy(), local_experts=sl["local_experts"],
-                          src_token_begin=tb, src_rep_weight=counts))
+        L_nat = np.bincount(natural, weights=we, minlength=P).astype(np.int64)
+        nat_counts = np.zeros((P, E, C_max), dtype=np.int32)
+        nat_counts[:, :, 0] = W
+        p_nat, p_pl = int(np.argmax(L_nat)), int(np.argmax(rank_load))
+        slowest["natural"].append((share_plan(nat_rank, nat_counts, p_nat), int(L_nat[p_nat])))
+        slowest["planned"].append((share_plan(copy_rank, counts, p_pl), int(rank_load[p_pl])))
     # GPU: per-source dispatch of the measured rank's planned share
     bf = torch.bfloat16
     d = spec.d
@@ -555,6 +574,48 @@ def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> d
     e1.record()
     torch.cuda.synchronize()
     dispatch_us = e0.elapsed_time(e1) * 1e3 / (rounds * len(ms))
+
+    # the whole layer on the slowest rank's share, natural vs planned
+    F = spec.F
+    gen = torch.Generator(device=dev).manual_seed(11)
+    W_max = max(pl.W for v in slowest.values() for pl, _ in v)
+    gu = (torch.randn((W_max, 2 * F, d), generator=gen, device=dev) / d ** 0.5).to(bf)
+    dn = (torch.randn((W_max, d, F), generator=gen, device=dev) / F ** 0.5).to(bf)
+    dwgu = torch.zeros((W_max, 2 * F, d), dtype=torch.float32, device=dev)
+    dwdn = torch.zeros((W_max, d, F), dtype=torch.float32, device=dev)
+    dy = torch.randn((T, d), generator=gen, device=dev).to(bf)
+    rws, wws = api.ffn_workspace(dev), api.wgrad_workspace(d, F, dev)
+    gates = [torch.from_numpy(w.micro[i].gates).to(dev) for i in range(len(ms))]
+
+    def layer(m, g):
+        so = dispatch(m)
+        h, y_perm, au = api.grouped_ffn_fwd(x_perm, so, m["plan"].slot_widx, gu, dn, ws=rws)
+        api.combine(y_perm, p2r, g, out_dtype=bf)
+        dy_perm, _ = api.combine_bwd(dy, y_perm, p2r, g)
+        d_au, dx_perm = api.grouped_ffn_dgrad(dy_perm, au, so, m["plan"].slot_widx, gu, dn, ws=rws)
+        api.grouped_ffn_wgrad(x_perm, h, dy_perm, d_au, so, m["plan"].slot_gidx, dwgu, dwdn, ws=wws)
+        api.permute_bwd(dx_perm, p2r, T, K, out_dtype=bf)
+        return so
+
+    layer_us, pairs = {}, {}
+    for name, v in slowest.items():
+        mm = []
+        for i, (pl, n_exp) in enumerate(v):
+            dp = api.DevicePlan.from_host(pl, dev)
+            m = dict(ms[i], plan=dp, cplan=dp.c_struct())
+            got = int(layer(m, gates[i])[-1].item())  # warm-up pass, checked against the planner
+            if got != n_exp:
+                raise RuntimeError(f"{name} share of micro-step {i}: {got} local pairs, planner says {n_exp}")
+            mm.append(m)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(2):
+            for i, m in enumerate(mm):
+                layer(m, gates[i])
+        e1.record()
+        torch.cuda.synchronize()
+        layer_us[name] = round(e0.elapsed_time(e1) * 1e3 / (2 * len(mm)), 1)
+        pairs[name] = round(float(np.mean([n for _, n in v])), 1)
     med = {k: round(float(np.median(v)), 3) for k, v in imb.items()}
     return {"plan_us_per_micro_step": round(host_s / len(loads) * 1e6, 1),
             "imbalance_median": med,
@@ -562,7 +623,11 @@ def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> d
             "planned_share": {"rank": int(w.rank), "n_pairs_mean": round(float(np.mean(Ns)), 1),
                               "n_pairs_max": int(max(Ns)), "n_pairs_min": int(min(Ns)),
                               "dispatch_us_per_micro_step": round(dispatch_us, 2),
-                              "note": "histogram_src + assign_replicas + permute, (source, expert) keys"}}
+                              "note": "histogram_src + assign_replicas + permute, (source, expert) keys"},
+            "slowest_rank_layer": {"us_per_micro_step": layer_us, "n_pairs_mean": pairs,
+                                   "speedup": round(layer_us["natural"] / layer_us["planned"], 3),
+                                   "note": "dispatch + expert FFN fwd/dgrad/wgrad + combine + backward "
+                                           "gathers, one stream, on the slowest rank's share"}}
 
 
 def measured_traffic(phase: str):
