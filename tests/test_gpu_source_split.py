@@ -111,6 +111,48 @@ def test_planned_share_bit_exact_and_ffn(gpu):
     check_close("y_perm (sampled rows)", to_np(y_perm)[rows], ref)
 
 
+def natural_share(w, m, rank, C_max=8):
+    """Rank `rank`'s slot table for micro-step m under the natural placement
+    (expert e on rank e / (E/P), one copy each), written as a per-source
+    plan: copy 0 of every expert takes all of its source's pairs."""
+    P, E, T = w.spec.P, w.spec.E, w.spec.T
+    tb = np.arange(P + 1, dtype=np.int32) * (T // P)
+    local = np.arange(rank * (E // P), (rank + 1) * (E // P), dtype=np.int32)
+    wts = np.zeros((P, E, C_max), dtype=np.int32)
+    wts[:, :, 0] = source_loads(m.ids, E, tb)
+    widx = np.arange(len(local), dtype=np.int32)
+    return Plan(E=E, R_max=C_max, slot_expert=local, slot_replica=np.zeros(len(local), np.int32),
+                expert_nrep=np.ones(E, np.int32), expert_rep_weight=None, slot_widx=widx, slot_gidx=widx.copy(),
+                local_experts=local, src_token_begin=tb, src_rep_weight=wts)
+
+
+@pytest.mark.parametrize("placement", ["natural", "planned"])
+def test_slowest_rank_share_bit_exact(gpu, placement):
+    """The share of the micro-step's most loaded rank (the one every rank
+    waits for, Sec. 7.1 Eq. 1) under either placement: bit-exact dispatch,
+    and its local pairs equal to that rank's load."""
+    w = config_workload("qwen3-30b-a3b-ep8-share")
+    m = w.micro[w.measured]
+    P, E, T = w.spec.P, w.spec.E, w.spec.T
+    T_, K = m.ids.shape
+    if placement == "natural":
+        v = m.ids.reshape(-1)
+        L = np.bincount(np.arange(E) // (E // P), weights=np.bincount(v[v >= 0], minlength=E), minlength=P)
+        rank = int(np.argmax(L))
+        plan, load = natural_share(w, m, rank), int(L[rank])
+    else:
+        tb = np.arange(P + 1, dtype=np.int64) * (T // P)
+        loads = [source_loads(mm.ids, E, tb) for mm in w.micro]
+        base = PL.base_placement(np.sum(loads, axis=0), 1, P, E // P)
+        RL = PL.policy_update_plan(loads[m.index], base, 1, P, E // P, 4, C_max=8).rank_load()
+        rank = int(np.argmax(RL))
+        plan, _ = planned_share(w, m, rank=rank)
+        load = int(RL[rank])
+    print(f"{placement} placement: slowest rank {rank}, load {load}, S={plan.S}", flush=True)
+    got = run_both(m.ids, plan, w.x(m.index), T_ * K, tdtype(w), gpu, fused=True)
+    assert int(got["ref"]["so"][-1]) == load
+
+
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_random_sources_bit_exact(gpu, seed):
     rng = np.random.default_rng(seed)
