@@ -104,15 +104,15 @@ def main() -> int:
     import torch
 
     from paper_2606_11867_amd import _lib, api
-    from workload import CONFIG_IDS, CONFIGS, make_workload
+    from workload import make_workload
     from workload import accounting as acc
 
     lib = _lib.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    spec = CONFIGS[CONFIG_IDS["qwen3-30b-a3b-ep8-policy-update"]]
     t0 = time.time()
-    w = make_workload(spec)
+    w = make_workload("qwen3-30b-a3b-ep8-policy-update")
+    spec = w.spec
     n_micro = min(args.micro_steps, len(w.micro))
     T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
     bf = torch.bfloat16
