@@ -163,3 +163,15 @@ def test_empty_calls_launch_nothing(lib):
     # zero slots: the FFN returns before any launch
     assert lib.foremoe_grouped_ffn_fwd(None, 1, 128, 128, 0, FAKE, None, 1, None, None, 0, None, None, None,
                                        None, 0, None) == 0
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark measures one GPU's share; asking for several GPUs ends
+    with status 2 and a message, before anything touches a GPU."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], cwd=root,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and not r.stdout.strip()
