@@ -49,6 +49,21 @@ def test_worked_water_filling_case(api):
     compare(api, [[60, 10], [40, 0]], M=1, R=2, N_b=1, N_r=1)
 
 
+def test_worked_stage_cases(api):
+    # the hand-worked Stage 2, Stage 3-4 and machine-confinement cases of the
+    # planner pins, through the C++ planner
+    for w, M, R, N_b, N_r, base in (
+            ([[10, 9, 1, 1], [0, 0, 0, 0]], 1, 2, 2, 0, [0, 0, 1, 1]),
+            ([[100, 90, 70, 10], [0] * 4, [0] * 4, [0] * 4], 1, 4, 1, 1, [0, 1, 2, 3]),
+            ([[500, 10, 0, 0], [0] * 4, [0] * 4, [0] * 4], 2, 2, 1, 1, [0, 1, 2, 3])):
+        w = np.asarray(w, dtype=np.int64)
+        mp = PL.policy_update_plan(w, np.asarray(base), M, R, N_b, N_r)
+        cr_o, cnt_o = oracle_arrays(mp, 8)
+        cr_g, cnt_g, load_g = api.plan_micro_step(w, np.asarray(base), M, R, N_b, N_r, 8)
+        assert np.array_equal(cr_g, cr_o) and np.array_equal(cnt_g, cnt_o)
+        assert load_g.tolist() == mp.rank_load().tolist()
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_random_machines(api, seed):
     rng = np.random.default_rng(seed)

@@ -201,6 +201,88 @@ def test_policy_update_lowers_imbalance_on_generated_routing():
 
 
 # ---------------------------------------------------------------------------
+# Hand-worked cases that tell the App. D rules apart
+# ---------------------------------------------------------------------------
+def check_stage2_relocation():
+    # One machine of two ranks with two base slots each; all tokens come
+    # from source 0. The base placement (from the aggregate) put e0, e1 on r0
+    # and e2, e3 on r1, but this micro-step's loads are 10, 9, 1, 1.
+    # Stage 2 (LPT on the micro-step load): e0 (10) -> r0 (0/0, lower id);
+    # e1 (9) -> r1 (0 < 10); e2 (1) -> r1 (9 < 10); e3 (1) -> tie 10/10 ->
+    # r0. Main ranks [0, 1, 1, 0], loads 11 / 10 (the base gives 19 / 2).
+    w = np.array([[10, 9, 1, 1], [0, 0, 0, 0]])
+    mp = PL.policy_update_plan(w, np.array([0, 0, 1, 1]), M=1, R=2, N_b=2, N_r=0)
+    return mp.main.tolist() == [0, 1, 1, 0] and mp.rank_load().tolist() == [11, 10]
+
+
+STAGE34_W = np.array([[100, 90, 70, 10], [0, 0, 0, 0], [0, 0, 0, 0], [0, 0, 0, 0]])
+
+
+def check_stage3_replication():
+    # One machine of four ranks, one base and one redundant slot each; loads
+    # 100, 90, 70, 10 (source 0). Stage 2 keeps e_i on r_i. Stage 3, four
+    # rounds (RL = current rank loads, copies sharing their expert's load):
+    #  1. load per copy 100, 90, 70, 10 -> e0. RL 100/90/70/10; ranks with
+    #     a free redundant slot and no e0: r1, r2, r3 -> least r3 (10).
+    #  2. per copy 50, 90, 70, 10 -> e1 (total load would pick e0 again).
+    #     RL r0 = 50, r1 = 90, r2 = 70, r3 = 10 + 50 = 60; free and no e1:
+    #     r0, r2 -> r0 (50; a main rank still holding e0's whole 100 would
+    #     lose to r2).
+    #  3. per copy 50, 45, 70, 10 -> e2. RL 95/45/70/60; free and no e2: r1.
+    #  4. per copy 50, 45, 35, 10 -> e0. RL 95/80/35/60; free and no e0: r2.
+    # Copies: e0 [r0, r3, r2], e1 [r1, r0], e2 [r2, r1], e3 [r3].
+    mp = PL.policy_update_plan(STAGE34_W, np.arange(4), M=1, R=4, N_b=1, N_r=1)
+    return mp.copies == [[0, 3, 2], [1, 0], [2, 1], [3]]
+
+
+def check_stage4_two_replicated():
+    # Stage 4 on the placement above. Start: r3 holds e3 (10), the rest 0.
+    #  e0 (100, the heaviest) over copies r0/r3/r2 at 0/10/0: 20 units
+    #     bring r0 and r2 to 10, then the three take turns from copy 0:
+    #     80 = 26 rounds + 2 -> counts 37, 27, 36; loads r0 37, r3 37, r2 36.
+    #  e1 (90) over r1/r0 at 0/37: 37 units to r1, then 53 in turns from
+    #     copy 0 -> 27 / 26: counts 64, 26; loads r1 64, r0 63.
+    #  e2 (70) over r2/r1 at 36/64: 28 units to r2, then 42 in turns ->
+    #     21 / 21: counts 49, 21; loads r2 85, r1 85.
+    # Rank loads 63 / 85 / 85 / 37. (Filling e2 before e1, ascending, would
+    # split e2 35 / 35 over two empty ranks.)
+    mp = PL.policy_update_plan(STAGE34_W, np.arange(4), M=1, R=4, N_b=1, N_r=1)
+    c = mp.counts[0]
+    return (c[0, :3].tolist() == [37, 27, 36] and c[1, :2].tolist() == [64, 26]
+            and c[2, :2].tolist() == [49, 21] and c[3, 0] == 10
+            and mp.rank_load().tolist() == [63, 85, 85, 37])
+
+
+def test_stage2_relocation_worked_example():
+    assert check_stage2_relocation()
+
+
+def test_stage3_replication_worked_example():
+    assert check_stage3_replication()
+
+
+def test_stage4_two_replicated_experts_worked_example():
+    assert check_stage4_two_replicated()
+
+
+def test_stage3_machine_confinement():
+    # Two machines of two ranks, one base and one redundant slot per rank
+    # (App. D: replicas stay inside their machine). Machine 0 holds e0 (500)
+    # and e1 (10): round 1 puts a replica of e0 on r1; round 2 picks e0
+    # again (250 per copy > 10) but r0 holds it and r1's slot is used, so
+    # the machine stops, although machine 1's ranks carry no load at all.
+    # Machine 1 holds e2, e3 with no load: round 1 takes e2 (equal loads per
+    # copy, lower id) onto r3; round 2 takes e2 again (0/2 = 0/1, lower id),
+    # which no rank can take.
+    w = np.array([[500, 10, 0, 0], [0, 0, 0, 0], [0, 0, 0, 0], [0, 0, 0, 0]])
+    mp = PL.policy_update_plan(w, np.array([0, 1, 2, 3]), M=2, R=2, N_b=1, N_r=1)
+    assert mp.copies == [[0, 1], [1], [2, 3], [3]]
+    # Stage 4: r1 starts at 10 (e1), so e0's first 10 units go to r0, then
+    # the other 490 alternate from copy 0: 255 / 245
+    assert mp.counts[0, 0, :2].tolist() == [255, 245]
+
+
+# ---------------------------------------------------------------------------
 # Mutation tests
 # ---------------------------------------------------------------------------
 def test_mutation_ascending_lpt_is_caught(monkeypatch):
@@ -237,3 +319,42 @@ def test_mutation_split_ignores_base_load_is_caught(monkeypatch):
 
     monkeypatch.setattr(PL, "policy_update_plan", wrong)
     assert not check_water_filling_worked_example()
+
+
+def test_mutation_stage2_deleted_is_caught(monkeypatch):
+    # Stage 2 skipped: the base placement stays
+    monkeypatch.setattr(PL, "stage2_relocate", lambda we, local, ranks, N_b: {})
+    assert not check_stage2_relocation()
+
+
+def test_mutation_stage3_most_loaded_rank_is_caught(monkeypatch):
+    monkeypatch.setattr(PL, "stage3_rank",
+                        lambda RL, cands: max(sorted(cands), key=lambda r: (RL[r], -r)) if cands else None)
+    assert not check_stage3_replication()
+
+
+def test_mutation_stage3_total_load_is_caught(monkeypatch):
+    # heaviest by total load instead of load per copy
+    monkeypatch.setattr(PL, "heaviest_expert",
+                        lambda we, local, copies: max(sorted(local), key=lambda e: (int(we[e]), -e)) if local else None)
+    assert not check_stage3_replication()
+
+
+@pytest.mark.parametrize("kind", ["main_keeps_all", "every_copy_full"])
+def test_mutation_stage3_unshared_load_is_caught(monkeypatch, kind):
+    # rank loads that ignore how the copies of an expert share its load
+    def wrong(we, local, copies, ranks):
+        RL = {r: 0 for r in ranks}
+        for e in local:
+            for i, r in enumerate(copies[e]):
+                if kind == "every_copy_full" or i == 0:
+                    RL[r] += int(we[e])
+        return RL
+
+    monkeypatch.setattr(PL, "copy_loads", wrong)
+    assert not check_stage3_replication()
+
+
+def test_mutation_stage4_ascending_order_is_caught(monkeypatch):
+    monkeypatch.setattr(PL, "stage4_order", lambda we, reps: sorted(reps, key=lambda e: (int(we[e]), e)))
+    assert not check_stage4_two_replicated()
