@@ -192,16 +192,18 @@ def main() -> int:
         def call(phase, st, rc_fn):
             def run():
                 timed = ev is not None and phase in ev
-                # row GEMMs carry their events on the kernel dispatch itself
-                # (no event commands between the kernels); the other phases
-                # are bracketed by event records on their stream
-                on_launch = timed and phase in ROW_GEMMS
-                if on_launch:
-                    lib.foremoe_set_launch_events(ev[phase][0].cuda_event, ev[phase][1].cuda_event)
-                elif timed:
+                # row GEMMs (rc_fn takes the two events) carry their events on
+                # the kernel dispatch itself (no event commands between the
+                # kernels); the other phases are bracketed by event records
+                # on their stream
+                if phase in ROW_GEMMS:
+                    e = (ev[phase][0].cuda_event, ev[phase][1].cuda_event) if timed else (None, None)
+                    chk(rc_fn(st.cuda_stream, *e), phase)
+                    return
+                if timed:
                     ev[phase][0].record(st)
                 chk(rc_fn(st.cuda_stream), phase)
-                if timed and not on_launch:
+                if timed:
                     ev[phase][1].record(st)
             ops.append((phase, run))
 
@@ -223,10 +225,10 @@ def main() -> int:
         call("permute", main, lambda q: lib.foremoe_permute(
             ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
             P["r2p"], P["p2r"], P["ws"], wsz, q))
-        call("gate_up_fwd", main, lambda q: lib.foremoe_ffn_gate_up_fwd(
-            P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"], P["au"], rws, rwsz, q))
-        call("down_fwd", main, lambda q: lib.foremoe_ffn_down_fwd(
-            P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], rws, rwsz, q))
+        call("gate_up_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_fwd_timed(
+            P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"], P["au"], rws, rwsz, q, e0, e1))
+        call("down_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_down_fwd_timed(
+            P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], rws, rwsz, q, e0, e1))
         call("combine", main, lambda q: lib.foremoe_combine(
             P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap, P["y"], BF16, q))
         call("combine_bwd", main, lambda q: lib.foremoe_combine_bwd(
@@ -235,13 +237,14 @@ def main() -> int:
         if overlap:
             dep(side, main)
             down_wgrad(side)
-        call("down_dgrad", main, lambda q: lib.foremoe_ffn_down_dgrad(
-            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["d_au"], rws, rwsz, q))
+        call("down_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_down_dgrad_timed(
+            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["d_au"], rws, rwsz, q,
+            e0, e1))
         if overlap:
             dep(side, main)
             gate_up_wgrad(side)
-        call("gate_up_dgrad", main, lambda q: lib.foremoe_ffn_gate_up_dgrad(
-            P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["dx_perm"], rws, rwsz, q))
+        call("gate_up_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_dgrad_timed(
+            P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["dx_perm"], rws, rwsz, q, e0, e1))
         if not overlap:
             gate_up_wgrad(main)
             down_wgrad(main)

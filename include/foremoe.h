@@ -22,7 +22,9 @@
  * Conventions (all entry points):
  *  - Every pointer argument is a DEVICE pointer unless stated otherwise; the
  *    caller owns every buffer. The library never allocates device memory and
- *    keeps no state besides a per-thread error message.
+ *    keeps no state besides a per-thread error message and the cached
+ *    compute-unit count of each device; no call changes what a later call
+ *    does.
  *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
  *    stream) and never synchronises the host. Sizes that depend on the
  *    routing (N = local pairs, slot offsets) stay on the device.
@@ -123,9 +125,10 @@ typedef struct foremoe_plan {
 #define FOREMOE_WS_INVALID_IDS 0  /* ids outside [-1, E): skipped, written by histogram */
 #define FOREMOE_WS_DROPPED 1      /* local pairs beyond n_cap, written by permute       */
 #define FOREMOE_WS_PLAN_ERRORS 2  /* device-side plan errors, written by assign         */
-/* Word 63 is the arrival ticket of foremoe_histogram_assign: it must be zero
- * before that call is first made on a workspace (zero-fill the workspace once)
- * and every such call leaves it zero. */
+/* Word 63 is the arrival ticket of foremoe_histogram_assign; that call's
+ * first kernel zeroes it, so a workspace needs no initialisation and a stale
+ * ticket (a workspace not zero-filled, an earlier call that did not
+ * complete) cannot misfire. */
 size_t foremoe_workspace_size(int64_t T, int32_t K, int32_t E);
 
 /*
@@ -429,19 +432,37 @@ int foremoe_plan_rank_slots(const int32_t* copy_rank, int32_t E, int32_t C_max, 
                             int32_t* S_out, int32_t* W_out);
 
 /*
- * Kernel timing (a measurement hook, not an operation of the method).
- * start, stop: hipEvent_t handles owned by the caller, created beforehand
- * with timing enabled, or NULL. They are attached to the next bf16 row-GEMM
- * kernel this host thread launches (foremoe_ffn_gate_up_fwd,
- * foremoe_ffn_down_fwd, foremoe_ffn_down_dgrad, foremoe_ffn_gate_up_dgrad;
- * in foremoe_grouped_ffn_fwd and foremoe_grouped_ffn_dgrad the first of their
- * two launches) and then dropped: the events are set when that kernel
- * starts and when it ends, with no separate event command in the stream, so
- * hipEventElapsedTime(start, stop) is the kernel's own duration. A call that
- * fails before launching leaves them attached; NULL, NULL detaches them.
- * Always returns FOREMOE_OK.
+ * Timed forms of the four row-GEMM calls (a measurement aid, not an
+ * operation of the method): the same arguments, work and results as
+ * foremoe_ffn_gate_up_fwd, foremoe_ffn_down_fwd, foremoe_ffn_down_dgrad and
+ * foremoe_ffn_gate_up_dgrad, plus two hipEvent_t handles owned by the
+ * caller (created beforehand, timing enabled; either may be NULL). The
+ * events are attached to the call's one kernel launch: they are set when
+ * that kernel starts and when it ends, with no separate event command in
+ * the stream, so hipEventElapsedTime(start, stop) is the kernel's own
+ * duration. A call that launches nothing (S == 0 or n_cap == 0) records
+ * both events back to back; a call that fails before launching leaves them
+ * untouched. Nothing is kept after the call returns.
  */
-int foremoe_set_launch_events(void* start, void* stop);
+int foremoe_ffn_gate_up_fwd_timed(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
+                                  int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
+                                  int32_t W, const void* w_gate_up, int64_t n_cap, void* h,
+                                  void* save_au, void* workspace, size_t ws_bytes, void* stream,
+                                  void* start_event, void* stop_event);
+int foremoe_ffn_down_fwd_timed(const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                               const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
+                               const void* w_down, int64_t n_cap, void* y_perm, void* workspace,
+                               size_t ws_bytes, void* stream, void* start_event, void* stop_event);
+int foremoe_ffn_down_dgrad_timed(const void* dy_perm, const void* save_au, foremoe_dtype dtype,
+                                 int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
+                                 const int32_t* slot_widx, int32_t W, const void* w_down,
+                                 int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes,
+                                 void* stream, void* start_event, void* stop_event);
+int foremoe_ffn_gate_up_dgrad_timed(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F,
+                                    int32_t S, const int32_t* slot_offset, const int32_t* slot_widx,
+                                    int32_t W, const void* w_gate_up, int64_t n_cap, void* dx_perm,
+                                    void* workspace, size_t ws_bytes, void* stream,
+                                    void* start_event, void* stop_event);
 
 /* Utilities (host only, no GPU work). */
 const char* foremoe_status_string(int status);

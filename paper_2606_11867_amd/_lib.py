@@ -78,7 +78,14 @@ SIGNATURES = {
     "foremoe_plan_base": (ctypes.c_int, [c_p, c_i32, PMachine, c_i64, c_i64, c_p]),
     "foremoe_plan_micro_step": (ctypes.c_int, [c_p, c_i32, PMachine, c_p, c_i32, c_p, c_p, c_p]),
     "foremoe_plan_rank_slots": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p, c_p, c_p, c_p]),
-    "foremoe_set_launch_events": (ctypes.c_int, [c_p, c_p]),
+    "foremoe_ffn_gate_up_fwd_timed": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
+                                                     c_i64, c_p, c_p, c_p, c_sz, c_p, c_p, c_p]),
+    "foremoe_ffn_down_fwd_timed": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_i64,
+                                                  c_p, c_p, c_sz, c_p, c_p, c_p]),
+    "foremoe_ffn_down_dgrad_timed": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
+                                                    c_i64, c_p, c_p, c_sz, c_p, c_p, c_p]),
+    "foremoe_ffn_gate_up_dgrad_timed": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p,
+                                                       c_i64, c_p, c_p, c_sz, c_p, c_p, c_p]),
     "foremoe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "foremoe_last_error": (ctypes.c_char_p, []),
     "foremoe_version": (ctypes.c_char_p, []),

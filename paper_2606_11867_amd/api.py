@@ -95,8 +95,7 @@ def workspace(T: int, K: int, E: int, device) -> torch.Tensor:
     n = _lib.load().foremoe_workspace_size(T, K, E)
     if n == 0:
         raise ValueError("invalid workspace sizes")
-    # zero-filled: foremoe_histogram_assign's arrival ticket (a header word)
-    # must start at zero; every call leaves it zero again
+    # zero-filled so that the status words read 0 before the first call
     return torch.zeros(n, dtype=torch.uint8, device=device)
 
 

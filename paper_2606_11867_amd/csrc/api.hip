@@ -23,14 +23,6 @@ int check_launch(const char* what) {
   return FOREMOE_OK;
 }
 
-static thread_local hipEvent_t g_launch_start = nullptr, g_launch_stop = nullptr;
-
-void take_launch_events(hipEvent_t* start, hipEvent_t* stop) {
-  *start = g_launch_start;
-  *stop = g_launch_stop;
-  g_launch_start = g_launch_stop = nullptr;
-}
-
 int num_cus() {
   // Cached per device: compute units of the current device.
   static thread_local int cached_dev = -1;
@@ -62,12 +54,6 @@ const char* foremoe_status_string(int status) {
 }
 
 const char* foremoe_last_error(void) { return foremoe::g_last_error; }
-
-int foremoe_set_launch_events(void* start, void* stop) {
-  foremoe::g_launch_start = (hipEvent_t)start;
-  foremoe::g_launch_stop = (hipEvent_t)stop;
-  return FOREMOE_OK;
-}
 
 const char* foremoe_version(void) { return "foremoe-mi355x 0.1 (gfx950)"; }
 

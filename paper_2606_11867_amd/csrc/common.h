@@ -81,7 +81,4 @@ namespace foremoe {
 int set_error(int status, const char* fmt, ...);
 int check_launch(const char* what);
 int num_cus();
-// Events attached by foremoe_set_launch_events for the next row-GEMM
-// launch of this thread; returns them and detaches them.
-void take_launch_events(hipEvent_t* start, hipEvent_t* stop);
 }  // namespace foremoe

@@ -69,12 +69,16 @@ __device__ __forceinline__ int pair_key(int v, int64_t p, const KeyMap& km, cons
 // ---------------------------------------------------------------------------
 // Step 1a: per-block counts of each key (bucket nkeys counts invalid ids).
 // ---------------------------------------------------------------------------
+// ticket (may be NULL): the arrival ticket of the scan+split kernel that
+// follows on the same stream; workgroup 0 zeroes it, so that kernel always
+// starts from a zero ticket whatever the workspace held before.
 __global__ __launch_bounds__(kHistThreads) void hist_count_kernel(const int32_t* __restrict__ ids, int64_t npairs,
                                                                   KeyMap km, int E, int nbits,
-                                                                  int32_t* __restrict__ partial) {
+                                                                  int32_t* __restrict__ partial, uint32_t* ticket) {
   __shared__ int s_cnt[FOREMOE_MAX_EXPERTS + 1];
   __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
   const int tid = threadIdx.x;
+  if (ticket && blockIdx.x == 0 && tid == 0) atomicExch(ticket, 0u);
   for (int e = tid; e <= E; e += kHistThreads) s_cnt[e] = 0;
   load_sources(km, s_tb);
   __syncthreads();
@@ -298,7 +302,8 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(const int32_t* _
 // caches are not coherent with each other: the totals are stored and loaded
 // with device scope (SC1 cache policy: written through, never read from a
 // stale line), and each workgroup drains its stores before it takes its
-// ticket. No workgroup waits for another.
+// ticket. No workgroup waits for another. The ticket is zero on entry: the
+// count kernel before it on the same stream has zeroed it.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kHistThreads) void hist_scan_assign_kernel(
     int32_t* __restrict__ partial, int64_t nblocks, int nkeys, int32_t* __restrict__ counts, uint32_t* ticket,
@@ -748,7 +753,7 @@ static int histogram_common(const char* who, const int32_t* ids, int64_t T, int3
   int32_t* status = (int32_t*)ws;
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
   hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, E,
-                     key_bits(E), partial);
+                     key_bits(E), partial, (uint32_t*)nullptr);
   hipLaunchKernelGGL(hist_scan_kernel, dim3(E + 1), dim3(kHistThreads), 0, st, partial, nb, E, counts, status);
   return check_launch(who);
 }
@@ -835,10 +840,11 @@ int foremoe_histogram_assign(const int32_t* ids, int64_t T, int32_t K, const for
   const int64_t nb = hist_blocks(npairs);
   int32_t* status = (int32_t*)ws;
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
+  uint32_t* ticket = (uint32_t*)(status + kWsTicketWord);
   hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, nkeys,
-                     key_bits(nkeys), partial);
+                     key_bits(nkeys), partial, ticket);
   hipLaunchKernelGGL(hist_scan_assign_kernel, dim3(nkeys + 1), dim3(kHistThreads), 0, st, partial, nb, nkeys, counts,
-                     (uint32_t*)(status + kWsTicketWord), P, rep_begin, slot_count, slot_offset,
+                     ticket, P, rep_begin, slot_count, slot_offset,
                      (int32_t*)((char*)ws + kWsVSlotOff), (int32_t*)((char*)ws + kWsRepSlotOff), status);
   return check_launch("foremoe_histogram_assign");
 }

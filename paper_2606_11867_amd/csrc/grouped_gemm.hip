@@ -1487,15 +1487,14 @@ size_t rows_workspace_bytes() { return kRowsCountBytes + (size_t)persistent_grid
 
 // Row-grouped launches: 256-row tiles; 256-wide output tiles with 2 LDS
 // stages of 64-deep K slices (128 KiB), or 128-wide with 3 stages (144 KiB).
+// e0, e1: optional timing events set when the kernel starts and ends (they
+// ride on the dispatch itself, so no event command sits in the stream).
 template <int BN, bool KMAJ, int EPI>
-void launch_rows(RowsArgs a, void* ws, hipStream_t st) {
+void launch_rows(RowsArgs a, void* ws, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   if (ws && persistent_grid() <= (int)(kRowsCountBytes / 4)) {
     a.sk_count = (unsigned*)ws;
     a.sk_part = (float*)((char*)ws + kRowsCountBytes);
   }
-  // events attached by foremoe_set_launch_events ride on the dispatch itself
-  hipEvent_t e0, e1;
-  take_launch_events(&e0, &e1);
   if constexpr (BN == 256) {
     constexpr int WGM = FM_ROWS_WGM, WGN = FM_ROWS_WGN;
     hipExtLaunchKernelGGL(gemm_rows_kernel<256, 256, FM_ROWS_BK, FM_ROWS_NS, WGM, WGN, KMAJ, EPI>,
@@ -1545,20 +1544,31 @@ static int check_rows_ws(const char* who, const void* workspace, size_t ws_bytes
   return FOREMOE_OK;
 }
 
+// A timed call that launches nothing still sets its events, back to back on
+// the stream, so that their elapsed time reads as zero.
+static int no_launch(hipEvent_t e0, hipEvent_t e1, void* stream) {
+  if (!e0 && !e1) return FOREMOE_OK;
+  if (e0 && hipEventRecord(e0, (hipStream_t)stream) != hipSuccess)
+    return set_error(FOREMOE_EHIP, "row GEMM: recording the start event failed");
+  if (e1 && hipEventRecord(e1, (hipStream_t)stream) != hipSuccess)
+    return set_error(FOREMOE_EHIP, "row GEMM: recording the stop event failed");
+  return FOREMOE_OK;
+}
+
 static dim3 f32_grid(int cols, int64_t rows) {
   return dim3((unsigned)((cols + 15) / 16), (unsigned)((rows + 15) / 16 > 0 ? (rows + 15) / 16 : 1));
 }
 
 extern "C" {
 
-int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+static int ffn_gate_up_fwd_impl(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                             const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
-                            int64_t n_cap, void* h, void* save_au, void* workspace, size_t ws_bytes, void* stream) {
+                            int64_t n_cap, void* h, void* save_au, void* workspace, size_t ws_bytes, void* stream, hipEvent_t e0, hipEvent_t e1) {
   int rc = check_ffn("gate_up_fwd", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
   rc = check_rows_ws("gate_up_fwd", workspace, ws_bytes);
   if (rc) return rc;
-  if (S == 0 || n_cap == 0) return FOREMOE_OK;
+  if (S == 0 || n_cap == 0) return no_launch(e0, e1, stream);
   REQUIRE(x_perm && slot_widx && w_gate_up && h && W >= 1, "gate_up_fwd: NULL buffer or W < 1");
   hipStream_t st = (hipStream_t)stream;
   if (dtype == FOREMOE_BF16) {
@@ -1580,23 +1590,23 @@ int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, 
     a.ldc = F;
     a.C2 = (uint16_t*)save_au;
     a.ldc2 = 2 * (int64_t)F;
-    launch_rows<256, true, kEpiSwigluFwd>(a, workspace, st);
+    launch_rows<256, true, kEpiSwigluFwd>(a, workspace, st, e0, e1);
   } else {
-    hipLaunchKernelGGL(f32_rows_kernel<kF32GateUpFwd>, f32_grid(F, n_cap), dim3(256), 0, st, (const float*)x_perm,
+    hipExtLaunchKernelGGL(f32_rows_kernel<kF32GateUpFwd>, f32_grid(F, n_cap), dim3(256), 0, st, e0, e1, 0, (const float*)x_perm,
                        (const float*)w_gate_up, nullptr, d, F, W, slot_offset, slot_widx, S, n_cap, (float*)h,
                        (float*)save_au);
   }
   return check_launch("foremoe_ffn_gate_up_fwd");
 }
 
-int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+static int ffn_down_fwd_impl(const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                          const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_down,
-                         int64_t n_cap, void* y_perm, void* workspace, size_t ws_bytes, void* stream) {
+                         int64_t n_cap, void* y_perm, void* workspace, size_t ws_bytes, void* stream, hipEvent_t e0, hipEvent_t e1) {
   int rc = check_ffn("down_fwd", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
   rc = check_rows_ws("down_fwd", workspace, ws_bytes);
   if (rc) return rc;
-  if (S == 0 || n_cap == 0) return FOREMOE_OK;
+  if (S == 0 || n_cap == 0) return no_launch(e0, e1, stream);
   REQUIRE(h && slot_widx && w_down && y_perm && W >= 1, "down_fwd: NULL buffer or W < 1");
   hipStream_t st = (hipStream_t)stream;
   if (dtype == FOREMOE_BF16) {
@@ -1616,10 +1626,10 @@ int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t 
     a.n_cap = n_cap;
     a.C = (uint16_t*)y_perm;
     a.ldc = d;
-    if (d % 256 == 0) launch_rows<256, true, kEpiStore>(a, workspace, st);
-    else launch_rows<128, true, kEpiStore>(a, workspace, st);
+    if (d % 256 == 0) launch_rows<256, true, kEpiStore>(a, workspace, st, e0, e1);
+    else launch_rows<128, true, kEpiStore>(a, workspace, st, e0, e1);
   } else {
-    hipLaunchKernelGGL(f32_rows_kernel<kF32DownFwd>, f32_grid(d, n_cap), dim3(256), 0, st, (const float*)h,
+    hipExtLaunchKernelGGL(f32_rows_kernel<kF32DownFwd>, f32_grid(d, n_cap), dim3(256), 0, st, e0, e1, 0, (const float*)h,
                        (const float*)w_down, nullptr, d, F, W, slot_offset, slot_widx, S, n_cap, (float*)y_perm,
                        nullptr);
   }
@@ -1636,14 +1646,14 @@ int foremoe_grouped_ffn_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, 
                               stream);
 }
 
-int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,
+static int ffn_down_dgrad_impl(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,
                            int32_t S, const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
-                           const void* w_down, int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes, void* stream) {
+                           const void* w_down, int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes, void* stream, hipEvent_t e0, hipEvent_t e1) {
   int rc = check_ffn("down_dgrad", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
   rc = check_rows_ws("down_dgrad", workspace, ws_bytes);
   if (rc) return rc;
-  if (S == 0 || n_cap == 0) return FOREMOE_OK;
+  if (S == 0 || n_cap == 0) return no_launch(e0, e1, stream);
   REQUIRE(dy_perm && save_au && slot_widx && w_down && d_au && W >= 1, "down_dgrad: NULL buffer or W < 1");
   hipStream_t st = (hipStream_t)stream;
   if (dtype == FOREMOE_BF16) {
@@ -1665,24 +1675,24 @@ int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dty
     a.ldc = 2 * (int64_t)F;
     a.AU = (const uint16_t*)save_au;
     a.ldau = 2 * (int64_t)F;
-    if (F % 256 == 0) launch_rows<256, false, kEpiSwigluBwd>(a, workspace, st);
-    else launch_rows<128, false, kEpiSwigluBwd>(a, workspace, st);
+    if (F % 256 == 0) launch_rows<256, false, kEpiSwigluBwd>(a, workspace, st, e0, e1);
+    else launch_rows<128, false, kEpiSwigluBwd>(a, workspace, st, e0, e1);
   } else {
-    hipLaunchKernelGGL(f32_rows_kernel<kF32DownDgrad>, f32_grid(F, n_cap), dim3(256), 0, st, (const float*)dy_perm,
+    hipExtLaunchKernelGGL(f32_rows_kernel<kF32DownDgrad>, f32_grid(F, n_cap), dim3(256), 0, st, e0, e1, 0, (const float*)dy_perm,
                        (const float*)w_down, (const float*)save_au, d, F, W, slot_offset, slot_widx, S, n_cap,
                        (float*)d_au, nullptr);
   }
   return check_launch("foremoe_ffn_down_dgrad");
 }
 
-int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+static int ffn_gate_up_dgrad_impl(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
                               const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
-                              int64_t n_cap, void* dx_perm, void* workspace, size_t ws_bytes, void* stream) {
+                              int64_t n_cap, void* dx_perm, void* workspace, size_t ws_bytes, void* stream, hipEvent_t e0, hipEvent_t e1) {
   int rc = check_ffn("gate_up_dgrad", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
   rc = check_rows_ws("gate_up_dgrad", workspace, ws_bytes);
   if (rc) return rc;
-  if (S == 0 || n_cap == 0) return FOREMOE_OK;
+  if (S == 0 || n_cap == 0) return no_launch(e0, e1, stream);
   REQUIRE(d_au && slot_widx && w_gate_up && dx_perm && W >= 1, "gate_up_dgrad: NULL buffer or W < 1");
   hipStream_t st = (hipStream_t)stream;
   if (dtype == FOREMOE_BF16) {
@@ -1702,14 +1712,75 @@ int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, 
     a.n_cap = n_cap;
     a.C = (uint16_t*)dx_perm;
     a.ldc = d;
-    if (d % 256 == 0) launch_rows<256, false, kEpiStore>(a, workspace, st);
-    else launch_rows<128, false, kEpiStore>(a, workspace, st);
+    if (d % 256 == 0) launch_rows<256, false, kEpiStore>(a, workspace, st, e0, e1);
+    else launch_rows<128, false, kEpiStore>(a, workspace, st, e0, e1);
   } else {
-    hipLaunchKernelGGL(f32_rows_kernel<kF32GateUpDgrad>, f32_grid(d, n_cap), dim3(256), 0, st, (const float*)d_au,
+    hipExtLaunchKernelGGL(f32_rows_kernel<kF32GateUpDgrad>, f32_grid(d, n_cap), dim3(256), 0, st, e0, e1, 0, (const float*)d_au,
                        (const float*)w_gate_up, nullptr, d, F, W, slot_offset, slot_widx, S, n_cap, (float*)dx_perm,
                        nullptr);
   }
   return check_launch("foremoe_ffn_gate_up_dgrad");
+}
+
+int foremoe_ffn_gate_up_fwd(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                            const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
+                            int64_t n_cap, void* h, void* save_au, void* workspace, size_t ws_bytes, void* stream) {
+  return ffn_gate_up_fwd_impl(x_perm, dtype, d, F, S, slot_offset, slot_widx, W, w_gate_up, n_cap, h, save_au,
+                              workspace, ws_bytes, stream, nullptr, nullptr);
+}
+
+int foremoe_ffn_gate_up_fwd_timed(const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                                  const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
+                                  const void* w_gate_up, int64_t n_cap, void* h, void* save_au, void* workspace,
+                                  size_t ws_bytes, void* stream, void* start_event, void* stop_event) {
+  return ffn_gate_up_fwd_impl(x_perm, dtype, d, F, S, slot_offset, slot_widx, W, w_gate_up, n_cap, h, save_au,
+                              workspace, ws_bytes, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+}
+
+int foremoe_ffn_down_fwd(const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                         const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_down,
+                         int64_t n_cap, void* y_perm, void* workspace, size_t ws_bytes, void* stream) {
+  return ffn_down_fwd_impl(h, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, y_perm, workspace, ws_bytes,
+                           stream, nullptr, nullptr);
+}
+
+int foremoe_ffn_down_fwd_timed(const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                               const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_down,
+                               int64_t n_cap, void* y_perm, void* workspace, size_t ws_bytes, void* stream,
+                               void* start_event, void* stop_event) {
+  return ffn_down_fwd_impl(h, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, y_perm, workspace, ws_bytes,
+                           stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+}
+
+int foremoe_ffn_down_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,
+                           int32_t S, const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
+                           const void* w_down, int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  return ffn_down_dgrad_impl(dy_perm, save_au, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, d_au,
+                             workspace, ws_bytes, stream, nullptr, nullptr);
+}
+
+int foremoe_ffn_down_dgrad_timed(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,
+                                 int32_t S, const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
+                                 const void* w_down, int64_t n_cap, void* d_au, void* workspace, size_t ws_bytes,
+                                 void* stream, void* start_event, void* stop_event) {
+  return ffn_down_dgrad_impl(dy_perm, save_au, dtype, d, F, S, slot_offset, slot_widx, W, w_down, n_cap, d_au,
+                             workspace, ws_bytes, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+}
+
+int foremoe_ffn_gate_up_dgrad(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                              const int32_t* slot_offset, const int32_t* slot_widx, int32_t W, const void* w_gate_up,
+                              int64_t n_cap, void* dx_perm, void* workspace, size_t ws_bytes, void* stream) {
+  return ffn_gate_up_dgrad_impl(d_au, dtype, d, F, S, slot_offset, slot_widx, W, w_gate_up, n_cap, dx_perm,
+                                workspace, ws_bytes, stream, nullptr, nullptr);
+}
+
+int foremoe_ffn_gate_up_dgrad_timed(const void* d_au, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
+                                    const int32_t* slot_offset, const int32_t* slot_widx, int32_t W,
+                                    const void* w_gate_up, int64_t n_cap, void* dx_perm, void* workspace,
+                                    size_t ws_bytes, void* stream, void* start_event, void* stop_event) {
+  return ffn_gate_up_dgrad_impl(d_au, dtype, d, F, S, slot_offset, slot_widx, W, w_gate_up, n_cap, dx_perm,
+                                workspace, ws_bytes, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
 }
 
 int foremoe_grouped_ffn_dgrad(const void* dy_perm, const void* save_au, foremoe_dtype dtype, int32_t d, int32_t F,

@@ -48,11 +48,19 @@ def test_version_and_status_strings(lib):
     assert lib.foremoe_status_string(-2) == b"unsupported shape or dtype"
 
 
-def test_set_launch_events_is_host_only(lib):
-    # attaching and detaching events touches no GPU state (no HIP call)
-    assert lib.foremoe_set_launch_events(None, None) == 0
-    assert lib.foremoe_set_launch_events(ctypes.c_void_p(0x1000), None) == 0
-    assert lib.foremoe_set_launch_events(None, None) == 0
+def test_timed_row_gemms_check_like_the_plain_calls(lib):
+    # the timed forms validate their arguments like the plain calls, before
+    # any launch or event record; the ABI keeps no launch state
+    assert not hasattr(lib, "foremoe_set_launch_events")
+    ev = (None, None)
+    assert lib.foremoe_ffn_gate_up_fwd_timed(FAKE, 1, 96, 256, 4, FAKE, FAKE, 3, FAKE, 64, FAKE, None, None, 0,
+                                             None, *ev) == -2
+    assert lib.foremoe_ffn_down_fwd_timed(FAKE, 7, 128, 256, 4, FAKE, FAKE, 3, FAKE, 64, FAKE, None, 0,
+                                          None, *ev) == -1
+    assert lib.foremoe_ffn_down_dgrad_timed(FAKE, FAKE, 1, 128, 200, 4, FAKE, FAKE, 3, FAKE, 64, FAKE, None, 0,
+                                            None, *ev) == -2
+    assert lib.foremoe_ffn_gate_up_dgrad_timed(FAKE, 1, 128, 256, 4, FAKE, FAKE, 3, FAKE, 64, FAKE, FAKE, 16,
+                                               None, *ev) == -1  # workspace too small
 
 
 def test_workspace_size(lib):

@@ -63,6 +63,29 @@ def test_dispatch_bit_exact(gpu, name, fused):
     assert status[63] == 0, "histogram_assign ticket not reset"
 
 
+def test_histogram_assign_stale_workspace(gpu):
+    """A workspace full of garbage (a nonzero arrival ticket, as after a call
+    that did not complete or a workspace never zero-filled) still gives the
+    exact offsets: the count kernel zeroes the ticket first."""
+    from paper_2606_11867_amd import api
+    w = _wl("share")
+    print("\n[case] histogram_assign on a 0xA5-filled workspace, share micro-steps", flush=True)
+    m0 = w.micro[0]
+    T, K = m0.ids.shape
+    ws = api.workspace(T, K, m0.plan.E, gpu)
+    for m in w.micro:
+        ws.fill_(0xA5)
+        ids = torch.from_numpy(m.ids).to(gpu)
+        plan = api.DevicePlan.from_host(m.plan, gpu)
+        counts, rb, sc, so = api.histogram_assign(ids, plan, ws)
+        rc, _ = O.histogram(m.ids, m.plan.E)
+        rrb, rsc, rso = O.assign_replicas(rc, m.plan)
+        assert np.array_equal(counts.cpu().numpy(), rc) and np.array_equal(rb.cpu().numpy(), rrb)
+        assert np.array_equal(sc.cpu().numpy(), rsc) and np.array_equal(so.cpu().numpy(), rso)
+        status = ws[:256].view(torch.int32).cpu().numpy()
+        assert status[2] == 0 and status[63] == 0
+
+
 def test_histogram_assign_repeated_calls(gpu):
     """One workspace, consecutive micro-steps through the fused steps 1-2:
     every call matches the oracle (the arrival ticket is reset each time)."""
