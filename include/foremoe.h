@@ -215,6 +215,31 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Steps 1-3 without a workspace argument, for callers that cannot allocate
+ * device memory (code under stream capture, serving loops that forbid
+ * allocation): the same work and outputs as foremoe_histogram_assign
+ * followed by foremoe_permute with the same arguments, bitwise, and the same
+ * argument rules and errors. The workspace of those two calls lives in a
+ * device array of FOREMOE_STATIC_SCRATCH_BYTES that the library holds on
+ * every device it runs on until the process ends; the call allocates
+ * nothing. Inputs whose workspace would exceed it, i.e.
+ * foremoe_workspace_size(T, K, n_src * E) > FOREMOE_STATIC_SCRATCH_BYTES
+ * (about 8.3 M pairs at E = 128, 1 M pairs at 1024 keys), are rejected with
+ * FOREMOE_EINVAL before anything is launched.
+ * status  int32 [3] out or NULL: the status words FOREMOE_WS_INVALID_IDS,
+ *         FOREMOE_WS_DROPPED and FOREMOE_WS_PLAN_ERRORS of the call.
+ * Every call on one device shares that device's array, which keeps the last
+ * call's contents: calls that overlap in time on one device (two streams,
+ * two host threads) race and give wrong results; order them.
+ */
+#define FOREMOE_STATIC_SCRATCH_BYTES ((size_t)8 << 20)
+int foremoe_dispatch_static(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan,
+                            const void* x, foremoe_dtype dtype, int32_t d, int64_t n_cap,
+                            int32_t* counts, int32_t* rep_begin, int32_t* slot_count,
+                            int32_t* slot_offset, void* x_perm, int32_t* row_to_pair,
+                            int32_t* pair_to_row, int32_t* status, void* stream);
+
+/*
  * Step 4, forward (App. A: SwiGLU expert with gate, up and down matrices).
  * For each slot j, rows [slot_offset[j], slot_offset[j+1]) (clamped to
  * n_cap), with w = slot_widx[j]:

@@ -20,6 +20,7 @@ MAX_SLOTS = 1024
 MAX_REPLICAS = 16
 MAX_TOPK = 64
 MAX_SOURCES = 64
+STATIC_SCRATCH_BYTES = 8 << 20
 
 c_i32, c_i64, c_sz, c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
 
@@ -51,6 +52,8 @@ SIGNATURES = {
     "foremoe_histogram_assign": (ctypes.c_int, [c_p, c_i64, c_i32, PPlan, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]),
     "foremoe_permute": (ctypes.c_int, [c_p, c_i32, c_i64, c_i32, c_p, c_i32, PPlan, c_p, c_p, c_i64,
                                        c_p, c_p, c_p, c_p, c_sz, c_p]),
+    "foremoe_dispatch_static": (ctypes.c_int, [c_p, c_i64, c_i32, PPlan, c_p, c_i32, c_i32, c_i64, c_p, c_p,
+                                               c_p, c_p, c_p, c_p, c_p, c_p, c_p]),
     "foremoe_ffn_workspace_size": (c_sz, []),
     "foremoe_grouped_ffn_fwd": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_p,
                                                c_i64, c_p, c_p, c_p, c_p, c_sz, c_p]),

@@ -173,6 +173,33 @@ def permute(x: torch.Tensor, ids: torch.Tensor, plan: DevicePlan, rep_begin: tor
     return x_perm, row_to_pair, pair_to_row
 
 
+def dispatch_static(x: torch.Tensor, ids: torch.Tensor, plan: DevicePlan, n_cap: int):
+    """Steps 1-3 (as histogram_assign + permute) with the library's static
+    device scratch instead of a workspace; the C call allocates nothing.
+    Returns counts, rep_begin, slot_count, slot_offset, x_perm, row_to_pair,
+    pair_to_row and the three status words (device tensors)."""
+    T, d = x.shape
+    K = ids.shape[1]
+    dev = x.device
+    nkeys = plan.E * max(plan.n_src, 1)
+    shape = (plan.E, plan.R_max + 1) if plan.n_src <= 1 else (plan.n_src, plan.E, plan.R_max + 1)
+    counts = torch.empty(nkeys, dtype=torch.int32, device=dev)
+    rep_begin = torch.empty(shape, dtype=torch.int32, device=dev)
+    slot_count = torch.empty(max(plan.S, 1), dtype=torch.int32, device=dev)[: plan.S]
+    slot_offset = torch.empty(plan.S + 1, dtype=torch.int32, device=dev)
+    x_perm = torch.empty((n_cap, d), dtype=x.dtype, device=dev)
+    row_to_pair = torch.empty(n_cap, dtype=torch.int32, device=dev)
+    pair_to_row = torch.empty(T * K, dtype=torch.int32, device=dev)
+    status = torch.empty(3, dtype=torch.int32, device=dev)
+    cp = plan.c_struct()
+    check(_lib.load().foremoe_dispatch_static(_ptr(ids), T, K, ctypes.byref(cp), _ptr(x), _dt(x), d, n_cap,
+                                              _ptr(counts), _ptr(rep_begin), slot_count.data_ptr(),
+                                              _ptr(slot_offset), x_perm.data_ptr(), row_to_pair.data_ptr(),
+                                              pair_to_row.data_ptr(), _ptr(status), _stream(dev)),
+          "foremoe_dispatch_static")
+    return counts, rep_begin, slot_count, slot_offset, x_perm, row_to_pair, pair_to_row, status
+
+
 def ffn_workspace(device) -> torch.Tensor:
     """Scratch that lets the row GEMMs cut a partial last round of tiles
     along K (foremoe_ffn_workspace_size() bytes for the current device).

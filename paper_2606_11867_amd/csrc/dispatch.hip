@@ -4,6 +4,7 @@
 // ranks come from wavefront ballots plus prefix sums, never from the order
 // in which atomics land.
 #include <climits>
+#include <mutex>
 
 #include "common.h"
 
@@ -743,14 +744,15 @@ static int check_hist(const char* who, const int32_t* ids, int64_t T, int32_t K,
   return FOREMOE_OK;
 }
 
+// status: where the status words go (the workspace header, or a caller's
+// array in foremoe_dispatch_static).
 static int histogram_common(const char* who, const int32_t* ids, int64_t T, int32_t K, int32_t E, KeyMap km,
-                            int32_t* counts, void* ws, size_t ws_bytes, void* stream) {
+                            int32_t* counts, void* ws, size_t ws_bytes, int32_t* status, void* stream) {
   int rc = check_hist(who, ids, T, K, E, counts, ws, ws_bytes);
   if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
-  int32_t* status = (int32_t*)ws;
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
   hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, E,
                      key_bits(E), partial, (uint32_t*)nullptr);
@@ -760,7 +762,8 @@ static int histogram_common(const char* who, const int32_t* ids, int64_t T, int3
 
 int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t* counts, void* ws,
                       size_t ws_bytes, void* stream) {
-  return histogram_common("foremoe_histogram", ids, T, K, E, KeyMap{E, 1, K, nullptr}, counts, ws, ws_bytes, stream);
+  return histogram_common("foremoe_histogram", ids, T, K, E, KeyMap{E, 1, K, nullptr}, counts, ws, ws_bytes,
+                          (int32_t*)ws, stream);
 }
 
 int foremoe_histogram_src(const int32_t* ids, int64_t T, int32_t K, int32_t E, int32_t n_src,
@@ -771,7 +774,7 @@ int foremoe_histogram_src(const int32_t* ids, int64_t T, int32_t K, int32_t E, i
           FOREMOE_MAX_EXPERTS);
   REQUIRE(src_token_begin, "histogram_src: src_token_begin is NULL");
   return histogram_common("foremoe_histogram_src", ids, T, K, E * n_src, KeyMap{E, n_src, K, src_token_begin},
-                          counts, ws, ws_bytes, stream);
+                          counts, ws, ws_bytes, (int32_t*)ws, stream);
 }
 
 static int check_plan(const foremoe_plan* plan, const int32_t* counts, const int32_t* rep_begin,
@@ -802,13 +805,12 @@ static PlanDev plan_dev(const foremoe_plan* plan) {
                  plan->expert_rep_weight, n_src >= 2 ? plan->src_rep_weight : nullptr};
 }
 
-int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
-                            int32_t* slot_offset, void* ws, size_t ws_bytes, void* stream) {
+static int assign_impl(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
+                       int32_t* slot_offset, void* ws, size_t ws_bytes, int32_t* status, void* stream) {
   int rc = check_plan(plan, counts, rep_begin, slot_count, slot_offset, ws, ws_bytes);
   if (rc) return rc;
   const PlanDev P = plan_dev(plan);
   const int n_src = P.n_src;
-  int32_t* status = (int32_t*)ws;
   int32_t* rep_slot = (int32_t*)((char*)ws + kWsRepSlotOff);
   int32_t* vslot = (int32_t*)((char*)ws + kWsVSlotOff);
   if (n_src * plan->E <= 256)
@@ -820,27 +822,31 @@ int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int
   return check_launch("foremoe_assign_replicas");
 }
 
-int foremoe_histogram_assign(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan, int32_t* counts,
-                             int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset, void* ws, size_t ws_bytes,
-                             void* stream) {
+int foremoe_assign_replicas(const int32_t* counts, const foremoe_plan* plan, int32_t* rep_begin, int32_t* slot_count,
+                            int32_t* slot_offset, void* ws, size_t ws_bytes, void* stream) {
+  return assign_impl(counts, plan, rep_begin, slot_count, slot_offset, ws, ws_bytes, (int32_t*)ws, stream);
+}
+
+static int histogram_assign_impl(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan,
+                                 int32_t* counts, int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset,
+                                 void* ws, size_t ws_bytes, int32_t* status, void* stream) {
   int rc = check_plan(plan, counts, rep_begin, slot_count, slot_offset, ws, ws_bytes);
   if (rc) return rc;
   const PlanDev P = plan_dev(plan);
   const int nkeys = P.n_src * P.E;
   const KeyMap km{P.E, P.n_src, K, P.n_src >= 2 ? plan->src_token_begin : nullptr};
   if (nkeys > 256) {  // large key sets: the three separate launches
-    rc = histogram_common("foremoe_histogram_assign", ids, T, K, nkeys, km, counts, ws, ws_bytes, stream);
+    rc = histogram_common("foremoe_histogram_assign", ids, T, K, nkeys, km, counts, ws, ws_bytes, status, stream);
     if (rc) return rc;
-    return foremoe_assign_replicas(counts, plan, rep_begin, slot_count, slot_offset, ws, ws_bytes, stream);
+    return assign_impl(counts, plan, rep_begin, slot_count, slot_offset, ws, ws_bytes, status, stream);
   }
   rc = check_hist("foremoe_histogram_assign", ids, T, K, nkeys, counts, ws, ws_bytes);
   if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
-  int32_t* status = (int32_t*)ws;
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
-  uint32_t* ticket = (uint32_t*)(status + kWsTicketWord);
+  uint32_t* ticket = (uint32_t*)ws + kWsTicketWord;
   hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, nkeys,
                      key_bits(nkeys), partial, ticket);
   hipLaunchKernelGGL(hist_scan_assign_kernel, dim3(nkeys + 1), dim3(kHistThreads), 0, st, partial, nb, nkeys, counts,
@@ -849,10 +855,17 @@ int foremoe_histogram_assign(const int32_t* ids, int64_t T, int32_t K, const for
   return check_launch("foremoe_histogram_assign");
 }
 
-int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, const int32_t* ids, int32_t K,
-                    const foremoe_plan* plan, const int32_t* rep_begin, const int32_t* slot_offset, int64_t n_cap,
-                    void* x_perm, int32_t* row_to_pair, int32_t* pair_to_row, void* ws, size_t ws_bytes,
-                    void* stream) {
+int foremoe_histogram_assign(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan, int32_t* counts,
+                             int32_t* rep_begin, int32_t* slot_count, int32_t* slot_offset, void* ws, size_t ws_bytes,
+                             void* stream) {
+  return histogram_assign_impl(ids, T, K, plan, counts, rep_begin, slot_count, slot_offset, ws, ws_bytes,
+                               (int32_t*)ws, stream);
+}
+
+static int check_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, const int32_t* ids, int32_t K,
+                         const foremoe_plan* plan, const int32_t* rep_begin, const int32_t* slot_offset,
+                         int64_t n_cap, void* x_perm, int32_t* row_to_pair, int32_t* pair_to_row, void* ws,
+                         size_t ws_bytes) {
   REQUIRE(plan, "permute: plan is NULL");
   REQUIRE(dtype == FOREMOE_F32 || dtype == FOREMOE_BF16, "permute: bad dtype");
   REQUIRE(T >= 0 && n_cap >= 0 && d >= 1, "permute: bad sizes");
@@ -874,12 +887,23 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, co
             "permute: n_src out of range");
     REQUIRE(plan->src_token_begin, "permute: plan->src_token_begin is NULL");
   }
+  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, n_src * plan->E), "permute: workspace too small");
+  return FOREMOE_OK;
+}
+
+static int permute_impl(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, const int32_t* ids, int32_t K,
+                        const foremoe_plan* plan, const int32_t* rep_begin, const int32_t* slot_offset, int64_t n_cap,
+                        void* x_perm, int32_t* row_to_pair, int32_t* pair_to_row, void* ws, size_t ws_bytes,
+                        int32_t* status, void* stream) {
+  int rc = check_permute(x, dtype, T, d, ids, K, plan, rep_begin, slot_offset, n_cap, x_perm, row_to_pair,
+                         pair_to_row, ws, ws_bytes);
+  if (rc) return rc;
+  const int esz = dtype == FOREMOE_BF16 ? 2 : 4;
+  const int n_src = plan->n_src < 1 ? 1 : plan->n_src;
   const int nkeys = n_src * plan->E;
-  REQUIRE(ws_bytes >= ws_bytes_needed(T, K, nkeys), "permute: workspace too small");
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
-  int32_t* status = (int32_t*)ws;
   const int32_t* rep_slot = (const int32_t*)((char*)ws + kWsRepSlotOff);
   const int32_t* base = (const int32_t*)((char*)ws + kWsPartialOff);
   // rows come from the virtual slots' offsets (the slot offsets themselves
@@ -893,6 +917,14 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, co
   hipLaunchKernelGGL(gather_rows_kernel, dim3(gather_grid(n_cap)), dim3(256), 0, st, (const uint4*)x, vpr, K,
                      npairs, row_to_pair, slot_offset + plan->S, n_cap, (uint4*)x_perm);
   return check_launch("foremoe_permute");
+}
+
+int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d, const int32_t* ids, int32_t K,
+                    const foremoe_plan* plan, const int32_t* rep_begin, const int32_t* slot_offset, int64_t n_cap,
+                    void* x_perm, int32_t* row_to_pair, int32_t* pair_to_row, void* ws, size_t ws_bytes,
+                    void* stream) {
+  return permute_impl(x, dtype, T, d, ids, K, plan, rep_begin, slot_offset, n_cap, x_perm, row_to_pair, pair_to_row,
+                      ws, ws_bytes, (int32_t*)ws, stream);
 }
 
 static int launch_combine(const void* y_perm, foremoe_dtype in_dtype, const int32_t* pair_to_row, const float* gates,
@@ -967,6 +999,87 @@ int foremoe_combine_bwd(const void* dy, const void* y_perm, foremoe_dtype dtype,
     hipLaunchKernelGGL(combine_bwd_kernel<float>, grid, block, 0, st, (const float*)dy, (const float*)y_perm,
                        pair_to_row, gates, T, K, d, n_cap, (float*)dy_perm, dgates);
   return check_launch("foremoe_combine_bwd");
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Steps 1-3 without a caller workspace: the workspace of foremoe_histogram_assign
+// and foremoe_permute lives in a file-scope device array instead, for callers
+// that cannot allocate device memory.
+// ---------------------------------------------------------------------------
+namespace foremoe {
+namespace {
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;  // FOREMOE_STATIC_SCRATCH_BYTES
+constexpr int kMaxStaticDevices = 64;
+static_assert(kStaticScratchBytes == FOREMOE_STATIC_SCRATCH_BYTES, "header and library disagree");
+}  // namespace
+}  // namespace foremoe
+
+// Every device the library runs on holds its own copy of this array until the
+// process ends. In host code `scratch` names a host-side stand-in, never the
+// device memory: kernels receive the per-device address from
+// hipGetSymbolAddress below.
+static __device__ __align__(256) unsigned char scratch[foremoe::kStaticScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[foremoe::kMaxStaticDevices];
+
+// The current device's address of `scratch`, looked up once per device with
+// that device current.
+static int static_scratch_ptr(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_error(FOREMOE_EHIP, "dispatch_static: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= foremoe::kMaxStaticDevices)
+    return set_error(FOREMOE_EUNSUPPORTED, "dispatch_static: device %d above %d", dev, foremoe::kMaxStaticDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(FOREMOE_EHIP, "dispatch_static: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FOREMOE_OK;
+}
+
+extern "C" {
+
+int foremoe_dispatch_static(const int32_t* ids, int64_t T, int32_t K, const foremoe_plan* plan, const void* x,
+                            foremoe_dtype dtype, int32_t d, int64_t n_cap, int32_t* counts, int32_t* rep_begin,
+                            int32_t* slot_count, int32_t* slot_offset, void* x_perm, int32_t* row_to_pair,
+                            int32_t* pair_to_row, int32_t* status, void* stream) {
+  REQUIRE(plan, "dispatch_static: plan is NULL");
+  REQUIRE(T >= 0 && K >= 1 && K <= FOREMOE_MAX_TOPK, "dispatch_static: T or K out of range");
+  REQUIRE(T * (int64_t)K < (int64_t)INT_MAX, "dispatch_static: T*K must be below 2^31");
+  REQUIRE(plan->E >= 1 && plan->E <= FOREMOE_MAX_EXPERTS, "dispatch_static: E=%d out of range", plan->E);
+  const int n_src = plan->n_src < 1 ? 1 : plan->n_src;
+  REQUIRE(n_src <= FOREMOE_MAX_SOURCES && (int64_t)n_src * plan->E <= FOREMOE_MAX_EXPERTS,
+          "dispatch_static: n_src * E above %d", FOREMOE_MAX_EXPERTS);
+  const size_t need = ws_bytes_needed(T, K, n_src * plan->E);
+  REQUIRE(need <= kStaticScratchBytes,
+          "dispatch_static: %lld pairs over %d keys need %zu bytes of scratch, above the %zu of the static array",
+          (long long)(T * K), n_src * plan->E, need, kStaticScratchBytes);
+  void* ws = nullptr;
+  int rc = static_scratch_ptr(&ws);
+  if (rc) return rc;
+  // every argument of both steps is checked before anything is launched
+  rc = check_plan(plan, counts, rep_begin, slot_count, slot_offset, ws, kStaticScratchBytes);
+  if (rc) return rc;
+  rc = check_hist("dispatch_static", ids, T, K, n_src * plan->E, counts, ws, kStaticScratchBytes);
+  if (rc) return rc;
+  rc = check_permute(x, dtype, T, d, ids, K, plan, rep_begin, slot_offset, n_cap, x_perm, row_to_pair, pair_to_row,
+                     ws, kStaticScratchBytes);
+  if (rc) return rc;
+  // status words into the caller's array, else into the scratch header
+  int32_t* st = status ? status : (int32_t*)ws;
+  rc = histogram_assign_impl(ids, T, K, plan, counts, rep_begin, slot_count, slot_offset, ws, kStaticScratchBytes, st,
+                             stream);
+  if (rc) return rc;
+  return permute_impl(x, dtype, T, d, ids, K, plan, rep_begin, slot_offset, n_cap, x_perm, row_to_pair, pair_to_row,
+                      ws, kStaticScratchBytes, st, stream);
 }
 
 }  // extern "C"
