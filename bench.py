@@ -43,13 +43,9 @@ if ROOT not in sys.path:
 
 METRIC = "grouped-FFN TFLOP/s & % bf16 MFMA peak; permute+combine GB/s; tokens/s per micro-step"
 
-PHASES = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
-          "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
 # phases that are exactly one kernel launch (candidates for the roofline line)
 SINGLE_LAUNCH = {"gate_up_fwd", "down_fwd", "combine", "combine_bwd", "down_dgrad",
                  "gate_up_dgrad", "permute_bwd"}
-# row-GEMM phases: one kernel each, timed by events attached to the launch
-ROW_GEMMS = {"gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad"}
 
 
 def parse():
@@ -104,6 +100,7 @@ def main() -> int:
     import torch
 
     from paper_2606_11867_amd import _lib, api
+    from paper_2606_11867_amd.policy_update import PHASES, MicroStep, PolicyUpdate
     from workload import make_workload
     from workload import accounting as acc
 
@@ -129,146 +126,27 @@ def main() -> int:
     for i in range(n_micro):
         m = w.micro[i]
         assert np.array_equal(m.plan.local_experts, local)
-        dp = api.DevicePlan.from_host(m.plan, dev)
-        mss.append(dict(ids=torch.from_numpy(m.ids).to(dev), gates=torch.from_numpy(m.gates).to(dev),
-                        x=dv(w.x(i)), dy=dv(w.dy(i)), plan=dp, cplan=dp.c_struct(), S=m.plan.S))
-    S_max = max(ms["S"] for ms in mss)
-    n_cap = T * K
-    z = lambda *s, dt=bf: torch.zeros(s, dtype=dt, device=dev)  # noqa: E731
-    def step_buffers():
-        return dict(
-            counts=z(E, dt=torch.int32), rep_begin=z(E, 3, dt=torch.int32), slot_count=z(S_max, dt=torch.int32),
-            slot_offset=z(S_max + 1, dt=torch.int32), ws=api.workspace(T, K, E, dev),
-            x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
-            y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d), dy_perm=z(n_cap, d),
-            dgates=z(T, K, dt=torch.float32), d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d), dx=z(T, d))
-
-    # activations of one micro-step; a second set lets the next micro-step's
-    # forward start while this one's weight gradients still read its set
-    sets = [step_buffers(), step_buffers()]
-    buf = dict(sets[0], dwgu=z(G, 2 * F, d, dt=torch.float32), dwdn=z(G, d, F, dt=torch.float32),
-               wws=api.wgrad_workspace(d, F, dev), rws=api.ffn_workspace(dev))
-    P = {k: v.data_ptr() for k, v in buf.items()}
-    PS = [dict(P, **{k: v.data_ptr() for k, v in st.items()}) for st in sets]
-    wsz = buf["ws"].numel()
-    wwsz = buf["wws"].numel()
-    # row-GEMM workspace (tail split of a partial last round of tiles)
-    rws, rwsz = (None, 0) if args.no_split else (P["rws"], buf["rws"].numel())
-    stream = torch.cuda.current_stream(dev)
-    BF16 = _lib.BF16
+        mss.append(MicroStep(ids=torch.from_numpy(m.ids).to(dev), gates=torch.from_numpy(m.gates).to(dev),
+                             x=dv(w.x(i)), dy=dv(w.dy(i)), plan=api.DevicePlan.from_host(m.plan, dev)))
+    S_max = max(ms.S for ms in mss)
+    # buffers, workspaces and the two streams of the benchmark's schedule
+    pu = PolicyUpdate(T, K, d, F, E, G, S_max, gu, dn, dev, split=not args.no_split)
+    stream = pu.main
+    buf = pu.sets[0]
     setup_s = time.time() - t0
 
-    def chk(rc, what):
-        if rc != 0:
-            raise _lib.ForeMoEError(rc, what)
-
-    side = torch.cuda.Stream(dev)  # default priority, like every stream here
-
-    done = [torch.cuda.Event(), torch.cuda.Event()]  # side-stream work of the micro-step using set b
-
-    def step_ops(i, ev=None, overlap=False, pipelined=False):
-        """The operations of one micro-step, in order, as (phase, thunk)
-        pairs (phase None: a stream dependency). With overlap the two
-        weight-gradient GEMMs run on the side stream, each beside the
-        data-gradient GEMM that does not feed it: down wgrad (needs dy_perm)
-        beside down dgrad, gate/up wgrad (needs d_au) beside gate/up dgrad.
-        Both share one workspace, so they stay ordered on that one stream;
-        the main stream waits for the side stream before the step ends, so
-        the next step's buffers are free. Pipelined, the streams are not
-        joined: micro-step i uses buffer set i % 2, and before reusing it
-        the main stream waits for the side-stream work of micro-step i - 2.
-        ev maps phases to (begin, end) event pairs recorded on the stream
-        the phase runs on."""
-        main = stream
-        bset = i % 2 if pipelined else 0
-        P = PS[bset]
-        ms = mss[i % n_micro]
-        S = ms["S"]
-        so = P["slot_offset"]
-        widx, gidx = ms["plan"].slot_widx.data_ptr(), ms["plan"].slot_gidx.data_ptr()
-        cp = ctypes.byref(ms["cplan"])
-        ops = []
-
-        def call(phase, st, rc_fn):
-            def run():
-                timed = ev is not None and phase in ev
-                # row GEMMs (rc_fn takes the two events) carry their events on
-                # the kernel dispatch itself (no event commands between the
-                # kernels); the other phases are bracketed by event records
-                # on their stream
-                if phase in ROW_GEMMS:
-                    e = (ev[phase][0].cuda_event, ev[phase][1].cuda_event) if timed else (None, None)
-                    chk(rc_fn(st.cuda_stream, *e), phase)
-                    return
-                if timed:
-                    ev[phase][0].record(st)
-                chk(rc_fn(st.cuda_stream), phase)
-                if timed:
-                    ev[phase][1].record(st)
-            ops.append((phase, run))
-
-        def dep(waiter, on):
-            ops.append((None, lambda: waiter.wait_stream(on)))
-
-        def gate_up_wgrad(st):
-            call("gate_up_wgrad", st, lambda q: lib.foremoe_ffn_gate_up_wgrad(
-                P["d_au"], P["x_perm"], BF16, d, F, S, so, gidx, G, n_cap, P["dwgu"], P["wws"], wwsz, q))
-
-        def down_wgrad(st):
-            call("down_wgrad", st, lambda q: lib.foremoe_ffn_down_wgrad(
-                P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, P["dwdn"], P["wws"], wwsz, q))
-
-        if pipelined:  # set bset was last used two micro-steps ago: its weight gradients must be done
-            ops.append((None, lambda: main.wait_event(done[bset])))
-        call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
-            ms["ids"].data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
-        call("permute", main, lambda q: lib.foremoe_permute(
-            ms["x"].data_ptr(), BF16, T, d, ms["ids"].data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
-            P["r2p"], P["p2r"], P["ws"], wsz, q))
-        call("gate_up_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_fwd_timed(
-            P["x_perm"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["h"], P["au"], rws, rwsz, q, e0, e1))
-        call("down_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_down_fwd_timed(
-            P["h"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["y_perm"], rws, rwsz, q, e0, e1))
-        call("combine", main, lambda q: lib.foremoe_combine(
-            P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap, P["y"], BF16, q))
-        call("combine_bwd", main, lambda q: lib.foremoe_combine_bwd(
-            ms["dy"].data_ptr(), P["y_perm"], BF16, P["p2r"], ms["gates"].data_ptr(), T, K, d, n_cap,
-            P["dy_perm"], P["dgates"], q))
-        if overlap:
-            dep(side, main)
-            down_wgrad(side)
-        call("down_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_down_dgrad_timed(
-            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn.data_ptr(), n_cap, P["d_au"], rws, rwsz, q,
-            e0, e1))
-        if overlap:
-            dep(side, main)
-            gate_up_wgrad(side)
-        call("gate_up_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_dgrad_timed(
-            P["d_au"], BF16, d, F, S, so, widx, G, gu.data_ptr(), n_cap, P["dx_perm"], rws, rwsz, q, e0, e1))
-        if not overlap:
-            gate_up_wgrad(main)
-            down_wgrad(main)
-        call("permute_bwd", main, lambda q: lib.foremoe_permute_bwd(
-            P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], BF16, q))
-        if pipelined:
-            ops.append((None, lambda: done[bset].record(side)))
-        elif overlap:
-            dep(main, side)
-        return ops
-
     def run_step(i, ev=None, overlap=False, pipelined=False):
-        for _, op in step_ops(i, ev, overlap or pipelined, pipelined):
-            op()
+        pu.run(i, mss[i % n_micro], ev, overlap, pipelined)
 
     # ---- realised per-micro-step sizes (read back once, outside the timed region)
     Ns, Gs = [], []
     for i in range(n_micro):
         run_step(i)
         torch.cuda.synchronize()
-        S = mss[i]["S"]
+        S = mss[i].S
         sc = buf["slot_count"][:S].cpu().numpy()
         Ns.append(int(buf["slot_offset"][S].item()))
-        gidx = mss[i]["plan"].slot_gidx.cpu().numpy()
+        gidx = mss[i].plan.slot_gidx.cpu().numpy()
         Gs.append(int(len(set(gidx[sc > 0].tolist()))))
 
     overlap = not args.no_overlap
@@ -319,16 +197,15 @@ def main() -> int:
         run_step(i, ev, overlap=overlap, pipelined=pipelined)
 
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for e in done:
-        e.record(side)
+    pu.start()
     for i in range(2):
         timed_step(i, None)
-    stream.wait_stream(side)
+    pu.finish()
     torch.cuda.synchronize()
     start.record(stream)
     for s in range(args.steps):
         timed_step(s, evs[s])
-    stream.wait_stream(side)
+    pu.finish()
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)

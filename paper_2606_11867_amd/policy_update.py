@@ -1,0 +1,201 @@
+"""One policy-update micro-step of the expert layer through the C ABI, in the
+launch configuration the benchmark times (Sec. 7.1: the policy update runs
+forward and backward per micro-step; Sec. 6.2 and App. A.4: the expert
+gradients accumulate in fp32 over the micro-steps).
+
+Only ABI calls and stream ordering live here; every step of the path runs in
+libforemoe.so. A micro-step is
+
+  histogram + assign_replicas (one call) -> permute -> gate/up (+SwiGLU) -> down
+  -> combine -> combine_bwd -> down dgrad (+SwiGLU') -> gate/up dgrad
+  -> gate/up wgrad, down wgrad -> permute_bwd
+
+Schedules:
+  * one stream: every call in that order;
+  * overlap: the two weight-gradient GEMMs run on a second stream (default
+    priority), each beside the data-gradient GEMM that does not feed it
+    (down wgrad beside down dgrad, gate/up wgrad beside gate/up dgrad); both
+    share one workspace, so they stay ordered on that stream, and the main
+    stream waits for it at the end of the micro-step;
+  * pipelined: as overlap, but the streams are never joined: micro-step i
+    uses activation buffer set i % 2 and, before reusing it, the main
+    stream waits for the side-stream work of micro-step i - 2, so the next
+    micro-step's dispatch and forward start while this one's weight
+    gradients run.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Dict, List, Optional
+
+import torch
+
+from . import _lib
+from .api import DevicePlan, ffn_workspace, wgrad_workspace, workspace
+
+PHASES = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
+          "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
+# row-GEMM phases: one kernel each, timed by events attached to the launch
+ROW_GEMMS = {"gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad"}
+
+
+class MicroStep:
+    """The resident inputs of one micro-step: routing, gates, tokens, the
+    upstream gradient and the slot table, all device tensors."""
+
+    def __init__(self, ids: torch.Tensor, gates: torch.Tensor, x: torch.Tensor, dy: torch.Tensor,
+                 plan: DevicePlan):
+        self.ids, self.gates, self.x, self.dy, self.plan = ids, gates, x, dy, plan
+        self.cplan = plan.c_struct()
+        self.S = plan.S
+
+
+class PolicyUpdate:
+    """Buffers, workspaces and streams for running micro-steps of one rank's
+    share (T tokens, top-K, width d, FFN width F, E experts, G gradient
+    groups, at most S_max slots) with bf16 activations and weights, and the
+    fp32 weight gradients dw_gate_up [G, 2F, d], dw_down [G, d, F] that every
+    micro-step accumulates into.
+
+    split: give the row GEMMs their workspace (a partial last round of tiles
+    is cut along K)."""
+
+    def __init__(self, T: int, K: int, d: int, F: int, E: int, G: int, S_max: int, w_gate_up: torch.Tensor,
+                 w_down: torch.Tensor, device, split: bool = True, y_dtype=torch.bfloat16,
+                 dx_dtype=torch.bfloat16):
+        self.lib = _lib.load()
+        self.T, self.K, self.d, self.F, self.E, self.G = T, K, d, F, E, G
+        self.dev = torch.device(device)
+        self.n_cap = T * K
+        self.gu, self.dn = w_gate_up, w_down
+        self.y_dt, self.dx_dt = _lib.BF16 if y_dtype == torch.bfloat16 else _lib.F32, \
+            _lib.BF16 if dx_dtype == torch.bfloat16 else _lib.F32
+        bf = torch.bfloat16
+        dev = self.dev
+        z = lambda *s, dt=bf: torch.zeros(s, dtype=dt, device=dev)  # noqa: E731
+        n_cap = self.n_cap
+
+        def buffer_set():
+            return dict(
+                counts=z(E, dt=torch.int32), rep_begin=z(E, 17, dt=torch.int32), slot_count=z(S_max, dt=torch.int32),
+                slot_offset=z(S_max + 1, dt=torch.int32), ws=workspace(T, K, E, dev),
+                x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
+                y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d, dt=y_dtype), dy_perm=z(n_cap, d),
+                dgates=z(T, K, dt=torch.float32), d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d),
+                dx=z(T, d, dt=dx_dtype))
+
+        # two activation sets: the next micro-step's forward can start while
+        # this one's weight gradients still read its set
+        self.sets: List[Dict[str, torch.Tensor]] = [buffer_set(), buffer_set()]
+        self.dw_gate_up = z(G, 2 * F, d, dt=torch.float32)
+        self.dw_down = z(G, d, F, dt=torch.float32)
+        self.wws = wgrad_workspace(d, F, dev)
+        self.rws = ffn_workspace(dev) if split else None
+        self.main = torch.cuda.current_stream(dev)
+        self.side = torch.cuda.Stream(dev)  # default priority, like every stream here
+        self.done = [torch.cuda.Event(), torch.cuda.Event()]  # side-stream work of the micro-step using set b
+        self._ptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.sets]
+
+    def set_of(self, i: int, pipelined: bool) -> Dict[str, torch.Tensor]:
+        """The activation buffers micro-step i uses under that schedule."""
+        return self.sets[i % 2 if pipelined else 0]
+
+    def start(self) -> None:
+        """Before the first pipelined micro-step: nothing to wait for yet."""
+        for e in self.done:
+            e.record(self.side)
+
+    def finish(self) -> None:
+        """Join the side stream into the main stream."""
+        self.main.wait_stream(self.side)
+
+    def ops(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
+            pipelined: bool = False) -> list:
+        """The operations of micro-step i on inputs ms, in order, as (phase,
+        thunk) pairs (phase None: a stream dependency). ev maps phases to
+        (begin, end) torch events: row GEMMs carry theirs on the kernel
+        launch, the other phases are bracketed by event records on the stream
+        the phase runs on."""
+        lib, main, side = self.lib, self.main, self.side
+        overlap = overlap or pipelined
+        bset = i % 2 if pipelined else 0
+        P = self._ptrs[bset]
+        T, K, d, F, G, n_cap = self.T, self.K, self.d, self.F, self.G, self.n_cap
+        S = ms.S
+        so = P["slot_offset"]
+        widx, gidx = ms.plan.slot_widx.data_ptr(), ms.plan.slot_gidx.data_ptr()
+        cp = ctypes.byref(ms.cplan)
+        wsz = self.sets[bset]["ws"].numel()
+        rws, rwsz = (None, 0) if self.rws is None else (self.rws.data_ptr(), self.rws.numel())
+        wws, wwsz = self.wws.data_ptr(), self.wws.numel()
+        gu, dn = self.gu.data_ptr(), self.dn.data_ptr()
+        dwgu, dwdn = self.dw_gate_up.data_ptr(), self.dw_down.data_ptr()
+        BF16 = _lib.BF16
+        ops = []
+
+        def call(phase, st, rc_fn):
+            def run():
+                timed = ev is not None and phase in ev
+                if phase in ROW_GEMMS:
+                    e = (ev[phase][0].cuda_event, ev[phase][1].cuda_event) if timed else (None, None)
+                    _lib.check(rc_fn(st.cuda_stream, *e), phase)
+                    return
+                if timed:
+                    ev[phase][0].record(st)
+                _lib.check(rc_fn(st.cuda_stream), phase)
+                if timed:
+                    ev[phase][1].record(st)
+            ops.append((phase, run))
+
+        def dep(waiter, on):
+            ops.append((None, lambda: waiter.wait_stream(on)))
+
+        def gate_up_wgrad(st):
+            call("gate_up_wgrad", st, lambda q: lib.foremoe_ffn_gate_up_wgrad(
+                P["d_au"], P["x_perm"], BF16, d, F, S, so, gidx, G, n_cap, dwgu, wws, wwsz, q))
+
+        def down_wgrad(st):
+            call("down_wgrad", st, lambda q: lib.foremoe_ffn_down_wgrad(
+                P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, dwdn, wws, wwsz, q))
+
+        if pipelined:  # set bset was last used two micro-steps ago: its weight gradients must be done
+            ops.append((None, lambda: main.wait_event(self.done[bset])))
+        call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
+            ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
+        call("permute", main, lambda q: lib.foremoe_permute(
+            ms.x.data_ptr(), BF16, T, d, ms.ids.data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
+            P["r2p"], P["p2r"], P["ws"], wsz, q))
+        call("gate_up_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_fwd_timed(
+            P["x_perm"], BF16, d, F, S, so, widx, G, gu, n_cap, P["h"], P["au"], rws, rwsz, q, e0, e1))
+        call("down_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_down_fwd_timed(
+            P["h"], BF16, d, F, S, so, widx, G, dn, n_cap, P["y_perm"], rws, rwsz, q, e0, e1))
+        call("combine", main, lambda q: lib.foremoe_combine(
+            P["y_perm"], BF16, P["p2r"], ms.gates.data_ptr(), T, K, d, n_cap, P["y"], self.y_dt, q))
+        call("combine_bwd", main, lambda q: lib.foremoe_combine_bwd(
+            ms.dy.data_ptr(), P["y_perm"], BF16, P["p2r"], ms.gates.data_ptr(), T, K, d, n_cap,
+            P["dy_perm"], P["dgates"], q))
+        if overlap:
+            dep(side, main)
+            down_wgrad(side)
+        call("down_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_down_dgrad_timed(
+            P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn, n_cap, P["d_au"], rws, rwsz, q, e0, e1))
+        if overlap:
+            dep(side, main)
+            gate_up_wgrad(side)
+        call("gate_up_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_dgrad_timed(
+            P["d_au"], BF16, d, F, S, so, widx, G, gu, n_cap, P["dx_perm"], rws, rwsz, q, e0, e1))
+        if not overlap:
+            gate_up_wgrad(main)
+            down_wgrad(main)
+        call("permute_bwd", main, lambda q: lib.foremoe_permute_bwd(
+            P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], self.dx_dt, q))
+        if pipelined:
+            ops.append((None, lambda: self.done[bset].record(side)))
+        elif overlap:
+            dep(main, side)
+        return ops
+
+    def run(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
+            pipelined: bool = False) -> None:
+        for _, op in self.ops(i, ms, ev, overlap, pipelined):
+            op()

@@ -376,7 +376,7 @@ def test_ffn_backward(gpu, name, split):
 # ---------------------------------------------------------------------------
 # Step 5 and the backward gathers
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("name", SMALL + ["tiny", "qwen3", "dsv3"])
+@pytest.mark.parametrize("name", SMALL + ["tiny", "mixtral", "qwen3", "dsv3"])
 def test_gathers(gpu, name):
     from paper_2606_11867_amd import api
     w = _wl(name)

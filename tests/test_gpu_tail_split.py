@@ -51,16 +51,22 @@ def sampled(off, rng, per_slot=5):
     return np.array(rows), np.array(sub), np.array(widx)
 
 
-@pytest.mark.parametrize("F,rows", [(256, [9000, 20000, 9400]), (256, [5000, 12000, 3000]),
-                                    (384, [2000, 5000, 1500])],
-                         ids=["rounds+tail", "all-split", "128-wide-tiles"])
-def test_tail_split_parity_and_determinism(gpu, F, rows):
+# (F, rows of each slot, expected pieces of the gate/up forward and the down
+# dgrad on a 256-CU MI355X): 304 gate/up tiles leave a last round of 48 (4
+# pieces); 79 down-dgrad tiles (2 pieces); 102 tiles of either (2 pieces);
+# 64 gate/up tiles (3 pieces) and 32 down-dgrad tiles (4 pieces)
+@pytest.mark.parametrize("F,rows,pieces", [(256, [9000, 20000, 9400], (4, 1)), (256, [5000, 12000, 3000], (1, 2)),
+                                           (384, [2000, 5000, 1500], (2, 2)), (256, [4000, 4000], (3, 4))],
+                         ids=["rounds+tail", "all-split", "128-wide-tiles", "three-and-four-pieces"])
+def test_tail_split_parity_and_determinism(gpu, F, rows, pieces):
     from paper_2606_11867_amd import api
     grid = torch.cuda.get_device_properties(gpu).multi_processor_count
     s_fwd = expected_split(rows, 2 * F, D, grid)   # gate/up forward: N = 2F, K = d
     s_dgr = expected_split(rows, F, D, grid)       # down dgrad: N = F, K = d
-    print(f"F={F} rows {rows}: pieces gate/up fwd {s_fwd}, down dgrad {s_dgr}", flush=True)
+    print(f"F={F} rows {rows}: pieces gate/up fwd {s_fwd}, down dgrad {s_dgr} ({grid} CUs)", flush=True)
     assert max(s_fwd, s_dgr) >= 2, "layout no longer exercises the split"
+    if grid == 256:
+        assert (s_fwd, s_dgr) == pieces
     rng = np.random.default_rng(5)
     off = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
     N = int(off[-1])
