@@ -5,4 +5,5 @@ import this package. The product path (the HIP library and its binding)
 never calls it and shares no code with it.
 """
 from . import foremoe_oracle  # noqa: F401
+from . import foremoe_transfer  # noqa: F401
 from .foremoe_oracle import *  # noqa: F401,F403
