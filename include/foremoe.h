@@ -385,6 +385,84 @@ int foremoe_permute_bwd(const void* dx_perm, foremoe_dtype in_dtype, const int32
                         foremoe_dtype out_dtype, void* stream);
 
 /*
+ * Expert Transfer Engine, the part one GPU runs (Sec. 6).
+ *
+ * Records (App. A.3: one expert's state, S_e + S_g bytes). A record holds,
+ * in this order and each in the weights' own row-major layout, the parts
+ * `what` selects: FOREMOE_XFER_PARAMS = the gate/up parameters [2F, d] and
+ * the down parameters [d, F] in the parameter dtype (S_e = 3 d F p_w bytes);
+ * FOREMOE_XFER_GRADS = the fp32 gate/up gradient [2F, d] and down gradient
+ * [d, F] (S_g = 12 d F bytes, App. A.4 fp32 accumulation). Record i of a
+ * buffer starts at i * foremoe_xfer_record_bytes(d, F, dtype, what)
+ * (0 for invalid arguments). d * F must be a multiple of 8.
+ * Index lists (widx, gidx, gmode, expert) are HOST arrays of n entries,
+ * n <= FOREMOE_MAX_XFER_RECORDS; they are checked on the host before any
+ * launch. Expert arrays and buffers are device memory, 16-byte aligned:
+ * w_gate_up [W, 2F, d], w_down [W, d, F] (parameter dtype), dw_gate_up
+ * [G, 2F, d], dw_down [G, d, F] (fp32).
+ */
+#define FOREMOE_XFER_PARAMS 1
+#define FOREMOE_XFER_GRADS 2
+#define FOREMOE_XFER_ASSIGN 0 /* the gradient target takes the record           */
+#define FOREMOE_XFER_ADD 1    /* the record is added into the gradient target    */
+#define FOREMOE_MAX_XFER_RECORDS 64
+size_t foremoe_xfer_record_bytes(int32_t d, int32_t F, foremoe_dtype dtype, int32_t what);
+
+/*
+ * Copy-out (Sec. 6.2): pack the experts leaving this GPU into the send
+ * buffer, record i holding weight slot widx[i] (with PARAMS) and gradient
+ * slot gidx[i] (with GRADS). buf: at least n records. One kernel launch
+ * (none for n = 0); the source arrays are only read.
+ */
+int foremoe_copy_out(const void* w_gate_up, const void* w_down, foremoe_dtype dtype, int32_t W,
+                     const float* dw_gate_up, const float* dw_down, int32_t G, int32_t d, int32_t F,
+                     int32_t n, const int32_t* widx, const int32_t* gidx, int32_t what, void* buf,
+                     size_t buf_bytes, void* stream);
+
+/*
+ * Copy-in (Sec. 6.2): unpack the n records of a receive buffer. With PARAMS,
+ * record i's parameters go to weight slot widx[i] (< 0: skipped; two
+ * records may not name one slot). With GRADS, record i's gradient goes to
+ * gradient slot gidx[i] (< 0: skipped): gmode[i] = FOREMOE_XFER_ASSIGN moves
+ * it there (an expert arriving with its accumulated gradient),
+ * FOREMOE_XFER_ADD adds it (a replica's partial gradient accumulated into
+ * the main expert, Sec. 6.2). The records naming one gradient slot are
+ * applied in record order, starting from the slot's current value, every
+ * sum rounded to fp32, so the result is deterministic. One kernel launch.
+ */
+int foremoe_copy_in(const void* buf, size_t buf_bytes, int32_t n, const int32_t* widx,
+                    const int32_t* gidx, const int32_t* gmode, int32_t what, void* w_gate_up,
+                    void* w_down, foremoe_dtype dtype, int32_t W, float* dw_gate_up, float* dw_down,
+                    int32_t G, int32_t d, int32_t F, void* stream);
+
+/*
+ * CPU-assisted path (Sec. 6.1), host only, synchronous, no GPU work: of
+ * the n experts the next micro-step needs (needed[n], distinct), those
+ * already in a weight slot (resident[W]: expert of each slot, -1 empty)
+ * stay there; each missing one, in the order listed, takes the lowest slot
+ * whose expert is not needed. Outputs (host): slot_of[n], the weight slot
+ * of each needed expert, and the n_fetch fetches (fetch_expert[i] into
+ * weight slot fetch_widx[i]), exactly the needed experts not resident.
+ */
+int foremoe_plan_prefetch(const int32_t* resident, int32_t W, const int32_t* needed, int32_t n,
+                          int32_t* slot_of, int32_t* fetch_expert, int32_t* fetch_widx,
+                          int32_t* n_fetch);
+
+/*
+ * CPU-assisted prefetch (Sec. 6.1; App. A.2): copy the parameters of
+ * expert[i] from the host master copy (host_gate_up [E, 2F, d], host_down
+ * [E, d, F]; HOST memory, pinned with hipHostMalloc so that the copy runs
+ * asynchronously on the DMA engines) into weight slot widx[i] (distinct) of
+ * the device arrays, as host-to-device copies queued on `stream` (the
+ * caller's auxiliary stream, so that they overlap the current layer's work
+ * on the main stream). No kernel, no GPU buffer.
+ */
+int foremoe_prefetch_experts(const void* host_gate_up, const void* host_down, int32_t E,
+                             foremoe_dtype dtype, int32_t d, int32_t F, int32_t n,
+                             const int32_t* expert, const int32_t* widx, void* w_gate_up,
+                             void* w_down, int32_t W, void* stream);
+
+/*
  * Placement planner (host only: HOST arrays, no GPU work, synchronous).
  * Produces the placement that the GPU steps consume, from the routing
  * foreseen during rollout (Sec. 5). Ranks are numbered machine-major:

@@ -21,6 +21,11 @@ MAX_REPLICAS = 16
 MAX_TOPK = 64
 MAX_SOURCES = 64
 STATIC_SCRATCH_BYTES = 8 << 20
+XFER_PARAMS = 1
+XFER_GRADS = 2
+XFER_ASSIGN = 0
+XFER_ADD = 1
+MAX_XFER_RECORDS = 64
 
 c_i32, c_i64, c_sz, c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
 
@@ -78,6 +83,14 @@ SIGNATURES = {
     "foremoe_combine_bwd": (ctypes.c_int, [c_p, c_p, c_i32, c_p, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_p,
                                            c_p]),
     "foremoe_permute_bwd": (ctypes.c_int, [c_p, c_i32, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_i32, c_p]),
+    "foremoe_xfer_record_bytes": (c_sz, [c_i32, c_i32, c_i32, c_i32]),
+    "foremoe_copy_out": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p,
+                                        c_i32, c_p, c_sz, c_p]),
+    "foremoe_copy_in": (ctypes.c_int, [c_p, c_sz, c_i32, c_p, c_p, c_p, c_i32, c_p, c_p, c_i32, c_i32, c_p, c_p,
+                                       c_i32, c_i32, c_i32, c_p]),
+    "foremoe_plan_prefetch": (ctypes.c_int, [c_p, c_i32, c_p, c_i32, c_p, c_p, c_p, c_p]),
+    "foremoe_prefetch_experts": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p,
+                                                c_i32, c_p]),
     "foremoe_plan_base": (ctypes.c_int, [c_p, c_i32, PMachine, c_i64, c_i64, c_p]),
     "foremoe_plan_micro_step": (ctypes.c_int, [c_p, c_i32, PMachine, c_p, c_i32, c_p, c_p, c_p]),
     "foremoe_plan_rank_slots": (ctypes.c_int, [c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p, c_p, c_p, c_p]),

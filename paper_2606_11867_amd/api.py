@@ -312,6 +312,78 @@ def permute_bwd(dx_perm: torch.Tensor, pair_to_row: torch.Tensor, T: int, K: int
 
 
 # ---------------------------------------------------------------------------
+# Expert Transfer Engine, the part one GPU runs (see include/foremoe.h)
+# ---------------------------------------------------------------------------
+def xfer_record_bytes(d: int, F: int, dtype: torch.dtype, what: int) -> int:
+    return int(_lib.load().foremoe_xfer_record_bytes(d, F, _DT[dtype], what))
+
+
+def _host_list(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32).reshape(-1))
+
+
+def copy_out(w_gate_up: torch.Tensor, w_down: torch.Tensor, dw_gate_up: torch.Tensor, dw_down: torch.Tensor,
+             widx, gidx, what: int, buf: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Copy-out: records of weight slots widx / gradient slots gidx (host
+    lists) packed into a send buffer (uint8 device tensor)."""
+    W, F2, d = w_gate_up.shape
+    F = F2 // 2
+    G = dw_gate_up.shape[0]
+    wi, gi = _host_list(widx), _host_list(gidx)
+    n = len(wi)
+    rb = xfer_record_bytes(d, F, w_gate_up.dtype, what)
+    if buf is None:
+        buf = torch.empty(n * rb, dtype=torch.uint8, device=w_gate_up.device)
+    check(_lib.load().foremoe_copy_out(_ptr(w_gate_up), _ptr(w_down), _dt(w_gate_up), W, _ptr(dw_gate_up),
+                                       _ptr(dw_down), G, d, F, n, wi.ctypes.data, gi.ctypes.data, what, _ptr(buf),
+                                       buf.numel(), _stream(w_gate_up.device)), "foremoe_copy_out")
+    return buf
+
+
+def copy_in(buf: torch.Tensor, widx, gidx, gmode, what: int, w_gate_up: torch.Tensor, w_down: torch.Tensor,
+            dw_gate_up: torch.Tensor, dw_down: torch.Tensor) -> None:
+    """Copy-in: unpack the records of a receive buffer in place into the
+    expert arrays (host lists widx, gidx, gmode)."""
+    W, F2, d = w_gate_up.shape
+    F = F2 // 2
+    G = dw_gate_up.shape[0]
+    wi, gi, gm = _host_list(widx), _host_list(gidx), _host_list(gmode)
+    check(_lib.load().foremoe_copy_in(_ptr(buf), buf.numel(), len(wi), wi.ctypes.data, gi.ctypes.data,
+                                      gm.ctypes.data, what, _ptr(w_gate_up), _ptr(w_down), _dt(w_gate_up), W,
+                                      _ptr(dw_gate_up), _ptr(dw_down), G, d, F, _stream(buf.device)),
+          "foremoe_copy_in")
+
+
+def plan_prefetch(resident, needed):
+    """(slot_of [n], fetch_expert [m], fetch_widx [m]) from the host planner."""
+    res, need = _host_list(resident), _host_list(needed)
+    n = len(need)
+    slot_of = np.empty(max(n, 1), dtype=np.int32)
+    fe = np.empty(max(n, 1), dtype=np.int32)
+    fw = np.empty(max(n, 1), dtype=np.int32)
+    nf = ctypes.c_int32(0)
+    check(_lib.load().foremoe_plan_prefetch(res.ctypes.data, len(res), need.ctypes.data, n, slot_of.ctypes.data,
+                                            fe.ctypes.data, fw.ctypes.data, ctypes.byref(nf)),
+          "foremoe_plan_prefetch")
+    return slot_of[:n].copy(), fe[:nf.value].copy(), fw[:nf.value].copy()
+
+
+def prefetch_experts(host_gate_up: torch.Tensor, host_down: torch.Tensor, expert, widx, w_gate_up: torch.Tensor,
+                     w_down: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Host-to-device copies of experts from the pinned host master copy into
+    weight slots, queued on ``stream`` (default: the current stream)."""
+    if host_gate_up.is_cuda or host_down.is_cuda:
+        raise ValueError("the master copy lives in host memory")
+    E, F2, d = host_gate_up.shape
+    W = w_gate_up.shape[0]
+    ex, wi = _host_list(expert), _host_list(widx)
+    st = (stream or torch.cuda.current_stream(w_gate_up.device)).cuda_stream
+    check(_lib.load().foremoe_prefetch_experts(host_gate_up.data_ptr(), host_down.data_ptr(), E, _dt(host_gate_up),
+                                               d, F2 // 2, len(ex), ex.ctypes.data, wi.ctypes.data, _ptr(w_gate_up),
+                                               _ptr(w_down), W, st), "foremoe_prefetch_experts")
+
+
+# ---------------------------------------------------------------------------
 # Placement planner (host arrays; see include/foremoe.h)
 # ---------------------------------------------------------------------------
 def _machine(M: int, R: int, N_b: int, N_r: int) -> _lib.Machine:
