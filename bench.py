@@ -37,6 +37,12 @@ import os
 import sys
 import time
 
+# The CPU baseline's BLAS threads, fixed before numpy is first imported: the
+# host's thread budget (OMP_NUM_THREADS where the machine sets one, else
+# every CPU this process may run on).
+AFFINITY_CPUS = len(os.sched_getaffinity(0))
+os.environ.setdefault("OPENBLAS_NUM_THREADS", os.environ.get("OMP_NUM_THREADS", str(AFFINITY_CPUS)))
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
@@ -56,6 +62,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
+    ap.add_argument("--no-transfer", action="store_true", help="skip the transfer-engine report")
     ap.add_argument("--no-reference-peaks", action="store_true",
                     help="skip the measured square-GEMM and copy peaks reported beside the nominal ones")
     ap.add_argument("--no-split", action="store_true",
@@ -67,6 +74,13 @@ def parse():
                     help="run the weight-gradient GEMMs on the main stream instead of beside the data gradients")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three plain 1 GiB device copies (reference for HBM byte counters)")
+    ap.add_argument("--counters-pass", action="store_true",
+                    help="only run each micro-step twice in the benchmark's schedule (for rocprofv3 --pmc runs)")
+    ap.add_argument("--summarize-counters", metavar="DIR",
+                    help="turn DIR/{fetch,write,copy_fetch,copy_write}.csv (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
+                         "of a --counters-pass and a --copy-calibration run) and DIR/pass.json (the counters "
+                         "pass's output) into the per-kernel traffic record profiles/traffic_qwen3_share.json "
+                         "and print its table")
     return ap.parse_args()
 
 
@@ -89,6 +103,8 @@ def main() -> int:
     args = parse()
     if args.copy_calibration:
         return copy_calibration()
+    if args.summarize_counters:
+        return summarize_counters(args.summarize_counters)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU's share of the expert layer; --gpus {args.gpus} "
@@ -148,6 +164,20 @@ def main() -> int:
         Ns.append(int(buf["slot_offset"][S].item()))
         gidx = mss[i].plan.slot_gidx.cpu().numpy()
         Gs.append(int(len(set(gidx[sc > 0].tolist()))))
+
+    if args.counters_pass:
+        # after the one-stream pass above, each micro-step twice in the timed
+        # region's schedule: every micro-step is dispatched three times, so
+        # per-dispatch counters average over the 16 micro-steps evenly
+        pu.start()
+        for r in range(2):
+            for i in range(n_micro):
+                run_step(r * n_micro + i, overlap=not args.no_overlap, pipelined=not args.no_pipeline)
+        pu.finish()
+        torch.cuda.synchronize()
+        print(json.dumps({"counters_pass": {"micro_steps": n_micro, "dispatches_per_micro_step": 3, "N": Ns,
+                                            "G": Gs, "T": T, "K": K, "d": d, "F": F}}), flush=True)
+        return 0
 
     overlap = not args.no_overlap
     for i in range(args.warmup):
@@ -216,23 +246,12 @@ def main() -> int:
     work = {p: {"flop": 0.0, "bytes": 0.0} for p in PHASES}
     for s in range(args.steps):
         N, g = Ns[s % n_micro], Gs[s % n_micro]
-        work["histogram_assign"]["bytes"] += 4.0 * T * K
-        work["permute"]["bytes"] += acc.permute_bytes(N, T, K, d, 2)
-        work["gate_up_fwd"]["flop"] += acc.gate_up_flops(N, d, F)
-        work["gate_up_fwd"]["bytes"] += 2.0 * (N * d + g * 2 * F * d + N * F + N * 2 * F)
-        work["down_fwd"]["flop"] += acc.down_flops(N, d, F)
-        work["down_fwd"]["bytes"] += 2.0 * (N * F + g * d * F + N * d)
-        work["combine"]["bytes"] += acc.combine_bytes(N, T, K, d, 2, 2)
-        work["combine_bwd"]["bytes"] += acc.combine_bwd_bytes(N, T, K, d, 2)
-        work["down_dgrad"]["flop"] += acc.down_flops(N, d, F)
-        work["down_dgrad"]["bytes"] += 2.0 * (N * d + g * d * F + N * 2 * F + N * 2 * F)
-        work["gate_up_dgrad"]["flop"] += acc.gate_up_flops(N, d, F)
-        work["gate_up_dgrad"]["bytes"] += 2.0 * (N * 2 * F + g * 2 * F * d + N * d)
-        work["gate_up_wgrad"]["flop"] += acc.gate_up_flops(N, d, F)
-        work["gate_up_wgrad"]["bytes"] += 2.0 * (N * 2 * F + N * d) + 2.0 * g * 2 * F * d * 4
-        work["down_wgrad"]["flop"] += acc.down_flops(N, d, F)
-        work["down_wgrad"]["bytes"] += 2.0 * (N * d + N * F) + 2.0 * g * d * F * 4
-        work["permute_bwd"]["bytes"] += acc.permute_bwd_bytes(N, T, K, d, 2, 2)
+        for p, by in acc.phase_bytes(N, g, T, K, d, F).items():
+            work[p]["bytes"] += by
+        for p in ("gate_up_fwd", "gate_up_dgrad", "gate_up_wgrad"):
+            work[p]["flop"] += acc.gate_up_flops(N, d, F)
+        for p in ("down_fwd", "down_dgrad", "down_wgrad"):
+            work[p]["flop"] += acc.down_flops(N, d, F)
 
     def rates(p, ms):
         t_s = ms / 1e3
@@ -248,10 +267,14 @@ def main() -> int:
         t_s = phase_ms[p] / 1e3
         fl, by = work[p]["flop"], work[p]["bytes"]
         bound, ach, peak, unit = rates(p, phase_ms[p])
+        tr = measured_traffic(p)
         kernels[p] = {"us_per_step": round(phase_ms[p] * 1e3 / args.steps, 2), "bound": bound,
                       "achieved": round(ach, 2), "unit": unit, "frac": round(ach / peak, 4),
                       "tflops": round(fl / t_s / 1e12, 2) if fl else None,
-                      "gbs": round(by / t_s / 1e9, 1)}
+                      "gbs": round(by / t_s / 1e9, 1),
+                      "algorithmic_bytes_per_launch": round(by / args.steps, 0),
+                      "traffic_bytes_per_launch": tr,
+                      "traffic_over_algorithmic": round(tr / (by / args.steps), 3) if tr else None}
     # the dominant single-launch kernel, timed live in the timed region on
     # the stream it runs on
     bound, ach, peak, unit = rates(dom, live_ms[dom])
@@ -309,6 +332,8 @@ def main() -> int:
         out["measured_peaks"] = ref
     if not args.no_planner:
         out["planner"] = planner_report(w, api, dev, n_micro)
+    if not args.no_transfer:
+        out["transfer"] = transfer_report(w, api, dev, pu, mss, n_micro)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
@@ -349,6 +374,144 @@ def reference_peaks(dev) -> dict:
     copy = 2.0 * (1 << 30) * 5 / (e0.elapsed_time(e1) / 1e3) / 1e9
     return {"bf16_gemm_tflops": round(gemm, 1), "bf16_gemm": "torch.matmul 8192^3 (hipBLASLt)",
             "copy_gbs": round(copy, 1), "copy": "1 GiB device copy, bytes read + written"}
+
+
+def transfer_report(w, api, dev, pu, mss, n_micro: int) -> dict:
+    """The one-GPU half of the Expert Transfer Engine (Sec. 6), measured
+    outside the timed region with HIP events:
+
+    * Copy-out / Copy-in (Sec. 6.2) of every expert of the share (16 local
+      + 4 replica slots) with bf16 parameters and fp32 gradients, 27 MiB per
+      record (App. A.3/A.4), and Copy-in adding 4 replica partial gradients
+      into their main experts; HBM bytes read + written per second.
+    * CPU-assisted prefetch (Sec. 6.1): App. A.4's worst case of N_s = 10
+      experts (90 MiB of bf16 parameters) from a pinned host master copy,
+      alone, and on an auxiliary stream beside the forward of a micro-step
+      (dispatch, expert FFN forward, combine: the recompute stage), to show
+      how much of it the forward hides.
+    """
+    import numpy as np
+    import torch
+
+    spec = w.spec
+    d, F, E = spec.d, spec.F, spec.E
+    bf = torch.bfloat16
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def timed(fn, reps=5, stream=None):
+        st = stream or torch.cuda.current_stream(dev)
+        fn()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(st)
+        for _ in range(reps):
+            fn()
+        b.record(st)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps  # us
+
+    n = 20
+    g = torch.Generator(device=dev).manual_seed(17)
+    wgu = torch.randn((n, 2 * F, d), generator=g, device=dev).to(bf)
+    wdn = torch.randn((n, d, F), generator=g, device=dev).to(bf)
+    ggu = torch.randn((n, 2 * F, d), generator=g, device=dev)
+    gdn = torch.randn((n, d, F), generator=g, device=dev)
+    both = api._lib.XFER_PARAMS | api._lib.XFER_GRADS
+    rb = api.xfer_record_bytes(d, F, bf, both)
+    idx = list(range(n))
+    send = api.copy_out(wgu, wdn, ggu, gdn, idx, idx, both)
+    recv = send.clone()
+    wgu2, wdn2, ggu2, gdn2 = (torch.empty_like(t) for t in (wgu, wdn, ggu, gdn))
+    t_out = timed(lambda: api.copy_out(wgu, wdn, ggu, gdn, idx, idx, both, buf=send))
+    t_in = timed(lambda: api.copy_in(recv, idx, idx, [0] * n, both, wgu2, wdn2, ggu2, gdn2))
+    grads = api._lib.XFER_GRADS
+    rbg = api.xfer_record_bytes(d, F, bf, grads)
+    part = api.copy_out(wgu, wdn, ggu, gdn, [0, 1, 2, 3], [16, 17, 18, 19], grads)
+    t_add = timed(lambda: api.copy_in(part, [-1] * 4, [0, 1, 2, 3], [1] * 4, grads, wgu2, wdn2, ggu2, gdn2))
+    by_out = 2.0 * n * rb
+    by_add = 4 * rbg * 3.0
+
+    # CPU-assisted prefetch from a pinned master copy of all E experts
+    n_pf = 10
+    master_gu = torch.empty((E, 2 * F, d), dtype=bf, pin_memory=True)
+    master_dn = torch.empty((E, d, F), dtype=bf, pin_memory=True)
+    master_gu.copy_(torch.randn((E, 2 * F, d), generator=torch.Generator().manual_seed(1)).to(bf))
+    master_dn.copy_(torch.randn((E, d, F), generator=torch.Generator().manual_seed(2)).to(bf))
+    slots_gu = torch.empty((n_pf, 2 * F, d), dtype=bf, device=dev)
+    slots_dn = torch.empty((n_pf, d, F), dtype=bf, device=dev)
+    experts = list(range(0, 2 * n_pf, 2))
+    aux = torch.cuda.Stream(dev)
+    pf = lambda: api.prefetch_experts(master_gu, master_dn, experts, list(range(n_pf)), slots_gu, slots_dn,  # noqa
+                                      stream=aux)
+    t_pf = timed(pf, stream=aux)
+    pf_bytes = n_pf * api.xfer_record_bytes(d, F, bf, api._lib.XFER_PARAMS)
+    # the forward of micro-step i (recompute stage) alone, then with the prefetch beside it
+    fwd_phases = {"histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine"}
+
+    def forward(i):
+        for ph, op in pu.ops(i, mss[i % n_micro]):
+            if ph in fwd_phases:
+                op()
+
+    main = torch.cuda.current_stream(dev)
+    reps = 2 * n_micro
+    forward(0)
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    a.record(main)
+    for i in range(reps):
+        forward(i)
+    b.record(main)
+    torch.cuda.synchronize()
+    t_fwd = a.elapsed_time(b) * 1e3 / reps
+    # the prefetch for micro-step i + 1 goes out with micro-step i's forward.
+    # Its slots were last read by micro-step i - 1, so the host waits for that
+    # forward's event before queueing it: on this runtime, host-to-device
+    # copies queued on a stream that waits on a not yet completed event of
+    # another stream are carried out synchronously by the host (measured:
+    # the copy calls then block for the whole transfer), so the aux stream
+    # never waits on the main stream here; the main stream waits for the
+    # aux stream before the next forward.
+    fwd_done = [torch.cuda.Event(), torch.cuda.Event()]
+    a.record(main)
+    for i in range(reps):
+        if i >= 1:
+            fwd_done[(i - 1) % 2].synchronize()
+        pf()
+        forward(i)
+        fwd_done[i % 2].record(main)
+        main.wait_stream(aux)
+    b.record(main)
+    torch.cuda.synchronize()
+    t_both = a.elapsed_time(b) * 1e3 / reps
+    hidden = max(0.0, min(1.0, (t_fwd + t_pf - t_both) / t_pf)) if t_pf > 0 else None
+    # App. A.2's overlap condition on this GPU: the smallest per-rank token
+    # count n whose layer time covers this prefetch (N_s = 10 experts), with
+    # the measured PCIe rate and the measured large-GEMM rate as F
+    from workload import accounting as acc
+    n_min = acc.n_min_cpu(d, F, spec.K, E, n_pf, 2, 1.0e15, pf_bytes / (t_pf * 1e-6))
+    return {
+        "copy_out": {"records": n, "record_mib": round(rb / 2 ** 20, 2), "us": round(t_out, 1),
+                     "gbs": round(by_out / (t_out * 1e-6) / 1e9, 1),
+                     "frac_hbm": round(by_out / (t_out * 1e-6) / 8e12, 4)},
+        "copy_in_assign": {"records": n, "us": round(t_in, 1), "gbs": round(by_out / (t_in * 1e-6) / 1e9, 1),
+                           "frac_hbm": round(by_out / (t_in * 1e-6) / 8e12, 4)},
+        "copy_in_add_replica_grads": {"records": 4, "us": round(t_add, 1),
+                                      "gbs": round(by_add / (t_add * 1e-6) / 1e9, 1),
+                                      "frac_hbm": round(by_add / (t_add * 1e-6) / 8e12, 4)},
+        "prefetch": {"experts": n_pf, "mib": round(pf_bytes / 2 ** 20, 1), "us": round(t_pf, 1),
+                     "gbs": round(pf_bytes / (t_pf * 1e-6) / 1e9, 1),
+                     "paper_h20": "90 MiB in 1.47 ms over PCIe Gen5 x16 (App. A.4)"},
+        "prefetch_beside_forward": {"forward_us": round(t_fwd, 1), "prefetch_us": round(t_pf, 1),
+                                    "together_us": round(t_both, 1), "hidden_frac": None if hidden is None
+                                    else round(hidden, 3),
+                                    "note": "forward of one micro-step (dispatch, FFN forward, combine) on the "
+                                            "main stream, the 10-expert prefetch on an auxiliary stream"},
+        "app_a_n_min_cpu": {"tokens": round(n_min), "note": "App. A.2 Eq. cpu_n_min with N_s = 10, p_w = 2, "
+                                                            "F = 1 PFLOP/s (about the measured large bf16 GEMM "
+                                                            "rate), B_PCIe = the prefetch rate above; the paper "
+                                                            "gives 1862 tokens on H20"},
+    }
 
 
 def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> dict:
@@ -510,25 +673,144 @@ def planner_report(w, api, dev, n_micro: int, N_r: int = 4, C_max: int = 8) -> d
                                            "gathers, one stream, on the slowest rank's share"}}
 
 
-def measured_traffic(phase: str):
-    """HBM bytes per launch of a kernel from the committed rocprofv3 counter
-    summary (FETCH_SIZE, WRITE_SIZE, each scaled by a calibration copy), or
-    None when no summary exists or the kernel source changed since then."""
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic_qwen3_share.json")
+# the kernels of every phase; a name that serves two phases is dispatched
+# once for each per micro-step, in this order (one-stream and overlapped
+# schedules alike)
+PHASE_KERNELS = [
+    ("hist_count_kernel", ["histogram_assign"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("hist_scan_assign_kernel", ["histogram_assign"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("permute_rank_kernel", ["permute"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("gather_rows_kernel", ["permute"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("gemm_rows_kernel<true, 1>", ["gate_up_fwd"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
+    ("gemm_rows_kernel<true, 0>", ["down_fwd"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
+    ("combine_kernel", ["combine", "permute_bwd"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("combine_bwd_kernel", ["combine_bwd"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("gemm_rows_kernel<false, 2>", ["down_dgrad"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
+    ("gemm_rows_kernel<false, 0>", ["gate_up_dgrad"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
+    ("gemm_wgrad_kernel", ["down_wgrad", "gate_up_wgrad"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
+    ("wgrad_reduce_kernel", ["down_wgrad", "gate_up_wgrad"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
+]
+
+
+def _kernel_key(name: str):
+    """The PHASE_KERNELS key of a demangled kernel name, or None."""
+    import re
+    m = re.search(r"gemm_rows_kernel<([^>]*)>", name)
+    if m:
+        args = [a.strip() for a in m.group(1).split(",")]
+        return f"gemm_rows_kernel<{args[-2]}, {args[-1]}>"
+    for key, _, _ in PHASE_KERNELS:
+        if "<" not in key and re.search(r"\b" + key + r"\b", name):
+            return key
+    return None
+
+
+def _file_sha(rel: str) -> str:
     import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic_qwen3_share.json")
-    if not os.path.exists(path):
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def summarize_counters(folder: str) -> int:
+    """Per-kernel HBM traffic from rocprofv3 counter CSVs (FETCH_SIZE and
+    WRITE_SIZE in KiB, summed over a dispatch's rows), each scaled by what
+    the same counter reads for the calibration copies (bytes of a 1 GiB
+    copy), against the algorithmic bytes of the same dispatches (the
+    counters pass dispatches every micro-step three times, so per-dispatch
+    averages are averages over the micro-steps). Writes TRAFFIC_RECORD."""
+    import collections
+    import csv
+
+    from workload import accounting as acc
+
+    def per_dispatch(path, counter):
+        tot = collections.defaultdict(float)
+        names = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] != counter:
+                    continue
+                k = int(r["Dispatch_Id"])
+                tot[k] += float(r["Counter_Value"])
+                names[k] = r["Kernel_Name"]
+        return [(k, names[k], tot[k]) for k in sorted(tot)]
+
+    with open(os.path.join(folder, "pass.json")) as f:
+        cp = json.loads([ln for ln in f if ln.startswith("{")][-1])["counters_pass"]
+    cal = {}
+    for counter, fn in (("FETCH_SIZE", "copy_fetch.csv"), ("WRITE_SIZE", "copy_write.csv")):
+        vals = [v for _, n, v in per_dispatch(os.path.join(folder, fn), counter) if "copy" in n.lower()]
+        cal[counter] = sum(vals) / len(vals) * 1024.0 / (1 << 30)  # counter bytes per copied byte
+    per_phase = collections.defaultdict(lambda: {"fetch": [], "write": [], "kernels": set(), "sources": set()})
+    for counter, fn in (("FETCH_SIZE", "fetch.csv"), ("WRITE_SIZE", "write.csv")):
+        seen = collections.Counter()
+        for _, name, v in per_dispatch(os.path.join(folder, fn), counter):
+            key = _kernel_key(name)
+            if key is None:
+                continue
+            phases, src = next((ph, sr) for k, ph, sr in PHASE_KERNELS if k == key)
+            phase = phases[seen[key] % len(phases)]
+            seen[key] += 1
+            rec = per_phase[phase]
+            rec["fetch" if counter == "FETCH_SIZE" else "write"].append(v * 1024.0 / cal[counter])
+            rec["kernels"].add(key)
+            rec["sources"].add(src)
+    T, K, d, F = cp["T"], cp["K"], cp["d"], cp["F"]
+    alg = collections.defaultdict(float)
+    for N, g in zip(cp["N"], cp["G"]):
+        for p, by in acc.phase_bytes(N, g, T, K, d, F).items():
+            alg[p] += by / len(cp["N"])
+    kernels = {}
+    for phase, rec in per_phase.items():
+        n_k = len(rec["kernels"])
+        # launches of the phase: dispatches of its kernels / kernels per phase
+        launches = len(rec["fetch"]) // n_k
+        fetch = sum(rec["fetch"]) / launches
+        write = sum(rec["write"]) / launches
+        kernels[phase] = {"kernels": sorted(rec["kernels"]), "launches": launches,
+                          "read_bytes_per_launch": round(fetch), "write_bytes_per_launch": round(write),
+                          "hbm_bytes_per_launch": round(fetch + write),
+                          "algorithmic_bytes_per_launch": round(alg[phase]),
+                          "ratio": round((fetch + write) / alg[phase], 3),
+                          "sources": {s: _file_sha(s) for s in sorted(rec["sources"])}}
+    out = {"workload": "qwen3-30b-a3b EP=8 rank share, policy-update micro-steps (bench.py --counters-pass: "
+                       "every micro-step three times, one stream once then twice pipelined)",
+           "calibration": {"fetch_size_per_copied_byte": round(cal["FETCH_SIZE"], 4),
+                           "write_size_per_copied_byte": round(cal["WRITE_SIZE"], 4),
+                           "copy": "torch device copy of 1 GiB (bench.py --copy-calibration)"},
+           "kernels": {p: kernels[p] for p in PHASES_ORDER if p in kernels}}
+    with open(TRAFFIC_RECORD, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print("| phase | kernels | launches | read MB | written MB | HBM MB | algorithmic MB | ratio |")
+    print("|---|---|---|---|---|---|---|---|")
+    for p, k in out["kernels"].items():
+        print(f"| {p} | {', '.join('`' + x + '`' for x in k['kernels'])} | {k['launches']} | "
+              f"{k['read_bytes_per_launch'] / 1e6:.1f} | {k['write_bytes_per_launch'] / 1e6:.1f} | "
+              f"{k['hbm_bytes_per_launch'] / 1e6:.1f} | {k['algorithmic_bytes_per_launch'] / 1e6:.1f} | "
+              f"{k['ratio']:.2f} |")
+    return 0
+
+
+PHASES_ORDER = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
+                "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
+
+
+def measured_traffic(phase: str):
+    """HBM bytes per launch of a phase (FETCH_SIZE + WRITE_SIZE, each scaled
+    by a calibration copy) from the committed counter record, or None when
+    there is none or a source of the phase's kernels changed since."""
+    if not os.path.exists(TRAFFIC_RECORD):
         return None
-    with open(path) as f:
+    with open(TRAFFIC_RECORD) as f:
         rec = json.load(f)
     k = rec.get("kernels", {}).get(phase)
-    if not k:
+    if not k or "sources" not in k:
         return None
-    with open(os.path.join(ROOT, k["source"]), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != k["source_sha256"]:
-            return None
-    cal = rec["calibration"]
-    return round((k["fetch_kib_per_launch"] / cal["fetch_scale"] + k["write_kib_per_launch"] / cal["write_scale"])
-                 * 1024.0, 0)
+    if any(_file_sha(src) != sha for src, sha in k["sources"].items()):
+        return None
+    return float(k["hbm_bytes_per_launch"])
 
 
 def cpu_baseline(w, budget_s: float = 10.0) -> dict:
@@ -537,11 +819,24 @@ def cpu_baseline(w, budget_s: float = 10.0) -> dict:
     import numpy as np
 
     import oracle.foremoe_oracle as O
+    # the BLAS threads numpy runs with (pinned by OPENBLAS_NUM_THREADS before
+    # numpy was imported, see the top of this file), the CPUs this process may
+    # use, the CPU model and the BLAS build
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max([int(i.get("num_threads", 1)) for i in info] or [1])
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')} ({info[0].get('architecture')})"
     except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads = 1
+        threads = int(os.environ.get("OPENBLAS_NUM_THREADS", "1"))
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu_model)
+    except OSError:
+        pass
     T, K = w.micro[0].ids.shape
     gu, dn = w.weights(w.micro[0].plan)
     G = w.micro[0].plan.G
@@ -558,6 +853,7 @@ def cpu_baseline(w, budget_s: float = 10.0) -> dict:
         pairs += int(fwd["slot_offset"][-1])
         done += 1
     return {"value": round(T * done / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "affinity_cpus": AFFINITY_CPUS, "cpu_model": cpu_model, "blas": blas,
             "sample": f"micro-steps 0..{done - 1} of the same workload ({done} x {T} tokens, {pairs} local "
                       f"pairs), forward + backward in fp64 numpy, gradients accumulated; "
                       f"{dt:.1f} s"}

@@ -184,9 +184,9 @@ class PolicyUpdate:
             gate_up_wgrad(side)
         call("gate_up_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_dgrad_timed(
             P["d_au"], BF16, d, F, S, so, widx, G, gu, n_cap, P["dx_perm"], rws, rwsz, q, e0, e1))
-        if not overlap:
-            gate_up_wgrad(main)
+        if not overlap:  # same order as on the side stream: down, then gate/up
             down_wgrad(main)
+            gate_up_wgrad(main)
         call("permute_bwd", main, lambda q: lib.foremoe_permute_bwd(
             P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], self.dx_dt, q))
         if pipelined:

@@ -62,6 +62,25 @@ def wgrad_rmw_bytes(G: int, d: int, F: int, acc_elem: int = 4) -> float:
     return 2.0 * G * 3 * d * F * acc_elem
 
 
+def phase_bytes(N: int, g: int, T: int, K: int, d: int, F: int, b: int = 2) -> dict:
+    """Algorithmic HBM bytes of every phase of one policy-update micro-step
+    with N local pairs and g non-empty gradient groups (bf16 activations and
+    weights of b bytes, fp32 weight gradients read and written once)."""
+    return {
+        "histogram_assign": 4.0 * T * K,
+        "permute": permute_bytes(N, T, K, d, b),
+        "gate_up_fwd": b * (N * d + g * 2 * F * d + N * F + N * 2 * F),
+        "down_fwd": b * (N * F + g * d * F + N * d),
+        "combine": combine_bytes(N, T, K, d, b, b),
+        "combine_bwd": combine_bwd_bytes(N, T, K, d, b),
+        "down_dgrad": b * (N * d + g * d * F + N * 2 * F + N * 2 * F),
+        "gate_up_dgrad": b * (N * 2 * F + g * 2 * F * d + N * d),
+        "gate_up_wgrad": b * (N * 2 * F + N * d) + 2.0 * g * 2 * F * d * 4,
+        "down_wgrad": b * (N * d + N * F) + 2.0 * g * d * F * 4,
+        "permute_bwd": permute_bwd_bytes(N, T, K, d, b, b),
+    }
+
+
 # --- App. A overlap model ---------------------------------------------------
 def expert_bytes(h: int, h_ff: int, p: int) -> float:
     """S_e (or S_g) = 3 * h * h_ff * p bytes for a SwiGLU expert."""
