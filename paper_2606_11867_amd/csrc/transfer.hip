@@ -9,8 +9,9 @@
 // into their weight slots, gradients either moved into a slot (assign) or
 // accumulated into the main expert's gradient (add; Sec. 6.2), records that
 // name one gradient applied in record order in fp32, so the result is
-// deterministic. Both kernels are HBM-bound copies moving 16-byte vectors;
-// every record boundary and part boundary is a multiple of 16 bytes.
+// deterministic. Both kernels are HBM-bound copies moving 16-byte vectors
+// with the nontemporal hint (the data streams through once); every record
+// boundary and part boundary is a multiple of 16 bytes.
 //
 // The prefetch is a host-to-device DMA (hipMemcpyAsync on the caller's
 // stream) straight into the weight slots: no kernel and no GPU buffer.
@@ -80,8 +81,8 @@ __global__ __launch_bounds__(kXferThreads) void copy_out_kernel(RecordParts rp, 
     for (int u = 0; u < kXferVecPerThread; ++u) {
       const uint64_t v = v0 + (uint64_t)u * kXferThreads;
       if (v < nvec)
-        a[u] = *reinterpret_cast<const u32x4*>(part_addr(rp, v * 16, r, rec, (char*)wgu, (char*)wdn, (char*)ggu,
-                                                         (char*)gdn));
+        a[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+            part_addr(rp, v * 16, r, rec, (char*)wgu, (char*)wdn, (char*)ggu, (char*)gdn)));
     }
 #pragma unroll
     for (int u = 0; u < kXferVecPerThread; ++u) {
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(kXferThreads) void copy_in_kernel(RecordParts rp, X
         const uint64_t off = v * 16;
         char* dst = off < rp.gu_p ? wgu + (uint64_t)rec.widx[r] * rp.gu_p + off
                                   : wdn + (uint64_t)rec.widx[r] * rp.dn_p + (off - rp.gu_p);
-        *reinterpret_cast<u32x4*>(dst) = a[u];
+        __builtin_nontemporal_store(a[u], reinterpret_cast<u32x4*>(dst));
       }
     }
     return;
