@@ -63,6 +63,8 @@ def parse():
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
     ap.add_argument("--no-transfer", action="store_true", help="skip the transfer-engine report")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the per-phase report of the Mixtral-8x7B and DeepSeek-V3 rank shares")
     ap.add_argument("--no-reference-peaks", action="store_true",
                     help="skip the measured square-GEMM and copy peaks reported beside the nominal ones")
     ap.add_argument("--no-split", action="store_true",
@@ -334,6 +336,11 @@ def main() -> int:
         out["planner"] = planner_report(w, api, dev, n_micro)
     if not args.no_transfer:
         out["transfer"] = transfer_report(w, api, dev, pu, mss, n_micro)
+    if not args.no_other_configs:
+        del pu, mss, buf
+        torch.cuda.empty_cache()
+        out["other_configs"] = {name: config_report(name, api, dev)
+                                for name in ("mixtral-8x7b-share", "deepseek-v3-ep32-share")}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
@@ -374,6 +381,89 @@ def reference_peaks(dev) -> dict:
     copy = 2.0 * (1 << 30) * 5 / (e0.elapsed_time(e1) / 1e3) / 1e9
     return {"bf16_gemm_tflops": round(gemm, 1), "bf16_gemm": "torch.matmul 8192^3 (hipBLASLt)",
             "copy_gbs": round(copy, 1), "copy": "1 GiB device copy, bytes read + written"}
+
+
+def config_report(name: str, api, dev, reps: int = 5) -> dict:
+    """One micro-step of another rank share (its measured micro-step: the one
+    whose local pair count is closest to the share's nominal T * K / P),
+    forward and backward, every phase on one stream between HIP events,
+    averaged over `reps` runs after a warm-up. Routing and the slot table come
+    from the seeded generator; activations, upstream gradients and weights are
+    drawn on the device (N(0,1), N(0, 1/fan_in)): values do not change the
+    work. Rates are against the same algorithmic work as the main line."""
+    import numpy as np
+    import torch
+
+    from paper_2606_11867_amd.policy_update import PHASES, MicroStep, PolicyUpdate
+    from workload import accounting as acc
+    from workload import make_workload
+
+    w = make_workload(name)
+    spec = w.spec
+    T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
+    m = w.micro[w.measured]
+    bf = torch.bfloat16
+    g = torch.Generator(device=dev).manual_seed(23)
+    G = int(m.plan.G)
+    gu = (torch.randn((m.plan.W, 2 * F, d), generator=g, device=dev) / d ** 0.5).to(bf)
+    dn = (torch.randn((m.plan.W, d, F), generator=g, device=dev) / F ** 0.5).to(bf)
+    ms = MicroStep(ids=torch.from_numpy(m.ids).to(dev), gates=torch.from_numpy(m.gates).to(dev),
+                   x=torch.randn((T, d), generator=g, device=dev).to(bf),
+                   dy=torch.randn((T, d), generator=g, device=dev).to(bf),
+                   plan=api.DevicePlan.from_host(m.plan, dev))
+    n_cap = int(w.stats.get("local_pairs_max", T * K))
+    pu = PolicyUpdate(T, K, d, F, E, G, m.plan.S, gu, dn, dev, n_cap=n_cap)
+    pu.run(0, ms)
+    torch.cuda.synchronize()
+    st = pu.set_of(0, False)
+    N = int(st["slot_offset"][m.plan.S].item())
+    sc = st["slot_count"][:m.plan.S].cpu().numpy()
+    gidx = m.plan.slot_gidx
+    gn = int(len(set(np.asarray(gidx)[sc > 0].tolist())))
+    evs = []
+    for _ in range(reps):
+        ev = {p: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for p in PHASES}
+        for a, b in ev.values():
+            a.record(pu.main)
+            b.record(pu.main)
+        evs.append(ev)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(pu.main)
+    for ev in evs:
+        pu.run(0, ms, ev)
+    t1.record(pu.main)
+    torch.cuda.synchronize()
+    step_us = t0.elapsed_time(t1) * 1e3 / reps
+    by = acc.phase_bytes(N, gn, T, K, d, F)
+    fl = {p: 0.0 for p in PHASES}
+    for p in ("gate_up_fwd", "gate_up_dgrad", "gate_up_wgrad"):
+        fl[p] = acc.gate_up_flops(N, d, F)
+    for p in ("down_fwd", "down_dgrad", "down_wgrad"):
+        fl[p] = acc.down_flops(N, d, F)
+    phases = {}
+    for p in PHASES:
+        us = sum(ev[p][0].elapsed_time(ev[p][1]) for ev in evs) * 1e3 / reps
+        e = {"us": round(us, 2), "gbs": round(by[p] / (us * 1e-6) / 1e9, 1),
+             "hbm_frac": round(by[p] / (us * 1e-6) / acc.PEAK_HBM_BYTES_PER_S, 4)}
+        if fl[p]:
+            e["tflops"] = round(fl[p] / (us * 1e-6) / 1e12, 1)
+            e["mfma_frac"] = round(fl[p] / (us * 1e-6) / acc.PEAK_BF16_DENSE_FLOPS, 4)
+        phases[p] = e
+    ffn = ["gate_up_fwd", "down_fwd", "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad"]
+    ffn_us = sum(phases[p]["us"] for p in ffn)
+    ffn_fl = sum(fl[p] for p in ffn)
+    out = {"micro_step": int(w.measured), "T": T, "d": d, "F": F, "E": E, "K": K, "slots": int(m.plan.S),
+           "n_pairs": N, "slot_counts": sorted((int(c) for c in sc), reverse=True),
+           "us_per_micro_step_one_stream": round(step_us, 1),
+           "tokens_per_s_one_stream": round(T / (step_us * 1e-6), 1),
+           "grouped_ffn_tflops": round(ffn_fl / (ffn_us * 1e-6) / 1e12, 1),
+           "grouped_ffn_frac_bf16_peak": round(ffn_fl / (ffn_us * 1e-6) / acc.PEAK_BF16_DENSE_FLOPS, 4),
+           "phases": phases,
+           "data": "routing from the seeded generator; activations, gradients and weights drawn on the device"}
+    del pu, ms, gu, dn
+    torch.cuda.empty_cache()
+    return out
 
 
 def transfer_report(w, api, dev, pu, mss, n_micro: int) -> dict:

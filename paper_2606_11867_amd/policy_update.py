@@ -58,15 +58,16 @@ class PolicyUpdate:
     micro-step accumulates into.
 
     split: give the row GEMMs their workspace (a partial last round of tiles
-    is cut along K)."""
+    is cut along K). n_cap: rows of the permuted buffers (default T * K, every
+    pair local; a rank share needs only its largest local pair count)."""
 
     def __init__(self, T: int, K: int, d: int, F: int, E: int, G: int, S_max: int, w_gate_up: torch.Tensor,
                  w_down: torch.Tensor, device, split: bool = True, y_dtype=torch.bfloat16,
-                 dx_dtype=torch.bfloat16):
+                 dx_dtype=torch.bfloat16, n_cap: Optional[int] = None):
         self.lib = _lib.load()
         self.T, self.K, self.d, self.F, self.E, self.G = T, K, d, F, E, G
         self.dev = torch.device(device)
-        self.n_cap = T * K
+        self.n_cap = T * K if n_cap is None else int(n_cap)
         self.gu, self.dn = w_gate_up, w_down
         self.y_dt, self.dx_dt = _lib.BF16 if y_dtype == torch.bfloat16 else _lib.F32, \
             _lib.BF16 if dx_dtype == torch.bfloat16 else _lib.F32
