@@ -649,8 +649,18 @@ __device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& co
     } else if constexpr (EPI == kEpiSwigluBwd) {
       using SR = StagedRowsF32<CoreT::WN * 4>;
       const int nc = n0 + wn * CoreT::WN + SR::col_of() * 8;
-      // saved A and U of the rows this lane stores, loaded before the staging
-      // so that their latency overlaps it
+#pragma unroll
+      for (int jj = 0; jj < CoreT::NB; ++jj)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int q = g * 4;
+          SR::put4(ep, l32, jj * 32 + g * 8 + c4, core.acc[i][jj][q], core.acc[i][jj][q + 1], core.acc[i][jj][q + 2],
+                   core.acc[i][jj][q + 3]);
+        }
+      // saved A and U of the rows this lane stores, loaded once this block's
+      // accumulators are staged (their registers are free again; loaded
+      // before the staging, they made the kernel spill), overlapping the
+      // read-back of the staged dH
       uint4 xa[SR::NI], xu[SR::NI];
 #pragma unroll
       for (int it = 0; it < SR::NI; ++it) {
@@ -661,14 +671,6 @@ __device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& co
           xu[it] = *reinterpret_cast<const uint4*>(a.AU + row * a.ldau + a.F + nc);
         }
       }
-#pragma unroll
-      for (int jj = 0; jj < CoreT::NB; ++jj)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int q = g * 4;
-          SR::put4(ep, l32, jj * 32 + g * 8 + c4, core.acc[i][jj][q], core.acc[i][jj][q + 1], core.acc[i][jj][q + 2],
-                   core.acc[i][jj][q + 3]);
-        }
 #pragma unroll
       for (int it = 0; it < SR::NI; ++it) {
         const int r = SR::row_of(it);
