@@ -15,8 +15,12 @@ data-gradient GEMM that does not feed it (down wgrad beside down dgrad,
 gate/up wgrad beside gate/up dgrad), and the streams are not joined at the
 end of a micro-step: the next micro-step's dispatch and forward (which do
 not depend on this one's weight gradients) start while they run, on a
-second set of activation buffers. --no-pipeline joins the streams after
-every micro-step; --no-overlap runs all phases on one stream.
+second set of activation buffers. permute_bwd (whose output feeds nothing
+later in the micro-step) runs on the second stream too, after the gate/up
+weight gradient, so that the next micro-step's dispatch starts right after
+the gate/up dgrad. --no-pipeline joins the streams after every micro-step;
+--no-overlap runs all phases on one stream; --side-gathers 0 keeps
+permute_bwd on the main stream.
 
 All inputs are resident in HBM before timing. A first pass brackets every
 ABI call with HIP events on the stream it runs on, one kernel after
@@ -72,6 +76,9 @@ def parse():
     ap.add_argument("--no-pipeline", action="store_true",
                     help="join the two streams at the end of every micro-step instead of letting the next "
                          "micro-step's forward start while this one's weight gradients run")
+    ap.add_argument("--side-gathers", type=int, default=1, choices=(0, 1, 2),
+                    help="with overlap: run permute_bwd (1, the default), and also the combine (2), on the second "
+                         "stream; 0 keeps both on the main stream")
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the weight-gradient GEMMs on the main stream instead of beside the data gradients")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -154,7 +161,7 @@ def main() -> int:
     setup_s = time.time() - t0
 
     def run_step(i, ev=None, overlap=False, pipelined=False):
-        pu.run(i, mss[i % n_micro], ev, overlap, pipelined)
+        pu.run(i, mss[i % n_micro], ev, overlap, pipelined, args.side_gathers)
 
     # ---- realised per-micro-step sizes (read back once, outside the timed region)
     Ns, Gs = [], []
@@ -312,7 +319,7 @@ def main() -> int:
                    "micro_steps": n_micro, "n_pairs_mean": round(float(np.mean(Ns)), 1),
                    "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns)),
                    "backward_overlap": overlap, "tail_split": not args.no_split,
-                   "pipelined_micro_steps": pipelined},
+                   "pipelined_micro_steps": pipelined, "side_gathers": args.side_gathers if overlap else 0},
         "ms_per_step_sequential": round(seq_ms_per_step, 4),
         "roofline": roofline,
         "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),

@@ -21,7 +21,12 @@ Schedules:
     uses activation buffer set i % 2 and, before reusing it, the main
     stream waits for the side-stream work of micro-step i - 2, so the next
     micro-step's dispatch and forward start while this one's weight
-    gradients run.
+    gradients run;
+  * side_gathers (with overlap): permute_bwd (1), and also the combine (2),
+    move to the second stream, after the weight gradients; their outputs
+    feed nothing later in the micro-step, so the main stream goes on to the
+    next micro-step right after the gate/up dgrad. A caller reading dx (or
+    y) waits for the second stream first.
 """
 from __future__ import annotations
 
@@ -111,12 +116,14 @@ class PolicyUpdate:
         self.main.wait_stream(self.side)
 
     def ops(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
-            pipelined: bool = False) -> list:
+            pipelined: bool = False, side_gathers: int = 0) -> list:
         """The operations of micro-step i on inputs ms, in order, as (phase,
         thunk) pairs (phase None: a stream dependency). ev maps phases to
         (begin, end) torch events: row GEMMs carry theirs on the kernel
         launch, the other phases are bracketed by event records on the stream
-        the phase runs on."""
+        the phase runs on. side_gathers (with overlap): 1 runs permute_bwd,
+        2 also the combine, on the second stream (their outputs feed nothing
+        later in the micro-step)."""
         lib, main, side = self.lib, self.main, self.side
         overlap = overlap or pipelined
         bset = i % 2 if pipelined else 0
@@ -170,7 +177,9 @@ class PolicyUpdate:
             P["x_perm"], BF16, d, F, S, so, widx, G, gu, n_cap, P["h"], P["au"], rws, rwsz, q, e0, e1))
         call("down_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_down_fwd_timed(
             P["h"], BF16, d, F, S, so, widx, G, dn, n_cap, P["y_perm"], rws, rwsz, q, e0, e1))
-        call("combine", main, lambda q: lib.foremoe_combine(
+        if overlap and side_gathers >= 2:
+            dep(side, main)
+        call("combine", side if overlap and side_gathers >= 2 else main, lambda q: lib.foremoe_combine(
             P["y_perm"], BF16, P["p2r"], ms.gates.data_ptr(), T, K, d, n_cap, P["y"], self.y_dt, q))
         call("combine_bwd", main, lambda q: lib.foremoe_combine_bwd(
             ms.dy.data_ptr(), P["y_perm"], BF16, P["p2r"], ms.gates.data_ptr(), T, K, d, n_cap,
@@ -188,7 +197,9 @@ class PolicyUpdate:
         if not overlap:  # same order as on the side stream: down, then gate/up
             down_wgrad(main)
             gate_up_wgrad(main)
-        call("permute_bwd", main, lambda q: lib.foremoe_permute_bwd(
+        if overlap and side_gathers >= 1:
+            dep(side, main)
+        call("permute_bwd", side if overlap and side_gathers >= 1 else main, lambda q: lib.foremoe_permute_bwd(
             P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], self.dx_dt, q))
         if pipelined:
             ops.append((None, lambda: self.done[bset].record(side)))
@@ -197,6 +208,6 @@ class PolicyUpdate:
         return ops
 
     def run(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
-            pipelined: bool = False) -> None:
-        for _, op in self.ops(i, ms, ev, overlap, pipelined):
+            pipelined: bool = False, side_gathers: int = 0) -> None:
+        for _, op in self.ops(i, ms, ev, overlap, pipelined, side_gathers):
             op()

@@ -41,12 +41,16 @@ def test_policy_update_full_shape_matches_oracle(gpu):
     outs = []
     pu.start()
     for i, ms in enumerate(mss):
-        pu.run(i, ms, pipelined=True)
+        pu.run(i, ms, pipelined=True, side_gathers=1)
         st = pu.set_of(i, pipelined=True)
-        # copies on the main stream, after this micro-step's last main-stream
-        # kernel and before micro-step i + 2 reuses the set
-        outs.append(dict(y=st["y"].clone(), dgates=st["dgates"].clone(), dx=st["dx"].clone(),
-                         N=st["slot_offset"][ms.S].clone()))
+        # copies on the second stream, after permute_bwd (which waited for
+        # every main-stream kernel of this micro-step); the set's event is
+        # recorded again after them, so micro-step i + 2 reuses the set
+        # only once they are done
+        with torch.cuda.stream(pu.side):
+            outs.append(dict(y=st["y"].clone(), dgates=st["dgates"].clone(), dx=st["dx"].clone(),
+                             N=st["slot_offset"][ms.S].clone()))
+        pu.done[i % 2].record(pu.side)
     pu.finish()
     torch.cuda.synchronize()
     assert not pu.wws[:256].any().item() and not pu.rws[:4096].any().item(), "workspace counters not reset"
