@@ -37,6 +37,7 @@ import torch
 
 from . import _lib
 from .api import DevicePlan, ffn_workspace, wgrad_workspace, workspace
+from .hip_events import Event
 
 PHASES = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combine", "combine_bwd",
           "down_dgrad", "gate_up_dgrad", "gate_up_wgrad", "down_wgrad", "permute_bwd"]
@@ -99,7 +100,12 @@ class PolicyUpdate:
         self.rws = ffn_workspace(dev) if split else None
         self.main = torch.cuda.current_stream(dev)
         self.side = torch.cuda.Stream(dev)  # default priority, like every stream here
-        self.done = [torch.cuda.Event(), torch.cuda.Event()]  # side-stream work of the micro-step using set b
+        # stream ordering uses events without the system-scope fence (both
+        # streams are on this GPU; the fence would cost the recording stream
+        # a few microseconds per record)
+        self.done = [Event(), Event()]  # side-stream work of the micro-step using set b
+        self._dep = [Event() for _ in range(5)]  # the cross-stream dependencies of one micro-step
+        self._join = Event()
         self._ptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.sets]
 
     def set_of(self, i: int, pipelined: bool) -> Dict[str, torch.Tensor]:
@@ -113,14 +119,15 @@ class PolicyUpdate:
 
     def finish(self) -> None:
         """Join the side stream into the main stream."""
-        self.main.wait_stream(self.side)
+        self._join.record(self.side)
+        self._join.wait(self.main)
 
     def ops(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
             pipelined: bool = False, side_gathers: int = 0) -> list:
         """The operations of micro-step i on inputs ms, in order, as (phase,
         thunk) pairs (phase None: a stream dependency). ev maps phases to
-        (begin, end) torch events: row GEMMs carry theirs on the kernel
-        launch, the other phases are bracketed by event records on the stream
+        (begin, end) timing events (hip_events.Event or torch's): row GEMMs
+        carry theirs on the kernel launch, the other phases are bracketed by event records on the stream
         the phase runs on. side_gathers (with overlap): 1 runs permute_bwd,
         2 also the combine, on the second stream (their outputs feed nothing
         later in the micro-step)."""
@@ -155,8 +162,16 @@ class PolicyUpdate:
                     ev[phase][1].record(st)
             ops.append((phase, run))
 
+        n_dep = [0]
+
         def dep(waiter, on):
-            ops.append((None, lambda: waiter.wait_stream(on)))
+            e = self._dep[n_dep[0]]  # its record and the wait for it are queued back to back
+            n_dep[0] += 1
+
+            def run():
+                e.record(on)
+                e.wait(waiter)
+            ops.append((None, run))
 
         def gate_up_wgrad(st):
             call("gate_up_wgrad", st, lambda q: lib.foremoe_ffn_gate_up_wgrad(
@@ -167,7 +182,7 @@ class PolicyUpdate:
                 P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, dwdn, wws, wwsz, q))
 
         if pipelined:  # set bset was last used two micro-steps ago: its weight gradients must be done
-            ops.append((None, lambda: main.wait_event(self.done[bset])))
+            ops.append((None, lambda: self.done[bset].wait(main)))
         call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
             ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
         call("permute", main, lambda q: lib.foremoe_permute(
