@@ -76,6 +76,8 @@ def parse():
     ap.add_argument("--no-pipeline", action="store_true",
                     help="join the two streams at the end of every micro-step instead of letting the next "
                          "micro-step's forward start while this one's weight gradients run")
+    ap.add_argument("--fwd-after-side", action="store_true",
+                    help="pipelined: the gate/up forward waits for the previous micro-step's second-stream work")
     ap.add_argument("--side-gathers", type=int, default=1, choices=(0, 1, 2),
                     help="with overlap: run permute_bwd (1, the default), and also the combine (2), on the second "
                          "stream; 0 keeps both on the main stream")
@@ -162,7 +164,7 @@ def main() -> int:
     setup_s = time.time() - t0
 
     def run_step(i, ev=None, overlap=False, pipelined=False):
-        pu.run(i, mss[i % n_micro], ev, overlap, pipelined, args.side_gathers)
+        pu.run(i, mss[i % n_micro], ev, overlap, pipelined, args.side_gathers, args.fwd_after_side)
 
     # ---- realised per-micro-step sizes (read back once, outside the timed region)
     Ns, Gs = [], []

@@ -137,7 +137,8 @@ size_t foremoe_workspace_size(int64_t T, int32_t K, int32_t E);
  *         any other id outside [0, E) is invalid: skipped and counted in
  *         FOREMOE_WS_INVALID_IDS.
  * counts  [E] int32 out: counts[e] = #pairs with ids[p] == e over all T tokens.
- * Also fills the workspace with per-block partial counts used by permute.
+ * Also fills the workspace with per-block partial counts and every pair's
+ * rank within its block, both used by permute.
  * T >= 0, 1 <= K <= FOREMOE_MAX_TOPK, T*K < 2^31.
  */
 int foremoe_histogram(const int32_t* ids, int64_t T, int32_t K, int32_t E,
@@ -224,7 +225,7 @@ int foremoe_permute(const void* x, foremoe_dtype dtype, int64_t T, int32_t d,
  * every device it runs on until the process ends; the call allocates
  * nothing. Inputs whose workspace would exceed it, i.e.
  * foremoe_workspace_size(T, K, n_src * E) > FOREMOE_STATIC_SCRATCH_BYTES
- * (about 8.3 M pairs at E = 128, 1 M pairs at 1024 keys), are rejected with
+ * (about 2.7 M pairs at E = 128, 0.83 M pairs at 1024 keys), are rejected with
  * FOREMOE_EINVAL before anything is launched.
  * status  int32 [3] out or NULL: the status words FOREMOE_WS_INVALID_IDS,
  *         FOREMOE_WS_DROPPED and FOREMOE_WS_PLAN_ERRORS of the call.

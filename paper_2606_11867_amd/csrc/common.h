@@ -27,8 +27,10 @@ constexpr size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 //   [0, 256)                 int32 status words
 //   [256, +64 KiB)           rep_slot[keys * R_max]: (virtual) slot of replica (key, r) or -1
 //   [kWsVSlotOff, +4 KiB+4)  vslot_offset[S * n_src + 1]: row offsets of the virtual slots
-//   [kWsPartialOff, ...)     per-block histogram partials [NB][keys+1]; the rank
-//                            kernel turns them into exclusive block bases
+//   [kWsPartialOff, ...)     per-block histogram partials [NB][keys+1]; the scan
+//                            turns them into exclusive block bases
+//   [ws_rank_off(), ...)     uint16 rank of every pair within its block's list
+//                            of the same key [T*K] (written by the count kernel)
 constexpr size_t kWsRepSlotOff = kWsHeaderBytes;
 constexpr size_t kWsVSlotOff =
     kWsRepSlotOff + sizeof(int32_t) * (size_t)FOREMOE_MAX_EXPERTS * (size_t)FOREMOE_MAX_REPLICAS;
@@ -39,9 +41,13 @@ inline int64_t hist_blocks(int64_t npairs) {
   return nb < 1 ? 1 : nb;
 }
 
-inline size_t ws_bytes_needed(int64_t T, int32_t K, int32_t E) {
+inline size_t ws_rank_off(int64_t T, int32_t K, int32_t E) {
   const int64_t nb = hist_blocks(T * (int64_t)K);
   return align_up(kWsPartialOff + sizeof(int32_t) * (size_t)nb * (size_t)(E + 1), 256);
+}
+
+inline size_t ws_bytes_needed(int64_t T, int32_t K, int32_t E) {
+  return align_up(ws_rank_off(T, K, E) + sizeof(uint16_t) * (size_t)(T * (int64_t)K), 256);
 }
 
 // ---------------------------------------------------------------------------

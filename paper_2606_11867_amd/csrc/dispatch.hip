@@ -68,35 +68,63 @@ __device__ __forceinline__ int pair_key(int v, int64_t p, const KeyMap& km, cons
 }
 
 // ---------------------------------------------------------------------------
-// Step 1a: per-block counts of each key (bucket nkeys counts invalid ids).
+// Step 1a: per-block counts of each key (bucket nkeys counts invalid ids),
+// and every pair's stable rank within its block's list of the same key.
+// A block's 512 pairs form 8 groups of 64 consecutive pairs, one wavefront
+// each; a group's counts come from ballot key matches (no atomics), their
+// prefix over the groups in pair order gives each group's base, and a
+// pair's rank is its group's base plus the same-key lanes below it.
 // ---------------------------------------------------------------------------
 // ticket (may be NULL): the arrival ticket of the scan+split kernel that
 // follows on the same stream; workgroup 0 zeroes it, so that kernel always
 // starts from a zero ticket whatever the workspace held before.
+constexpr int kHistIters = kHistChunk / kHistThreads;
+constexpr int kHistGroups = kHistChunk / 64;
+static_assert(kHistChunk % kHistThreads == 0 && kHistChunk <= 65536, "ranks are uint16 within a block");
+
 __global__ __launch_bounds__(kHistThreads) void hist_count_kernel(const int32_t* __restrict__ ids, int64_t npairs,
                                                                   KeyMap km, int E, int nbits,
-                                                                  int32_t* __restrict__ partial, uint32_t* ticket) {
-  __shared__ int s_cnt[FOREMOE_MAX_EXPERTS + 1];
+                                                                  int32_t* __restrict__ partial,
+                                                                  uint16_t* __restrict__ rank, uint32_t* ticket) {
+  __shared__ int s_g[kHistGroups][FOREMOE_MAX_EXPERTS + 1];
   __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (ticket && blockIdx.x == 0 && tid == 0) atomicExch(ticket, 0u);
-  for (int e = tid; e <= E; e += kHistThreads) s_cnt[e] = 0;
+  for (int i = tid; i < kHistGroups * (E + 1); i += kHistThreads) s_g[i / (E + 1)][i % (E + 1)] = 0;
   load_sources(km, s_tb);
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * kHistChunk;
-  const int lane = tid & 63;
-#pragma unroll 1
-  for (int i = 0; i < kHistChunk / kHistThreads; ++i) {
+  int key[kHistIters];
+  uint64_t m[kHistIters];
+#pragma unroll
+  for (int i = 0; i < kHistIters; ++i) {
+    // group i * kWaves + w holds pairs base + (i * kWaves + w) * 64 + lane
     const int64_t p = base + (int64_t)i * kHistThreads + tid;
-    int key = -1;
-    if (p < npairs) key = pair_key(ids[p], p, km, s_tb);
-    const uint64_t active = __ballot(key >= 0);
-    const uint64_t m = match_key(key, nbits, active);
-    if (key >= 0 && lane == __builtin_ctzll(m)) atomicAdd(&s_cnt[key], __popcll(m));
+    key[i] = -1;
+    if (p < npairs) key[i] = pair_key(ids[p], p, km, s_tb);
+    const uint64_t active = __ballot(key[i] >= 0);
+    m[i] = match_key(key[i], nbits, active);
+    if (key[i] >= 0 && lane == __builtin_ctzll(m[i])) s_g[i * kWaves + w][key[i]] = __popcll(m[i]);
   }
   __syncthreads();
   int32_t* out = partial + (int64_t)blockIdx.x * (E + 1);
-  for (int e = tid; e <= E; e += kHistThreads) out[e] = s_cnt[e];
+  for (int e = tid; e <= E; e += kHistThreads) {
+    int run = 0;
+#pragma unroll
+    for (int g = 0; g < kHistGroups; ++g) {
+      const int c = s_g[g][e];
+      s_g[g][e] = run;
+      run += c;
+    }
+    out[e] = run;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kHistIters; ++i) {
+    const int64_t p = base + (int64_t)i * kHistThreads + tid;
+    if (p < npairs)
+      rank[p] = (uint16_t)((key[i] >= 0 && key[i] < E) ? s_g[i * kWaves + w][key[i]] + lanes_below(m[i]) : 0);
+  }
 }
 
 // Inclusive block-wide scan of one int per thread (NW wavefronts).
@@ -302,8 +330,9 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(const int32_t* _
 // assign_kernel does. Workgroups may run on different XCDs, whose L2
 // caches are not coherent with each other: the totals are stored and loaded
 // with device scope (SC1 cache policy: written through, never read from a
-// stale line), and each workgroup drains its stores before it takes its
-// ticket. No workgroup waits for another. The ticket is zero on entry: the
+// stale line), and each workgroup's total has reached memory before it
+// takes its ticket (its block bases, read only by later kernels, are stored
+// after). No workgroup waits for another. The ticket is zero on entry: the
 // count kernel before it on the same stream has zeroed it.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kHistThreads) void hist_scan_assign_kernel(
@@ -313,111 +342,68 @@ __global__ __launch_bounds__(kHistThreads) void hist_scan_assign_kernel(
   __shared__ int s_tmp[kWaves];
   __shared__ int s_cnt[257];
   __shared__ int s_last;
-  const int e = blockIdx.x;
+  // the plan's tables (at most 256 keys here), loaded by every workgroup
+  // beside its column so that the last one finds them in LDS
+  __shared__ int s_nrep[256];
+  __shared__ int s_w[256 * FOREMOE_MAX_REPLICAS];
+  __shared__ int s_se[FOREMOE_MAX_SLOTS];
+  __shared__ int s_sr[FOREMOE_MAX_SLOTS];
+  const int e = blockIdx.x, tid = threadIdx.x;
+  const int v_first = tid < nblocks ? partial[(int64_t)tid * (nkeys + 1) + e] : 0;
+  const int32_t* wsrc = P.src_rep_weight ? P.src_rep_weight : P.expert_rep_weight;
+  const int nw = P.src_rep_weight ? nkeys * P.R_max : (P.expert_rep_weight ? P.E * P.R_max : 0);
+  for (int i = tid; i < P.E; i += kHistThreads) s_nrep[i] = P.expert_nrep[i];
+  for (int i = tid; i < nw; i += kHistThreads) s_w[i] = wsrc[i];
+  for (int i = tid; i < P.S; i += kHistThreads) {
+    s_se[i] = P.slot_expert[i];
+    s_sr[i] = P.slot_replica[i];
+  }
+  // one chunk of blocks (the usual case): the block bases are stored after
+  // the ticket, so that taking it waits only for the total's store
+  const bool defer = nblocks <= kHistThreads;
+  int base_first = 0;
   int carry = 0;
   for (int64_t b0 = 0; b0 < nblocks; b0 += kHistThreads) {
-    const int64_t b = b0 + threadIdx.x;
-    const int v = b < nblocks ? partial[b * (nkeys + 1) + e] : 0;
+    const int64_t b = b0 + tid;
+    const int v = b0 == 0 ? v_first : (b < nblocks ? partial[b * (nkeys + 1) + e] : 0);
     int total;
     const int incl = block_inclusive_scan(v, s_tmp, total);
-    if (b < nblocks) partial[b * (nkeys + 1) + e] = carry + incl - v;
+    if (b < nblocks) {
+      if (defer) base_first = carry + incl - v;
+      else partial[b * (nkeys + 1) + e] = carry + incl - v;
+    }
     carry += total;
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     if (e < nkeys) __hip_atomic_store(counts + e, carry, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     else status[FOREMOE_WS_INVALID_IDS] = carry;
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the total has reached memory
     s_last = atomicAdd(ticket, 1u) == gridDim.x - 1;
   }
   __syncthreads();
+  if (defer && tid < nblocks) partial[(int64_t)tid * (nkeys + 1) + e] = base_first;
   if (!s_last) return;
-  for (int k = threadIdx.x; k < nkeys; k += kHistThreads)
+  for (int k = tid; k < nkeys; k += kHistThreads)
     s_cnt[k] = __hip_atomic_load(counts + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
-  assign_block<kHistThreads, 256>(s_cnt, P, rep_begin, slot_count, slot_offset, vslot_offset, rep_slot, status);
-  if (threadIdx.x == 0) atomicExch(ticket, 0u);  // ready for the next call
+  PlanDev L = P;
+  L.expert_nrep = s_nrep;
+  L.slot_expert = s_se;
+  L.slot_replica = s_sr;
+  if (P.src_rep_weight) L.src_rep_weight = s_w;
+  else if (P.expert_rep_weight) L.expert_rep_weight = s_w;
+  assign_block<kHistThreads, 256>(s_cnt, L, rep_begin, slot_count, slot_offset, vslot_offset, rep_slot, status);
+  if (tid == 0) atomicExch(ticket, 0u);  // ready for the next call
 }
 
 // ---------------------------------------------------------------------------
-// Step 3a: stable rank of every pair in its expert's list, replica, slot,
-// row; writes both index maps. Each wave ranks a contiguous quarter of the
-// block's pairs in ascending order.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kHistThreads) void permute_rank_kernel(
-    const int32_t* __restrict__ ids, int64_t npairs, KeyMap km, int E, int nbits, int R_max,
-    const int32_t* __restrict__ block_base, const int32_t* __restrict__ rep_begin,
-    const int32_t* __restrict__ rep_slot, const int32_t* __restrict__ slot_offset, int S, int64_t n_cap,
-    int32_t* __restrict__ pair_to_row, int32_t* __restrict__ row_to_pair, int32_t* __restrict__ status) {
-  __shared__ int s_w[kWaves][FOREMOE_MAX_EXPERTS + 1];
-  __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int e = lane; e <= E; e += 64) s_w[w][e] = 0;
-  load_sources(km, s_tb);
-  __syncthreads();
-  const int64_t wbase = (int64_t)blockIdx.x * kHistChunk + (int64_t)w * kPairsPerWave;
-  // pass 1: per-wave counts
-  for (int i = 0; i < kPairsPerWave / 64; ++i) {
-    const int64_t p = wbase + i * 64 + lane;
-    int key = -1;
-    if (p < npairs) key = pair_key(ids[p], p, km, s_tb);
-    if (key == E) key = -1;
-    const uint64_t active = __ballot(key >= 0);
-    const uint64_t m = match_key(key, nbits, active);
-    if (key >= 0 && lane == __builtin_ctzll(m)) s_w[w][key] += __popcll(m);
-  }
-  __syncthreads();
-  // pass 2: exclusive bases of each wave, starting from the block's base
-  for (int e = tid; e < E; e += kHistThreads) {
-    int run = block_base[(int64_t)blockIdx.x * (E + 1) + e];
-    for (int ww = 0; ww < kWaves; ++ww) {
-      const int c = s_w[ww][e];
-      s_w[ww][e] = run;
-      run += c;
-    }
-  }
-  __syncthreads();
-  // pass 3: rank, replica, slot, row
-  const int RS = R_max + 1;
-  for (int i = 0; i < kPairsPerWave / 64; ++i) {
-    const int64_t p = wbase + i * 64 + lane;
-    int key = -1;
-    if (p < npairs) key = pair_key(ids[p], p, km, s_tb);
-    if (key == E) key = -1;
-    const uint64_t active = __ballot(key >= 0);
-    const uint64_t m = match_key(key, nbits, active);
-    int q = 0;
-    if (key >= 0) q = s_w[w][key] + lanes_below(m);
-    __builtin_amdgcn_wave_barrier();
-    if (key >= 0 && lane == __builtin_ctzll(m)) s_w[w][key] = q + __popcll(m);
-    __builtin_amdgcn_wave_barrier();
-    if (p < npairs) {
-      int row = -1;
-      if (key >= 0) {
-        const int32_t* rb = rep_begin + (int64_t)key * RS;
-        int r = 0;
-        while (r + 1 < R_max && rb[r + 1] <= q) ++r;
-        const int j = rep_slot[key * R_max + r];
-        if (j >= 0 && j < S) {
-          const int64_t rr = (int64_t)slot_offset[j] + q - rb[r];
-          if (rr >= 0 && rr < n_cap) {
-            row = (int)rr;
-            row_to_pair[row] = (int32_t)p;
-          }
-        }
-      }
-      pair_to_row[p] = row;
-    }
-  }
-  if (blockIdx.x == 0 && tid == 0) {
-    const int64_t N = slot_offset[S];
-    status[FOREMOE_WS_DROPPED] = N > n_cap ? (int)(N - n_cap) : 0;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Step 3b: gather token rows into slot order. A wavefront moves kRowsPerWave
-// rows at a time: their pair indices arrive in one lane-parallel load, then
-// every 16-byte load of the group is issued before the stores.
+// Step 3: rank, replica, slot and row of every pair, both index maps, and
+// the rows of x gathered into slot order, in one pass over the pairs. A
+// wavefront takes 64 consecutive pairs, one per lane: a pair's rank in its
+// key's list is its block's base (the scanned partial counts) plus its rank
+// within the block (written by the count kernel). The wavefront then copies
+// the rows of its local pairs, kRowsPerWave at a time: every 16-byte load of
+// a group is issued before its stores.
 // ---------------------------------------------------------------------------
 constexpr int kRowsPerWave = 4;
 constexpr int kVecPerLane = 4;  // 16-byte vectors per lane per row and pass
@@ -435,50 +421,80 @@ struct RowReader {
   }
 };
 
-__device__ __forceinline__ int64_t uniform64(int64_t v) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restrict__ x, int64_t vec_per_row, int K,
-                                                          int64_t npairs, const int32_t* __restrict__ row_to_pair,
-                                                          const int32_t* __restrict__ n_rows_dev, int64_t n_cap,
-                                                          uint4* __restrict__ x_perm) {
+__global__ __launch_bounds__(256) void permute_gather_kernel(
+    const uint4* __restrict__ x, int64_t vec_per_row, const int32_t* __restrict__ ids, int64_t npairs, KeyMap km,
+    int nkeys, int R_max, const int32_t* __restrict__ block_base, const uint16_t* __restrict__ rank,
+    const int32_t* __restrict__ rep_begin, const int32_t* __restrict__ rep_slot, const int32_t* __restrict__ row_off,
+    int S, const int32_t* __restrict__ n_rows_dev, int64_t n_cap, int32_t* __restrict__ pair_to_row,
+    int32_t* __restrict__ row_to_pair, uint4* __restrict__ x_perm, int32_t* __restrict__ status) {
+  __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
+  load_sources(km, s_tb);
+  __syncthreads();
   const int lane = threadIdx.x & 63;
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nwaves = (int64_t)gridDim.x * 4;
-  int64_t N = *n_rows_dev;
-  if (N > n_cap) N = n_cap;
+  const int RS = R_max + 1;
   const uint32_t row_bytes = (uint32_t)(vec_per_row * 16);
-  for (int64_t r0 = wave * kRowsPerWave; r0 < N; r0 += nwaves * kRowsPerWave) {
-    int64_t mine = -1;
-    if (lane < kRowsPerWave && r0 + lane < N) {
-      const int64_t p = row_to_pair[r0 + lane];
-      if (p >= 0 && p < npairs) mine = p / K;  // never invalid when the maps are consistent
-    }
-    int64_t tok[kRowsPerWave];
-#pragma unroll
-    for (int r = 0; r < kRowsPerWave; ++r) tok[r] = uniform64(__shfl(mine, r, 64));
-    for (int64_t v0 = 0; v0 < vec_per_row; v0 += 64 * kVecPerLane) {
-      uint4 a[kRowsPerWave][kVecPerLane];
-#pragma unroll
-      for (int r = 0; r < kRowsPerWave; ++r) {
-        const RowReader rd(tok[r] >= 0 ? (const void*)(x + tok[r] * vec_per_row) : (const void*)x,
-                           tok[r] >= 0 ? row_bytes : 0u);
-#pragma unroll
-        for (int u = 0; u < kVecPerLane; ++u) a[r][u] = rd.load((uint32_t)((v0 + u * 64 + lane) * 16));
+  for (int64_t g = wave; g * 64 < npairs; g += nwaves) {
+    const int64_t p = g * 64 + lane;
+    int row = -1, tok = -1;
+    if (p < npairs) {
+      const int key = pair_key(ids[p], p, km, s_tb);
+      if (key >= 0 && key < nkeys) {
+        const int q = block_base[(p / kHistChunk) * (nkeys + 1) + key] + (int)rank[p];
+        const int32_t* rb = rep_begin + (int64_t)key * RS;
+        int r = 0;
+        while (r + 1 < R_max && rb[r + 1] <= q) ++r;
+        const int j = rep_slot[key * R_max + r];
+        if (j >= 0 && j < S) {
+          const int64_t rr = (int64_t)row_off[j] + q - rb[r];
+          if (rr >= 0 && rr < n_cap) {
+            row = (int)rr;
+            tok = (int)(p / km.K);
+            row_to_pair[row] = (int32_t)p;
+          }
+        }
       }
+      pair_to_row[p] = row;
+    }
+    uint64_t local = __ballot(row >= 0);
+    while (local) {
+      int rows[kRowsPerWave], toks[kRowsPerWave];
 #pragma unroll
       for (int r = 0; r < kRowsPerWave; ++r) {
-        if (tok[r] < 0) continue;
+        rows[r] = -1;
+        toks[r] = -1;
+        if (local) {
+          const int l = __builtin_ctzll(local);
+          local &= local - 1;
+          rows[r] = __builtin_amdgcn_readlane(row, l);
+          toks[r] = __builtin_amdgcn_readlane(tok, l);
+        }
+      }
+      for (int64_t v0 = 0; v0 < vec_per_row; v0 += 64 * kVecPerLane) {
+        uint4 a[kRowsPerWave][kVecPerLane];
 #pragma unroll
-        for (int u = 0; u < kVecPerLane; ++u) {
-          const int64_t vi = v0 + u * 64 + lane;
-          if (vi < vec_per_row) x_perm[(r0 + r) * vec_per_row + vi] = a[r][u];
+        for (int r = 0; r < kRowsPerWave; ++r) {
+          const RowReader rd(toks[r] >= 0 ? (const void*)(x + (int64_t)toks[r] * vec_per_row) : (const void*)x,
+                             toks[r] >= 0 ? row_bytes : 0u);
+#pragma unroll
+          for (int u = 0; u < kVecPerLane; ++u) a[r][u] = rd.load((uint32_t)((v0 + u * 64 + lane) * 16));
+        }
+#pragma unroll
+        for (int r = 0; r < kRowsPerWave; ++r) {
+          if (rows[r] < 0) continue;
+#pragma unroll
+          for (int u = 0; u < kVecPerLane; ++u) {
+            const int64_t vi = v0 + u * 64 + lane;
+            if (vi < vec_per_row) x_perm[(int64_t)rows[r] * vec_per_row + vi] = a[r][u];
+          }
         }
       }
     }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const int64_t N = *n_rows_dev;
+    status[FOREMOE_WS_DROPPED] = N > n_cap ? (int)(N - n_cap) : 0;
   }
 }
 
@@ -754,8 +770,9 @@ static int histogram_common(const char* who, const int32_t* ids, int64_t T, int3
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
+  uint16_t* rank = (uint16_t*)((char*)ws + ws_rank_off(T, K, E));
   hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, E,
-                     key_bits(E), partial, (uint32_t*)nullptr);
+                     key_bits(E), partial, rank, (uint32_t*)nullptr);
   hipLaunchKernelGGL(hist_scan_kernel, dim3(E + 1), dim3(kHistThreads), 0, st, partial, nb, E, counts, status);
   return check_launch(who);
 }
@@ -846,9 +863,10 @@ static int histogram_assign_impl(const int32_t* ids, int64_t T, int32_t K, const
   const int64_t npairs = T * (int64_t)K;
   const int64_t nb = hist_blocks(npairs);
   int32_t* partial = (int32_t*)((char*)ws + kWsPartialOff);
+  uint16_t* rank = (uint16_t*)((char*)ws + ws_rank_off(T, K, nkeys));
   uint32_t* ticket = (uint32_t*)ws + kWsTicketWord;
   hipLaunchKernelGGL(hist_count_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, nkeys,
-                     key_bits(nkeys), partial, ticket);
+                     key_bits(nkeys), partial, rank, ticket);
   hipLaunchKernelGGL(hist_scan_assign_kernel, dim3(nkeys + 1), dim3(kHistThreads), 0, st, partial, nb, nkeys, counts,
                      ticket, P, rep_begin, slot_count, slot_offset,
                      (int32_t*)((char*)ws + kWsVSlotOff), (int32_t*)((char*)ws + kWsRepSlotOff), status);
@@ -903,19 +921,18 @@ static int permute_impl(const void* x, foremoe_dtype dtype, int64_t T, int32_t d
   const int nkeys = n_src * plan->E;
   hipStream_t st = (hipStream_t)stream;
   const int64_t npairs = T * (int64_t)K;
-  const int64_t nb = hist_blocks(npairs);
   const int32_t* rep_slot = (const int32_t*)((char*)ws + kWsRepSlotOff);
   const int32_t* base = (const int32_t*)((char*)ws + kWsPartialOff);
+  const uint16_t* rank = (const uint16_t*)((char*)ws + ws_rank_off(T, K, nkeys));
   // rows come from the virtual slots' offsets (the slot offsets themselves
   // with one source)
   const int32_t* row_off = n_src >= 2 ? (const int32_t*)((char*)ws + kWsVSlotOff) : slot_offset;
   const KeyMap km{plan->E, n_src, K, n_src >= 2 ? plan->src_token_begin : nullptr};
-  hipLaunchKernelGGL(permute_rank_kernel, dim3((unsigned)nb), dim3(kHistThreads), 0, st, ids, npairs, km, nkeys,
-                     key_bits(nkeys), plan->R_max, base, rep_begin, rep_slot, row_off, n_src * plan->S, n_cap,
-                     pair_to_row, row_to_pair, status);
   const int64_t vpr = (int64_t)d * esz / 16;
-  hipLaunchKernelGGL(gather_rows_kernel, dim3(gather_grid(n_cap)), dim3(256), 0, st, (const uint4*)x, vpr, K,
-                     npairs, row_to_pair, slot_offset + plan->S, n_cap, (uint4*)x_perm);
+  const int64_t groups = (npairs + 63) / 64;
+  hipLaunchKernelGGL(permute_gather_kernel, dim3(gather_grid(groups)), dim3(256), 0, st, (const uint4*)x, vpr, ids,
+                     npairs, km, nkeys, plan->R_max, base, rank, rep_begin, rep_slot, row_off, n_src * plan->S,
+                     slot_offset + plan->S, n_cap, pair_to_row, row_to_pair, (uint4*)x_perm, status);
   return check_launch("foremoe_permute");
 }
 

@@ -123,7 +123,7 @@ class PolicyUpdate:
         self._join.wait(self.main)
 
     def ops(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
-            pipelined: bool = False, side_gathers: int = 0) -> list:
+            pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False) -> list:
         """The operations of micro-step i on inputs ms, in order, as (phase,
         thunk) pairs (phase None: a stream dependency). ev maps phases to
         (begin, end) timing events (hip_events.Event or torch's): row GEMMs
@@ -188,6 +188,9 @@ class PolicyUpdate:
         call("permute", main, lambda q: lib.foremoe_permute(
             ms.x.data_ptr(), BF16, T, d, ms.ids.data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
             P["r2p"], P["p2r"], P["ws"], wsz, q))
+        if pipelined and fwd_after_side:  # the previous micro-step's second-stream work ends first
+            prev = self.done[(i - 1) % 2]
+            ops.append((None, lambda: prev.wait(main)))
         call("gate_up_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_fwd_timed(
             P["x_perm"], BF16, d, F, S, so, widx, G, gu, n_cap, P["h"], P["au"], rws, rwsz, q, e0, e1))
         call("down_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_down_fwd_timed(
@@ -223,6 +226,6 @@ class PolicyUpdate:
         return ops
 
     def run(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
-            pipelined: bool = False, side_gathers: int = 0) -> None:
-        for _, op in self.ops(i, ms, ev, overlap, pipelined, side_gathers):
+            pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False) -> None:
+        for _, op in self.ops(i, ms, ev, overlap, pipelined, side_gathers, fwd_after_side):
             op()

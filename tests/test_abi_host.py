@@ -70,10 +70,11 @@ def test_workspace_size(lib):
     assert big > small
     # status words, the replica->slot table, the virtual-slot offsets
     # (1025 ints rounded to 256 bytes), then [blocks][E+1] partial counts
-    # (one block per 512 pairs)
+    # (one block per 512 pairs), then a uint16 in-block rank per pair
     fixed = 256 + 4 * 1024 * 16 + 4352
-    assert big >= fixed + 512 * 257 * 4
-    assert big - (fixed + 512 * 257 * 4) < 256
+    need = fixed + 512 * 257 * 4 + 2 * 32768 * 8
+    assert big >= need
+    assert big - need < 512
     assert lib.foremoe_workspace_size(-1, 2, 8) == 0
     assert lib.foremoe_workspace_size(10, 0, 8) == 0
     assert lib.foremoe_workspace_size(10, 2, 2000) == 0
