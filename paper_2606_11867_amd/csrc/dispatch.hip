@@ -471,14 +471,27 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
           toks[r] = __builtin_amdgcn_readlane(tok, l);
         }
       }
+      // a token's local pairs are consecutive lanes: a row of the group whose
+      // token equals the one before it is loaded once and stored twice
+      bool dup[kRowsPerWave];
+#pragma unroll
+      for (int r = 0; r < kRowsPerWave; ++r) dup[r] = r > 0 && toks[r] >= 0 && toks[r] == toks[r - 1];
       for (int64_t v0 = 0; v0 < vec_per_row; v0 += 64 * kVecPerLane) {
         uint4 a[kRowsPerWave][kVecPerLane];
 #pragma unroll
         for (int r = 0; r < kRowsPerWave; ++r) {
-          const RowReader rd(toks[r] >= 0 ? (const void*)(x + (int64_t)toks[r] * vec_per_row) : (const void*)x,
-                             toks[r] >= 0 ? row_bytes : 0u);
+          const bool ld = toks[r] >= 0 && !dup[r];
+          const RowReader rd(ld ? (const void*)(x + (int64_t)toks[r] * vec_per_row) : (const void*)x,
+                             ld ? row_bytes : 0u);
 #pragma unroll
           for (int u = 0; u < kVecPerLane; ++u) a[r][u] = rd.load((uint32_t)((v0 + u * 64 + lane) * 16));
+        }
+#pragma unroll
+        for (int r = 1; r < kRowsPerWave; ++r) {
+          if (dup[r]) {
+#pragma unroll
+            for (int u = 0; u < kVecPerLane; ++u) a[r][u] = a[r - 1][u];
+          }
         }
 #pragma unroll
         for (int r = 0; r < kRowsPerWave; ++r) {
