@@ -10,17 +10,20 @@ step = one micro-step through every step of the path:
   -> combine -> combine_bwd -> down dgrad (+SwiGLU') -> gate/up dgrad
   -> gate/up wgrad -> down wgrad -> permute_bwd
 
-The two weight-gradient GEMMs run on a second stream, each beside the
-data-gradient GEMM that does not feed it (down wgrad beside down dgrad,
-gate/up wgrad beside gate/up dgrad), and the streams are not joined at the
-end of a micro-step: the next micro-step's dispatch and forward (which do
-not depend on this one's weight gradients) start while they run, on a
-second set of activation buffers. permute_bwd (whose output feeds nothing
-later in the micro-step) runs on the second stream too, after the gate/up
-weight gradient, so that the next micro-step's dispatch starts right after
-the gate/up dgrad. --no-pipeline joins the streams after every micro-step;
---no-overlap runs all phases on one stream; --side-gathers 0 keeps
-permute_bwd on the main stream.
+The weight-gradient GEMMs of every group of 8 micro-steps (--wgrad-group)
+run as one launch pair over the group's rows after its last micro-step, on
+a third stream, while the next group's micro-steps run: the fp32 gradients
+are read and written once per group instead of once per micro-step (the
+fp32 accumulation over micro-steps of App. A.4; the operands stay resident
+in a ring of 17 buffer sets). The streams are not joined at the end of a
+micro-step: the next micro-step's dispatch and forward start on the other
+activation set. permute_bwd (whose output feeds nothing later in the
+micro-step) runs on a second stream, so that the next micro-step's dispatch
+starts right after the gate/up dgrad. --wgrad-group 1 gives every
+micro-step its own weight gradients on the second stream, each beside the
+data-gradient GEMM that does not feed it; --no-pipeline joins the streams
+after every micro-step; --no-overlap runs all phases on one stream;
+--side-gathers 0 keeps permute_bwd on the main stream.
 
 All inputs are resident in HBM before timing. A first pass brackets every
 ABI call with HIP events on the stream it runs on, one kernel after
@@ -81,6 +84,9 @@ def parse():
     ap.add_argument("--side-gathers", type=int, default=1, choices=(0, 1, 2),
                     help="with overlap: run permute_bwd (1, the default), and also the combine (2), on the second "
                          "stream; 0 keeps both on the main stream")
+    ap.add_argument("--wgrad-group", type=int, default=8,
+                    help="micro-steps per weight-gradient launch pair (their fp32 read-modify-write of dW "
+                         "is shared; 1: every micro-step its own, beside its data-gradient GEMMs)")
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the weight-gradient GEMMs on the main stream instead of beside the data gradients")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -158,9 +164,9 @@ def main() -> int:
                              x=dv(w.x(i)), dy=dv(w.dy(i)), plan=api.DevicePlan.from_host(m.plan, dev)))
     S_max = max(ms.S for ms in mss)
     # buffers, workspaces and the two streams of the benchmark's schedule
-    pu = PolicyUpdate(T, K, d, F, E, G, S_max, gu, dn, dev, split=not args.no_split)
+    M = args.wgrad_group  # a last incomplete group is launched by pu.finish(), inside the timed region
+    pu = PolicyUpdate(T, K, d, F, E, G, S_max, gu, dn, dev, split=not args.no_split, wgrad_group=M)
     stream = pu.main
-    buf = pu.sets[0]
     setup_s = time.time() - t0
 
     def run_step(i, ev=None, overlap=False, pipelined=False):
@@ -172,10 +178,12 @@ def main() -> int:
         run_step(i)
         torch.cuda.synchronize()
         S = mss[i].S
+        buf = pu.set_of(i, pipelined=False)
         sc = buf["slot_count"][:S].cpu().numpy()
         Ns.append(int(buf["slot_offset"][S].item()))
         gidx = mss[i].plan.slot_gidx.cpu().numpy()
         Gs.append(int(len(set(gidx[sc > 0].tolist()))))
+    pu.finish()
 
     if args.counters_pass:
         # after the one-stream pass above, each micro-step twice in the timed
@@ -194,6 +202,7 @@ def main() -> int:
     overlap = not args.no_overlap
     for i in range(args.warmup):
         run_step(i, overlap=overlap)
+    pu.finish()
     torch.cuda.synchronize()
 
     def new_events(phases=PHASES):
@@ -202,7 +211,11 @@ def main() -> int:
         return {p: (Event(timing=True), Event(timing=True)) for p in phases}
 
     def phase_sums(evs, phases=PHASES):
-        return {p: sum(ev[p][0].elapsed_time(ev[p][1]) for ev in evs) for p in phases}
+        # step s carries weight-gradient events only if it launched them
+        # (grouped: the last step of each group, counted from 0 after a finish())
+        def ran(p, s):
+            return p not in ("gate_up_wgrad", "down_wgrad") or M == 1 or pu.wgrad_launches_at(s)
+        return {p: sum(ev[p][0].elapsed_time(ev[p][1]) for s, ev in enumerate(evs) if ran(p, s)) for p in phases}
 
     # ---- per-kernel pass: every phase timed by HIP events, one kernel after
     # another, so that every phase's duration is its own (row GEMMs: events
@@ -212,11 +225,16 @@ def main() -> int:
     torch.cuda.synchronize()
     seq0, seq1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     seq0.record(stream)
+    flush_ev = new_events(["gate_up_wgrad", "down_wgrad"])
     for s in range(args.steps):
         run_step(s, evs_seq[s])
+    flushed = pu.finish(ev=flush_ev)  # grouped weight gradients: an incomplete last group's
     seq1.record(stream)
     torch.cuda.synchronize()
     phase_ms = phase_sums(evs_seq)
+    if flushed:
+        for p in ("gate_up_wgrad", "down_wgrad"):
+            phase_ms[p] += flush_ev[p][0].elapsed_time(flush_ev[p][1])
     seq_ms_per_step = seq0.elapsed_time(seq1) / args.steps
     # the dominant single-launch kernel; in the timed region only its calls
     # carry events (on the stream it runs on)
@@ -256,7 +274,7 @@ def main() -> int:
     work = {p: {"flop": 0.0, "bytes": 0.0} for p in PHASES}
     for s in range(args.steps):
         N, g = Ns[s % n_micro], Gs[s % n_micro]
-        for p, by in acc.phase_bytes(N, g, T, K, d, F).items():
+        for p, by in acc.phase_bytes(N, g, T, K, d, F, wgrad_group=M).items():
             work[p]["bytes"] += by
         for p in ("gate_up_fwd", "gate_up_dgrad", "gate_up_wgrad"):
             work[p]["flop"] += acc.gate_up_flops(N, d, F)
@@ -320,7 +338,8 @@ def main() -> int:
                    "micro_steps": n_micro, "n_pairs_mean": round(float(np.mean(Ns)), 1),
                    "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns)),
                    "backward_overlap": overlap, "tail_split": not args.no_split,
-                   "pipelined_micro_steps": pipelined, "side_gathers": args.side_gathers if overlap else 0},
+                   "pipelined_micro_steps": pipelined,
+                   "side_gathers": args.side_gathers if overlap else 0, "wgrad_group": M},
         "ms_per_step_sequential": round(seq_ms_per_step, 4),
         "roofline": roofline,
         "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),
@@ -852,7 +871,7 @@ def summarize_counters(folder: str) -> int:
     T, K, d, F = cp["T"], cp["K"], cp["d"], cp["F"]
     alg = collections.defaultdict(float)
     for N, g in zip(cp["N"], cp["G"]):
-        for p, by in acc.phase_bytes(N, g, T, K, d, F).items():
+        for p, by in acc.phase_bytes(N, g, T, K, d, F, wgrad_group=M).items():
             alg[p] += by / len(cp["N"])
     kernels = {}
     for phase, rec in per_phase.items():

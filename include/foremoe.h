@@ -57,6 +57,7 @@ extern "C" {
 #define FOREMOE_MAX_REPLICAS 16
 #define FOREMOE_MAX_TOPK 64
 #define FOREMOE_MAX_SOURCES 64
+#define FOREMOE_MAX_WGRAD_STEPS 16
 
 typedef enum foremoe_dtype {
   FOREMOE_F32 = 0,
@@ -351,6 +352,53 @@ int foremoe_ffn_down_wgrad(const void* dy_perm, const void* h, foremoe_dtype dty
                            int32_t d, int32_t F, int32_t S, const int32_t* slot_offset,
                            const int32_t* slot_gidx, int32_t G, int64_t n_cap,
                            float* dw_down, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 4, weight gradient of several micro-steps in one call (the same
+ * accumulation as above; App. A.4: the expert gradients are summed in fp32
+ * over the micro-steps of an update step). Each micro-step m contributes
+ * the rows of its own slots with its own operands and slot table:
+ *   dW_gate_up[g] += sum over m, then j with slot_gidx_m[j] == g, of
+ *                    d_au_m[rows of j]^T x_perm_m[rows of j]
+ *   dW_down[g]    += same with dy_perm_m and h_m
+ * Every group's rows are taken micro-step by micro-step in the order given,
+ * each micro-step's slots in slot order; the summation order is fixed, so
+ * the result is deterministic. It equals the sum of one call per micro-step
+ * up to fp32 rounding: one read-modify-write of dW serves all the
+ * micro-steps (a launch over 4 micro-steps moves a quarter of the fp32
+ * gradient traffic of 4 launches).
+ * steps: host array of n_steps records (read during the call only);
+ *   a, b: gate/up: d_au [n_cap, 2F] and x_perm [n_cap, d];
+ *         down: dy_perm [n_cap, d] and h [n_cap, F];
+ *   slot_offset [S+1], slot_gidx [S]: that micro-step's device slot table;
+ *   S, n_cap: its slots and buffer rows (S == 0 or n_cap == 0: skipped).
+ * part, parts (0 <= part < parts <= FOREMOE_MAX_WGRAD_STEPS): the call
+ *   updates only part `part` of every dW[g]: with 256 x 256 output tiles
+ *   (128 x 128 when a dimension is not a multiple of 256) numbered row-major,
+ *   the tiles t with t % parts == part (the fp32 path: rows m with
+ *   m % parts == part). The parts 0 .. parts-1 of the same steps together
+ *   give the whole update, so one group of micro-steps can be spread over
+ *   several launches. parts = 1: everything.
+ * 0 <= n_steps <= FOREMOE_MAX_WGRAD_STEPS; the S of all steps add up to at
+ * most FOREMOE_MAX_SLOTS. Workspace, dtype, shape and G rules as above.
+ */
+typedef struct foremoe_wgrad_step {
+  const void* a;
+  const void* b;
+  const int32_t* slot_offset;
+  const int32_t* slot_gidx;
+  int32_t S;
+  int64_t n_cap;
+} foremoe_wgrad_step;
+
+int foremoe_ffn_gate_up_wgrad_steps(const foremoe_wgrad_step* steps, int32_t n_steps,
+                                    foremoe_dtype dtype, int32_t d, int32_t F, int32_t G,
+                                    int32_t part, int32_t parts, float* dw_gate_up, void* ws,
+                                    size_t ws_bytes, void* stream);
+int foremoe_ffn_down_wgrad_steps(const foremoe_wgrad_step* steps, int32_t n_steps,
+                                 foremoe_dtype dtype, int32_t d, int32_t F, int32_t G,
+                                 int32_t part, int32_t parts, float* dw_down, void* ws,
+                                 size_t ws_bytes, void* stream);
 
 /*
  * Step 5 (Sec. 2.1: the output is the router-probability weighted sum of

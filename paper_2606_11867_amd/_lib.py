@@ -20,6 +20,7 @@ MAX_SLOTS = 1024
 MAX_REPLICAS = 16
 MAX_TOPK = 64
 MAX_SOURCES = 64
+MAX_WGRAD_STEPS = 16
 STATIC_SCRATCH_BYTES = 8 << 20
 XFER_PARAMS = 1
 XFER_GRADS = 2
@@ -47,6 +48,13 @@ class Machine(ctypes.Structure):
 
 
 PMachine = ctypes.POINTER(Machine)
+
+
+class WgradStep(ctypes.Structure):
+    _fields_ = [("a", c_p), ("b", c_p), ("slot_offset", c_p), ("slot_gidx", c_p), ("S", c_i32), ("n_cap", c_i64)]
+
+
+PWgradStep = ctypes.POINTER(WgradStep)
 
 # name -> (restype, argtypes)
 SIGNATURES = {
@@ -79,6 +87,10 @@ SIGNATURES = {
                                                  c_i64, c_p, c_p, c_sz, c_p]),
     "foremoe_ffn_down_wgrad": (ctypes.c_int, [c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_i32,
                                               c_i64, c_p, c_p, c_sz, c_p]),
+    "foremoe_ffn_gate_up_wgrad_steps": (ctypes.c_int, [PWgradStep, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                                       c_p, c_p, c_sz, c_p]),
+    "foremoe_ffn_down_wgrad_steps": (ctypes.c_int, [PWgradStep, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                                    c_p, c_p, c_sz, c_p]),
     "foremoe_combine": (ctypes.c_int, [c_p, c_i32, c_p, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_i32, c_p]),
     "foremoe_combine_bwd": (ctypes.c_int, [c_p, c_p, c_i32, c_p, c_p, c_i64, c_i32, c_i32, c_i64, c_p, c_p,
                                            c_p]),

@@ -278,6 +278,44 @@ def grouped_ffn_wgrad(x_perm: torch.Tensor, h: torch.Tensor, dy_perm: torch.Tens
           "foremoe_grouped_ffn_wgrad")
 
 
+def wgrad_steps(steps, *, a: str, b: str):
+    """ctypes array of foremoe_wgrad_step records for the micro-steps in
+    ``steps`` (mappings with tensors ``a`` and ``b`` named by the arguments,
+    ``slot_offset``, ``slot_gidx``)."""
+    arr = (_lib.WgradStep * max(len(steps), 1))()
+    for i, st in enumerate(steps):
+        A, B = st[a], st[b]
+        arr[i] = _lib.WgradStep(_ptr(A), _ptr(B), _ptr(st["slot_offset"]), _ptr(st["slot_gidx"]),
+                                int(st["slot_gidx"].shape[0]), int(A.shape[0]))
+    return arr
+
+
+def grouped_ffn_wgrad_steps(steps, dw_gate_up: torch.Tensor, dw_down: torch.Tensor,
+                            ws: Optional[torch.Tensor] = None, part: int = 0, parts: int = 1) -> None:
+    """Weight gradients of several micro-steps in one launch pair: each entry
+    of ``steps`` maps x_perm, h, dy_perm, d_au, slot_offset, slot_gidx to that
+    micro-step's tensors. Accumulates (+=) into dw_gate_up [G, 2F, d] and
+    dw_down [G, d, F] (fp32); the same sum as one grouped_ffn_wgrad call per
+    micro-step, in one read-modify-write of the gradients. ``part`` of
+    ``parts``: only that share of the output tiles (all parts together give
+    the whole update)."""
+    G, F2, d = dw_gate_up.shape
+    F = F2 // 2
+    if dw_gate_up.dtype != torch.float32 or dw_down.dtype != torch.float32:
+        raise TypeError("weight gradients are fp32")
+    if not steps:
+        return
+    dt = _dt(steps[0]["x_perm"])
+    wsp, wsn = (None, 0) if ws is None else (_ptr(ws), ws.numel())
+    lib, st = _lib.load(), _stream(dw_gate_up.device)
+    gu = wgrad_steps(steps, a="d_au", b="x_perm")
+    check(lib.foremoe_ffn_gate_up_wgrad_steps(gu, len(steps), dt, d, F, G, part, parts, _ptr(dw_gate_up), wsp, wsn,
+                                              st), "foremoe_ffn_gate_up_wgrad_steps")
+    dn = wgrad_steps(steps, a="dy_perm", b="h")
+    check(lib.foremoe_ffn_down_wgrad_steps(dn, len(steps), dt, d, F, G, part, parts, _ptr(dw_down), wsp, wsn, st),
+          "foremoe_ffn_down_wgrad_steps")
+
+
 def combine(y_perm: torch.Tensor, pair_to_row: torch.Tensor, gates: torch.Tensor,
             out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
     T, K = gates.shape

@@ -304,13 +304,15 @@ struct Core {
     }
   };
 
-  // Operand fragments of one k-step, double-buffered in registers.
+  // Operand fragments of FS k-steps in registers (the one being multiplied
+  // and the ones being read ahead).
+  template <int FS>
   struct Frags {
-    bf16x8 a[2][MB], b[2][NB];
+    bf16x8 a[FS][MB], b[FS][NB];
   };
 
-  template <class AT, class BT, int BK>
-  __device__ __forceinline__ static void load_frags(Frags& f, int set, const char* As, const char* Bs,
+  template <class AT, class BT, int BK, class FragsT>
+  __device__ __forceinline__ static void load_frags(FragsT& f, int set, const char* As, const char* Bs,
                                                     const Offsets<AT, BT, BK>& o, int kk) {
 #pragma unroll
     for (int i = 0; i < MB; ++i) f.a[set][i] = AT::frag(As, o.a[i], o.ka, kk);
@@ -318,25 +320,26 @@ struct Core {
     for (int j = 0; j < NB; ++j) f.b[set][j] = BT::frag(Bs, o.b[j], o.kb, kk);
   }
 
-  // The MFMAs of one k-step from register set `set`, with the LDS reads of
-  // the next k-step's fragments (if any) interleaved: one read after each of
-  // the first MB + NB MFMAs, so the reads complete under the matrix work.
-  // extra(q), q < NX, runs right after MFMA s when q < (s + 1) NX / (MB NB)
-  // and q >= s NX / (MB NB), evenly over the k-step: the loads
-  // of a later stage, spread over the k-step so that the address unit
-  // drains them while the matrix cores keep working.
-  template <class AT, class BT, int BK, int NX, class Extra>
-  __device__ __forceinline__ void mfma_step(Frags& f, int set, bool prefetch, const char* nAs, const char* nBs,
-                                            const Offsets<AT, BT, BK>& o, int nkk, Extra&& extra) {
+  // The MFMAs of one k-step from register set CUR, with the LDS reads of a
+  // later k-step's fragments (k-step nkk of the stage at nAs/nBs, into set
+  // NXT) interleaved: one read after each of the first MB + NB MFMAs, so the
+  // reads complete under the matrix work. extra(q), q < NX, runs right after
+  // MFMA s when q < (s + 1) NX / (MB NB) and q >= s NX / (MB NB), evenly
+  // over the k-step: the loads of a later stage, spread over the k-step so
+  // that the address unit drains them while the matrix cores keep working.
+  template <class AT, class BT, int BK, int NX, int CUR, int NXT, class FragsT, class Extra>
+  __device__ __forceinline__ void mfma_step(FragsT& f, const char* nAs, const char* nBs, const Offsets<AT, BT, BK>& o,
+                                            int nkk, Extra&& extra) {
     constexpr int NM = MB * NB;
     static_assert(NX >= 0 && NX <= NM, "loads per k-step");
+    static_assert(CUR != NXT, "the fragments being read go to another set");
 #pragma unroll
     for (int s = 0; s < NM; ++s) {
       const int i = s / NB, j = s % NB;
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[set][j], f.a[set][i], acc[i][j], 0, 0, 0);
-      if (prefetch && s < MB + NB) {
-        if (s < MB) f.a[set ^ 1][s] = AT::frag(nAs, o.a[s], o.ka, nkk);
-        else f.b[set ^ 1][s - MB] = BT::frag(nBs, o.b[s - MB], o.kb, nkk);
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[CUR][j], f.a[CUR][i], acc[i][j], 0, 0, 0);
+      if (s < MB + NB) {
+        if (s < MB) f.a[NXT][s] = AT::frag(nAs, o.a[s], o.ka, nkk);
+        else f.b[NXT][s - MB] = BT::frag(nBs, o.b[s - MB], o.kb, nkk);
       }
       if constexpr (NX > 0) {
 #pragma unroll
@@ -418,10 +421,21 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Fragment read distance of the row GEMMs: 2 for the gate/up forward (2%
+// faster than 1 on the benchmark), 1 for the others (with a third register
+// set they spill, and run 4-6% slower).
+#ifndef FM_FRAG_DIST_FWD
+#define FM_FRAG_DIST_FWD 2
+#endif
+#ifndef FM_FRAG_DIST
+#define FM_FRAG_DIST 1
+#endif
+
+// Fragments read one k-step ahead (two register sets).
 template <class CoreT, class AT, class BT, int BK, int NS, class Issue>
-__device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
-                                                 const typename CoreT::template Offsets<AT, BT, BK>& o,
-                                                 Issue&& issue) {
+__device__ __forceinline__ void pipelined_k_loop_d1(CoreT& core, char* lds, int KT,
+                                                    const typename CoreT::template Offsets<AT, BT, BK>& o,
+                                                    Issue&& issue) {
   static_assert(BK % 32 == 0, "the last k-step's fragments must be read before the barrier");
   constexpr int KK = BK / 16;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
@@ -432,7 +446,7 @@ __device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
   constexpr int SPREAD = FM_LOAD_SPREAD < KK ? FM_LOAD_SPREAD : KK;
   static_assert(SPREAD >= 1, "load spread");
   auto lo = [](int j) constexpr { return j * PER / SPREAD; };
-  typename CoreT::Frags f;
+  typename CoreT::template Frags<2> f;
   // stages 0 .. NS-2 whole, and the part of stage NS-1 that a previous
   // iteration's last k-step would have carried
 #pragma unroll
@@ -450,20 +464,97 @@ __device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
       constexpr int set = kk & 1;
       if constexpr (kk < KK - 1) {
         constexpr int j = kk + 1;  // position in the load window of stage kt - 1 + NS
-        core.template mfma_step<AT, BT, BK, (j < SPREAD ? lo(j + 1) - lo(j) : 0)>(
-            f, set, true, st, st + AT::BYTES, o, kk + 1, [&](int q) { issue(kt - 1 + NS, lo(j) + q); });
+        core.template mfma_step<AT, BT, BK, (j < SPREAD ? lo(j + 1) - lo(j) : 0), set, set ^ 1>(
+            f, st, st + AT::BYTES, o, kk + 1, [&](int q) { issue(kt - 1 + NS, lo(j) + q); });
       } else {
         wait_stage<NS, PER>(NS - 2);  // stage kt+1 (past the last: empty) has landed
         __syncthreads();
         const char* nst = lds + ((kt + 1) % NS) * STAGE;
         // (after the last stage this reads a stale buffer: harmless, and no
         // branch among the MFMAs)
-        core.template mfma_step<AT, BT, BK, lo(1)>(f, set, true, nst, nst + AT::BYTES, o, 0,
-                                                   [&](int q) { issue(kt + NS, q); });
+        core.template mfma_step<AT, BT, BK, lo(1), set, set ^ 1>(f, nst, nst + AT::BYTES, o, 0,
+                                                                 [&](int q) { issue(kt + NS, q); });
       }
     });
   }
   wait_vm<0>();  // the (empty) loads of stages past the last have landed too
+}
+
+// Fragments read D k-steps ahead (D + 1 register sets), so that each LDS read
+// has D k-steps of matrix work to complete under. The barrier then comes at
+// k-step KK - D of stage kt, the first whose reads reach into stage kt+1: by
+// then every read of stage kt's buffer has been issued, and the loads of
+// stage kt+NS go into it during k-steps KK - D .. KK - D + SPREAD - 1. The
+// set of global k-step g is g % (D + 1); the stage loop is unrolled U times
+// so that every set index is a compile-time constant.
+template <class CoreT, class AT, class BT, int BK, int NS, int D, class Issue>
+__device__ __forceinline__ void pipelined_k_loop_deep(CoreT& core, char* lds, int KT,
+                                                      const typename CoreT::template Offsets<AT, BT, BK>& o,
+                                                      Issue&& issue) {
+  constexpr int KK = BK / 16;
+  constexpr int FS = D + 1;
+  constexpr int STAGE = AT::BYTES + BT::BYTES;
+  constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
+  constexpr int SPREAD = FM_LOAD_SPREAD < D ? FM_LOAD_SPREAD : D;
+  static_assert(D >= 2 && KK >= D, "read distance");
+  static_assert(SPREAD >= 1, "load spread");
+  auto lo = [](int j) constexpr { return j * PER / SPREAD; };
+  constexpr int U = [] {
+    int u = 1;
+    while ((u * KK) % FS) ++u;
+    return u;
+  }();
+  typename CoreT::template Frags<FS> f;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) issue(s, p);
+  }
+  wait_stage<NS, PER>(NS - 1);  // stage 0 has landed
+  __syncthreads();
+  static_for<0, D>([&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    CoreT::template load_frags<AT, BT, BK>(f, k, lds, lds + AT::BYTES, o, k);
+  });
+  for (int kt = 0; kt < KT;) {
+    static_for<0, U>([&](auto phc) {
+      constexpr int ph = decltype(phc)::value;
+      if (kt >= KT) return;
+      const char* st = lds + (kt % NS) * STAGE;
+      const char* nst = lds + ((kt + 1) % NS) * STAGE;
+      static_for<0, KK>([&](auto kkc) {
+        constexpr int kk = decltype(kkc)::value;
+        constexpr int g = ph * KK + kk;
+        constexpr int cur = g % FS, nxt = (g + D) % FS;
+        constexpr int j = kk - (KK - D);  // position in the load window of stage kt + NS
+        constexpr int nx = (j >= 0 && j < SPREAD) ? lo(j + 1) - lo(j) : 0;
+        if constexpr (j == 0) {
+          wait_stage<NS, PER>(NS - 2);  // stage kt+1 (past the last: empty) has landed
+          __syncthreads();
+        }
+        // reads of k-step kk + D: in this stage's buffer, or in the next's
+        // (after the last stage a stale buffer: harmless, and no branch among
+        // the MFMAs)
+        const char* rs = kk + D < KK ? st : nst;
+        constexpr int rk = (kk + D) % KK;
+        core.template mfma_step<AT, BT, BK, nx, cur, nxt>(f, rs, rs + AT::BYTES, o, rk, [&](int q) {
+          if constexpr (j >= 0) issue(kt + NS, lo(j) + q);
+        });
+      });
+      ++kt;
+    });
+  }
+  wait_vm<0>();  // the (empty) loads of stages past the last have landed too
+}
+
+template <class CoreT, class AT, class BT, int BK, int NS, int D = FM_FRAG_DIST, class Issue>
+__device__ __forceinline__ void pipelined_k_loop(CoreT& core, char* lds, int KT,
+                                                 const typename CoreT::template Offsets<AT, BT, BK>& o,
+                                                 Issue&& issue) {
+  if constexpr (D >= 2 && BK / 16 >= D)
+    pipelined_k_loop_deep<CoreT, AT, BT, BK, NS, D>(core, lds, KT, o, issue);
+  else
+    pipelined_k_loop_d1<CoreT, AT, BT, BK, NS>(core, lds, KT, o, issue);
 }
 
 // ---------------------------------------------------------------------------
@@ -928,7 +1019,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     };
 
     core.zero();
-    pipelined_k_loop<CoreT, AT, BT, BK, NS>(core, lds, nk, offs, issue);
+    pipelined_k_loop<CoreT, AT, BT, BK, NS, SW ? FM_FRAG_DIST_FWD : FM_FRAG_DIST>(core, lds, nk, offs, issue);
     if (pieces > 1) {
       // piece q' of tail tile t - full is computed by the workgroup with
       // slot slot - q + q'; each keeps its partial sums in its own
@@ -995,56 +1086,113 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
 // stream) adds them in chunk order. Every output element therefore has one
 // fixed summation order: deterministic, no atomics on floats.
 // ---------------------------------------------------------------------------
-struct WgradArgs {
+// One micro-step's operands of a weight-gradient call: rows [0, n_cap) of A
+// and B, and its slot table.
+struct WgradStep {
   const uint16_t* A;  // [n_cap, M]
-  int64_t lda;
   const uint16_t* B;  // [n_cap, N]
-  int64_t ldb;
-  int M, N;
   const int32_t* slot_offset;
   const int32_t* slot_gidx;
-  int S, G;
+  int S;
+  int vbase;  // first virtual slot of this step (prefix of S over the steps before)
   int64_t n_cap;
+};
+
+struct WgradArgs {
+  WgradStep step[FOREMOE_MAX_WGRAD_STEPS];
+  int n_steps;
+  int V;  // virtual slots: every step's slots, steps in order
+  int64_t lda, ldb;
+  int M, N;
+  int G;
   float* C;  // dW[g] at C + g * gstride, row-major [M, N]
   int64_t ldc;
   int64_t gstride;
   float* part;  // partial tiles [p_max][BM * BN]
   int p_max;
+  // with partial tiles: the plan the reduce kernel needs, written by
+  // workgroup 0 of the main kernel: {groups with rows, chunk rows, then per
+  // ordered group: gradient index, rows, first partial tile}
+  int* plan_out;
   // work counters {next item, finished workgroups} (zero on entry, zeroed
   // again by the last workgroup), or NULL for a static item order
   unsigned* sched;
+  // output tiles of this call: tile index t of a group's dW (row-major over
+  // the BM x BN tiles) with t % tparts == tpart
+  int tpart, tparts;
 };
 
+// Tiles of one group's dW that a call computes, and the index of the i-th.
+__device__ __forceinline__ int wgrad_call_tiles(const WgradArgs& a, int BM, int BN) {
+  return ((a.M / BM) * (a.N / BN) - a.tpart + a.tparts - 1) / a.tparts;
+}
+__device__ __forceinline__ int wgrad_tile(const WgradArgs& a, int i) { return a.tpart + i * a.tparts; }
+
+// The row sequence of gradient group g is the rows of every virtual slot v
+// (step m's slot j, v = vbase_m + j) with gradient index g, in v order: the
+// micro-steps in order, each one's slots in order.
 struct WgradPlan {
-  int off[FOREMOE_MAX_SLOTS + 1];   // clamped slot offsets
-  int gidx[FOREMOE_MAX_SLOTS];      // gradient index, -1 for empty/invalid slots
-  int rows[FOREMOE_MAX_SLOTS];      // rows per group
-  int order[FOREMOE_MAX_SLOTS];     // groups by descending rows
-  int ibase[FOREMOE_MAX_SLOTS + 1]; // work-item prefix over ordered groups
-  int pbase[FOREMOE_MAX_SLOTS + 1]; // partial-tile prefix over ordered groups
-  int nne;                          // non-empty groups
-  int ch;                           // chunk rows (INT_MAX: no split)
+  int beg[FOREMOE_MAX_SLOTS];        // clamped row range [beg, end) of virtual slot v in its step's rows
+  int end[FOREMOE_MAX_SLOTS];
+  int gs[FOREMOE_MAX_SLOTS];         // step << 16 | gradient index, -1 for empty/invalid slots
+  int rows[FOREMOE_MAX_SLOTS];       // rows per group
+  int order[FOREMOE_MAX_SLOTS];      // groups by descending rows
+  int ibase[FOREMOE_MAX_SLOTS + 1];  // work-item prefix over ordered groups
+  int pbase[FOREMOE_MAX_SLOTS + 1];  // partial-tile prefix over ordered groups
+  const uint16_t* A[FOREMOE_MAX_WGRAD_STEPS];  // operands of each step
+  const uint16_t* B[FOREMOE_MAX_WGRAD_STEPS];
+  int nne;                           // non-empty groups
+  int ch;                            // chunk rows (INT_MAX: no split)
+  __device__ __forceinline__ int gidx(int v) const { return gs[v] < 0 ? -1 : (gs[v] & 0xFFFF); }
+  __device__ __forceinline__ int step(int v) const { return gs[v] >> 16; }
 };
 
 template <int BM, int BN, int BK>
 __device__ void build_wgrad_plan(const WgradArgs& a, WgradPlan& P) {
   const int tid = threadIdx.x;
-  const int S = a.S, G = a.G;
-  const int tpg = (a.M / BM) * (a.N / BN);
+  const int G = a.G, V = a.V;
+  const int tpg = wgrad_call_tiles(a, BM, BN);
   const int nt = blockDim.x;
   if (tid == 0) P.nne = 0;
+  // the step table into LDS with compile-time indices (a kernel argument
+  // indexed at run time would be copied to scratch)
+#pragma unroll
+  for (int m = 0; m < FOREMOE_MAX_WGRAD_STEPS; ++m) {
+    if (tid == m && m < a.n_steps) {
+      P.A[m] = a.step[m].A;
+      P.B[m] = a.step[m].B;
+    }
+  }
   for (int g = tid; g < G; g += nt) P.rows[g] = 0;
-  for (int j = tid; j <= S; j += nt) {
-    const int64_t o = a.slot_offset[j];
-    P.off[j] = (int)(o < 0 ? 0 : (o > a.n_cap ? a.n_cap : o));
+  for (int v = tid; v < V; v += nt) {
+    int m = 0;
+#pragma unroll
+    for (int q = 1; q < FOREMOE_MAX_WGRAD_STEPS; ++q)
+      if (q < a.n_steps && v >= a.step[q].vbase) m = q;
+    const int32_t* off = nullptr;
+    const int32_t* gi = nullptr;
+    int64_t n_cap = 0;
+    int j = 0;
+#pragma unroll
+    for (int q = 0; q < FOREMOE_MAX_WGRAD_STEPS; ++q)
+      if (q == m) {
+        off = a.step[q].slot_offset;
+        gi = a.step[q].slot_gidx;
+        n_cap = a.step[q].n_cap;
+        j = v - a.step[q].vbase;
+      }
+    int64_t lo = off[j], hi = off[j + 1];
+    lo = lo < 0 ? 0 : (lo > n_cap ? n_cap : lo);
+    hi = hi < 0 ? 0 : (hi > n_cap ? n_cap : hi);
+    const int g = gi[j];
+    const bool ok = g >= 0 && g < G && hi > lo;
+    P.beg[v] = (int)lo;
+    P.end[v] = ok ? (int)hi : (int)lo;
+    P.gs[v] = ok ? (m << 16 | g) : -1;
   }
   __syncthreads();
-  for (int j = tid; j < S; j += nt) {
-    const int g = a.slot_gidx[j];
-    const int n = P.off[j + 1] - P.off[j];
-    P.gidx[j] = (g >= 0 && g < G && n > 0) ? g : -1;
-    if (P.gidx[j] >= 0) atomicAdd(&P.rows[g], n);
-  }
+  for (int v = tid; v < V; v += nt)
+    if (P.gs[v] >= 0) atomicAdd(&P.rows[P.gidx(v)], P.end[v] - P.beg[v]);
   __syncthreads();
   for (int g = tid; g < G; g += nt) {
     const int rg = P.rows[g];
@@ -1085,56 +1233,71 @@ __device__ void build_wgrad_plan(const WgradArgs& a, WgradPlan& P) {
 }
 
 // Walks the k-tiles of one chunk [s0, s1) of a group's row sequence: each
-// k-tile lies inside one slot's row range [lo, hi).
+// k-tile lies inside one virtual slot's row range [lo, hi).
 struct KCursor {
-  int j, pos, lo, hi, k;  // slot, sequence position of slot start, segment rows, tile start
+  int j, pos, lo, hi, k;  // virtual slot, sequence position of slot start, segment rows, tile start
   bool done;
+  const uint16_t* pa;  // operands of slot j's micro-step (wave-uniform: scalar registers)
+  const uint16_t* pb;
 };
 
-__device__ __forceinline__ void cursor_next_slot(const WgradPlan& P, int S, int g, int s1, KCursor& c) {
+__device__ __forceinline__ const uint16_t* uniform_ptr(const uint16_t* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const uint16_t*)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ void cursor_next_slot(const WgradPlan& P, int V, int g, int s1, KCursor& c) {
   int j = c.j, pos = c.pos;
   for (;;) {
-    if (j >= 0 && P.gidx[j] == g) pos += P.off[j + 1] - P.off[j];
+    if (j >= 0 && P.gidx(j) == g) pos += P.end[j] - P.beg[j];
     ++j;
-    if (j >= S || pos >= s1) {
+    if (j >= V || pos >= s1) {
       c.done = true;
       return;
     }
-    if (P.gidx[j] == g) break;
+    if (P.gidx(j) == g) break;
   }
   c.j = j;
   c.pos = pos;
-  c.lo = P.off[j];
-  const int n = P.off[j + 1] - P.off[j];
-  c.hi = P.off[j] + (n < s1 - pos ? n : s1 - pos);
+  c.lo = P.beg[j];
+  const int n = P.end[j] - P.beg[j];
+  c.hi = P.beg[j] + (n < s1 - pos ? n : s1 - pos);
   c.k = c.lo;
+  c.pa = uniform_ptr(P.A[P.step(j)]);
+  c.pb = uniform_ptr(P.B[P.step(j)]);
 }
 
-__device__ __forceinline__ KCursor cursor_begin(const WgradPlan& P, int S, int g, int s0, int s1) {
+__device__ __forceinline__ KCursor cursor_begin(const WgradPlan& P, int V, int g, int s0, int s1) {
   KCursor c;
   c.done = false;
   int pos = 0;
-  for (int j = 0; j < S; ++j) {
-    if (P.gidx[j] != g) continue;
-    const int n = P.off[j + 1] - P.off[j];
+  for (int j = 0; j < V; ++j) {
+    if (P.gidx(j) != g) continue;
+    const int n = P.end[j] - P.beg[j];
     if (pos + n > s0) {
       c.j = j;
       c.pos = pos;
-      c.lo = P.off[j] + (s0 - pos);
-      c.hi = P.off[j] + (n < s1 - pos ? n : s1 - pos);
+      c.lo = P.beg[j] + (s0 - pos);
+      c.hi = P.beg[j] + (n < s1 - pos ? n : s1 - pos);
       c.k = c.lo;
+      c.pa = uniform_ptr(P.A[P.step(j)]);
+      c.pb = uniform_ptr(P.B[P.step(j)]);
       return c;
     }
     pos += n;
   }
   c.done = true;
+  c.pa = uniform_ptr(P.A[0]);
+  c.pb = uniform_ptr(P.B[0]);
   return c;
 }
 
 template <int BK>
-__device__ __forceinline__ void cursor_advance(const WgradPlan& P, int S, int g, int s1, KCursor& c) {
+__device__ __forceinline__ void cursor_advance(const WgradPlan& P, int V, int g, int s1, KCursor& c) {
   c.k += BK;
-  if (c.k >= c.hi) cursor_next_slot(P, S, g, s1, c);
+  if (c.k >= c.hi) cursor_next_slot(P, V, g, s1, c);
 }
 
 template <int BM, int BN, int BK, int NS, int WGM, int WGN>
@@ -1149,8 +1312,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
   __shared__ WgradPlan P;
 
   build_wgrad_plan<BM, BN, BK>(a, P);
-  const int S = a.S;
-  const int mt_n = a.M / BM, nt_n = a.N / BN, tpg = mt_n * nt_n;
+  if (a.plan_out && blockIdx.x == 0) {
+    if (threadIdx.x == 0) {
+      a.plan_out[0] = P.nne;
+      a.plan_out[1] = P.ch;
+    }
+    for (int i = threadIdx.x; i < P.nne; i += blockDim.x) {
+      a.plan_out[2 + 3 * i] = P.order[i];
+      a.plan_out[3 + 3 * i] = P.rows[P.order[i]];
+      a.plan_out[4 + 3 * i] = P.pbase[i];
+    }
+  }
+  const int V = a.V;
+  const int nt_n = a.N / BN, tpg = wgrad_call_tiles(a, BM, BN);
   const int total = P.ibase[P.nne];
   const int lane = lane64(), wave = wave_id();
   const int wm = wave / WGN, wn = wave % WGN;
@@ -1179,7 +1353,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
     const int gi = __builtin_amdgcn_readfirstlane(lo);
     const int g = P.order[gi];
     const int local = t - P.ibase[gi];
-    const int c = local / tpg, tile = local % tpg;
+    const int c = local / tpg, tile_l = local % tpg, tile = wgrad_tile(a, tile_l);
     const int m0 = (tile / nt_n) * BM, n0 = (tile % nt_n) * BN;
     const int rg = P.rows[g];
     const int s0 = P.ch == INT_MAX ? 0 : c * P.ch;
@@ -1187,9 +1361,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
 
     // number of k-tiles of this chunk (each k-tile stays inside one slot)
     int KT = 0;
-    for (KCursor cc = cursor_begin(P, S, g, s0, s1); !cc.done; cursor_next_slot(P, S, g, s1, cc))
+    for (KCursor cc = cursor_begin(P, V, g, s0, s1); !cc.done; cursor_next_slot(P, V, g, s1, cc))
       KT += (cc.hi - cc.lo + BK - 1) / BK;
-    KCursor ic = cursor_begin(P, S, g, s0, s1);
+    KCursor ic = cursor_begin(P, V, g, s0, s1);
     auto koa = [&](int k) -> uint32_t { return (uint32_t)k * lda2 + (uint32_t)m0 * 2u; };
     auto kob = [&](int k) -> uint32_t { return (uint32_t)k * ldb2 + (uint32_t)n0 * 2u; };
     const uint32_t va0 = AT::voff(koa, 0), vb0 = BT::voff(kob, 0);
@@ -1209,12 +1383,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
       const int k = live ? ic.k : 0;
       const uint32_t nrow = live ? (uint32_t)(ic.hi - ic.k) : 0u;
       if (p < AT::PER_WAVE) {
-        AT::issue_s(buf_rsrc(a.A + (int64_t)k * a.lda, nrow * lda2), sa, va0, sa_[p], p);
+        AT::issue_s(buf_rsrc(ic.pa + (int64_t)k * a.lda, nrow * lda2), sa, va0, sa_[p], p);
       } else {
-        BT::issue_s(buf_rsrc(a.B + (int64_t)k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb0, sb_[p - AT::PER_WAVE],
+        BT::issue_s(buf_rsrc(ic.pb + (int64_t)k * a.ldb, nrow * ldb2), sa + AT::BYTES, vb0, sb_[p - AT::PER_WAVE],
                     p - AT::PER_WAVE);
       }
-      if (p == AT::PER_WAVE + BT::PER_WAVE - 1 && live) cursor_advance<BK>(P, S, g, s1, ic);
+      if (p == AT::PER_WAVE + BT::PER_WAVE - 1 && live) cursor_advance<BK>(P, V, g, s1, ic);
     };
 
     core.zero();
@@ -1295,7 +1469,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): LDS reads done before the region is refilled
       }
     } else {
-      float* Pt = a.part + (int64_t)(P.pbase[gi] + (c - 1) * tpg + tile) * (BM * BN);
+      float* Pt = a.part + (int64_t)(P.pbase[gi] + (c - 1) * tpg + tile_l) * (BM * BN);
 #pragma unroll
       for (int i = 0; i < CoreT::MB; ++i) {
         const int m = wm * CoreT::WM + i * 32 + l32;
@@ -1329,25 +1503,25 @@ constexpr int kReduceParts = 16;
 
 template <int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
-  __shared__ WgradPlan P;
-  build_wgrad_plan<BM, BN, BK>(a, P);
-  if (P.ch == INT_MAX) return;
-  const int mt_n = a.M / BM, nt_n = a.N / BN, tpg = mt_n * nt_n;
-  // split groups come first in the ordering (largest rows), so walk until C_g == 1
+  // the main kernel's plan (its split groups come first: largest rows)
+  const int* pl = a.plan_out;
+  const int nne = pl[0], ch = pl[1];
+  if (ch == INT_MAX) return;
+  const int nt_n = a.N / BN, tpg = wgrad_call_tiles(a, BM, BN);
   int nsplit = 0;
-  while (nsplit < P.nne && (P.rows[P.order[nsplit]] + P.ch - 1) / P.ch > 1) ++nsplit;
+  while (nsplit < nne && (pl[3 + 3 * nsplit] + ch - 1) / ch > 1) ++nsplit;
   const int total = nsplit * tpg * kReduceParts;
   constexpr int BAND = BM * BN / kReduceParts;  // elements per band
   constexpr int V = BAND / 1024 < 4 ? BAND / 1024 : 4;  // float4 per thread per pass
   static_assert(V >= 1 && BAND % (256 * 4 * V) == 0, "band split");
   for (int t = blockIdx.x; t < total; t += gridDim.x) {
     const int part = t % kReduceParts, tt = t / kReduceParts;
-    const int gi = tt / tpg, tile = tt % tpg;
-    const int g = P.order[gi];
-    const int cg = (P.rows[g] + P.ch - 1) / P.ch;
+    const int gi = tt / tpg, tile_l = tt % tpg, tile = wgrad_tile(a, tile_l);
+    const int g = pl[2 + 3 * gi];
+    const int cg = (pl[3 + 3 * gi] + ch - 1) / ch;
     const int m0 = (tile / nt_n) * BM, n0 = (tile % nt_n) * BN;
     float* Cg = a.C + (int64_t)g * a.gstride;
-    const float* P0 = a.part + (int64_t)(P.pbase[gi] + tile) * (BM * BN);
+    const float* P0 = a.part + (int64_t)(pl[4 + 3 * gi] + tile_l) * (BM * BN);
     const int64_t cstride = (int64_t)tpg * (BM * BN);
     for (int e0 = part * BAND + threadIdx.x * 4; e0 < (part + 1) * BAND; e0 += 256 * 4 * V) {
       float4 s[V];
@@ -1459,11 +1633,11 @@ __global__ __launch_bounds__(256) void f32_rows_kernel(const float* __restrict__
 __global__ __launch_bounds__(256) void f32_wgrad_kernel(const float* __restrict__ A, int lda, const float* __restrict__ B,
                                                         int ldb, int M, int N, const int32_t* __restrict__ off,
                                                         const int32_t* __restrict__ gidx, int S, int G, int64_t n_cap,
-                                                        float* __restrict__ C) {
+                                                        int part, int parts, float* __restrict__ C) {
   const int n = blockIdx.x * 16 + (threadIdx.x & 15);
   const int m = blockIdx.y * 16 + (threadIdx.x >> 4);
   const int g = blockIdx.z;
-  if (n >= N || m >= M) return;
+  if (n >= N || m >= M || m % parts != part) return;
   float s = 0.f;
   for (int j = 0; j < S; ++j) {
     if (gidx[j] != g) continue;
@@ -1510,8 +1684,10 @@ void launch_rows(RowsArgs a, void* ws, hipStream_t st, hipEvent_t e0, hipEvent_t
 // Weight-gradient workspace: a 256-byte header of work counters, then the
 // partial-tile budget of the split (tiles of 256 x 256 fp32).
 constexpr size_t kWgradHeaderBytes = 256;
+constexpr size_t kWgradPlanBytes = 16384;  // the exported plan: 2 + 3 * FOREMOE_MAX_SLOTS ints
 constexpr size_t kWgradPartialTiles = 256;
-constexpr size_t kWgradWorkspaceBytes = kWgradHeaderBytes + kWgradPartialTiles * 256 * 256 * 4;
+constexpr size_t kWgradWorkspaceBytes = kWgradHeaderBytes + kWgradPlanBytes + kWgradPartialTiles * 256 * 256 * 4;
+static_assert((2 + 3 * FOREMOE_MAX_SLOTS) * 4 <= kWgradPlanBytes, "plan export region");
 
 }  // namespace
 }  // namespace foremoe
@@ -1796,35 +1972,68 @@ int foremoe_grouped_ffn_dgrad(const void* dy_perm, const void* save_au, foremoe_
                                    workspace, ws_bytes, stream);
 }
 
-static int wgrad_common(const char* who, const void* A, int lda, const void* B, int ldb, int M, int N,
-                        foremoe_dtype dtype, int32_t S, const int32_t* slot_offset, const int32_t* slot_gidx, int32_t G,
-                        int64_t n_cap, float* dw, void* ws, size_t ws_bytes, void* stream) {
+// One weight-gradient GEMM over n steps' rows (every step: A [n_cap, M],
+// B [n_cap, N], slot table), accumulated into dw [G, M, N].
+static int wgrad_common(const char* who, const foremoe_wgrad_step* steps, int32_t n, int lda, int ldb, int M, int N,
+                        foremoe_dtype dtype, int32_t G, int32_t part, int32_t parts, float* dw, void* ws,
+                        size_t ws_bytes, void* stream) {
   REQUIRE(G >= 1 && G <= FOREMOE_MAX_SLOTS, "%s: G=%d out of range", who, G);
+  REQUIRE(parts >= 1 && parts <= FOREMOE_MAX_WGRAD_STEPS && part >= 0 && part < parts,
+          "%s: part %d of %d out of range", who, part, parts);
   REQUIRE(ws || ws_bytes == 0, "%s: ws is NULL but ws_bytes > 0", who);
-  if (S == 0 || n_cap == 0) return FOREMOE_OK;
-  REQUIRE(A && B && slot_gidx && dw, "%s: NULL buffer", who);
+  REQUIRE(n >= 0 && n <= FOREMOE_MAX_WGRAD_STEPS, "%s: n_steps=%d out of range", who, n);
+  REQUIRE(n == 0 || steps, "%s: steps is NULL", who);
+  int V = 0;
+  bool any = false;
+  for (int m = 0; m < n; ++m) {
+    const foremoe_wgrad_step& t = steps[m];
+    REQUIRE(t.S >= 0 && t.S <= FOREMOE_MAX_SLOTS, "%s: step %d: S=%d out of range", who, m, t.S);
+    REQUIRE(t.n_cap >= 0 && t.n_cap < (int64_t)INT_MAX, "%s: step %d: n_cap out of range", who, m);
+    if (t.S == 0 || t.n_cap == 0) continue;
+    REQUIRE(t.a && t.b && t.slot_offset && t.slot_gidx, "%s: step %d: NULL buffer", who, m);
+    if (dtype == FOREMOE_BF16 && (t.n_cap + 256) * (int64_t)(M > N ? M : N) * 2 >= ((int64_t)1 << 32))
+      return set_error(FOREMOE_EUNSUPPORTED, "%s: step %d: (n_cap + 256) * row bytes must stay below 4 GiB", who, m);
+    V += t.S;
+    any = true;
+  }
+  REQUIRE(V <= FOREMOE_MAX_SLOTS, "%s: %d slots over all steps, at most %d", who, V, FOREMOE_MAX_SLOTS);
+  if (!any) return FOREMOE_OK;
+  REQUIRE(dw, "%s: NULL buffer", who);
   hipStream_t st = (hipStream_t)stream;
   if (dtype == FOREMOE_BF16) {
     WgradArgs a{};
-    a.A = (const uint16_t*)A;
+    int v = 0;
+    for (int m = 0; m < n; ++m) {
+      const foremoe_wgrad_step& t = steps[m];
+      if (t.S == 0 || t.n_cap == 0) continue;  // contributes nothing
+      WgradStep& q = a.step[a.n_steps++];
+      q.A = (const uint16_t*)t.a;
+      q.B = (const uint16_t*)t.b;
+      q.slot_offset = t.slot_offset;
+      q.slot_gidx = t.slot_gidx;
+      q.S = t.S;
+      q.vbase = v;
+      q.n_cap = t.n_cap;
+      v += t.S;
+    }
+    a.V = v;
+    a.tpart = part;
+    a.tparts = parts;
     a.lda = lda;
-    a.B = (const uint16_t*)B;
     a.ldb = ldb;
     a.M = M;
     a.N = N;
-    a.slot_offset = slot_offset;
-    a.slot_gidx = slot_gidx;
-    a.S = S;
     a.G = G;
-    a.n_cap = n_cap;
     a.C = dw;
     a.ldc = N;
     a.gstride = (int64_t)M * N;
     // the workspace header holds the work counters; the rest partial tiles
     const bool has_ws = ws && ws_bytes >= kWgradHeaderBytes;
+    const bool has_part = has_ws && ws_bytes >= kWgradHeaderBytes + kWgradPlanBytes;
     a.sched = has_ws ? (unsigned*)ws : nullptr;
-    a.part = has_ws ? (float*)((char*)ws + kWgradHeaderBytes) : nullptr;
-    const size_t part_bytes = has_ws ? ws_bytes - kWgradHeaderBytes : 0;
+    a.plan_out = has_part ? (int*)((char*)ws + kWgradHeaderBytes) : nullptr;
+    a.part = has_part ? (float*)((char*)ws + kWgradHeaderBytes + kWgradPlanBytes) : nullptr;
+    const size_t part_bytes = has_part ? ws_bytes - kWgradHeaderBytes - kWgradPlanBytes : 0;
     const dim3 grid(persistent_grid()), block(256);
     if (M % 256 == 0 && N % 256 == 0) {
       constexpr int WGM = FM_WG_WGM, WGN = FM_WG_WGN;
@@ -1838,10 +2047,25 @@ static int wgrad_common(const char* who, const void* A, int lda, const void* B, 
       if (a.p_max > 0) hipLaunchKernelGGL((wgrad_reduce_kernel<128, 128, 64>), dim3(persistent_grid() * 4), block, 0, st, a);
     }
   } else {
-    hipLaunchKernelGGL(f32_wgrad_kernel, dim3((N + 15) / 16, (M + 15) / 16, G), dim3(256), 0, st, (const float*)A, lda,
-                       (const float*)B, ldb, M, N, slot_offset, slot_gidx, S, G, n_cap, dw);
+    // fp32 path: one launch per step, in step order (each adds into dw);
+    // a part is the rows m of dw with m % parts == part
+    for (int m = 0; m < n; ++m) {
+      const foremoe_wgrad_step& t = steps[m];
+      if (t.S == 0 || t.n_cap == 0) continue;
+      hipLaunchKernelGGL(f32_wgrad_kernel, dim3((N + 15) / 16, (M + 15) / 16, G), dim3(256), 0, st,
+                         (const float*)t.a, lda, (const float*)t.b, ldb, M, N, t.slot_offset, t.slot_gidx, t.S, G,
+                         t.n_cap, part, parts, dw);
+    }
   }
   return check_launch(who);
+}
+
+static int check_wgrad_shape(const char* who, foremoe_dtype dtype, int32_t d, int32_t F) {
+  REQUIRE(dtype == FOREMOE_F32 || dtype == FOREMOE_BF16, "%s: bad dtype", who);
+  REQUIRE(d >= 1 && F >= 1, "%s: d and F must be positive", who);
+  if (dtype == FOREMOE_BF16 && (d % 128 != 0 || F % 128 != 0))
+    return set_error(FOREMOE_EUNSUPPORTED, "%s: bf16 needs d %% 128 == 0 and F %% 128 == 0 (d=%d, F=%d)", who, d, F);
+  return FOREMOE_OK;
 }
 
 size_t foremoe_ffn_workspace_size(void) { return rows_workspace_bytes(); }
@@ -1851,13 +2075,31 @@ size_t foremoe_wgrad_workspace_size(int32_t d, int32_t F) {
   return kWgradWorkspaceBytes;
 }
 
+int foremoe_ffn_gate_up_wgrad_steps(const foremoe_wgrad_step* steps, int32_t n_steps, foremoe_dtype dtype,
+                                    int32_t d, int32_t F, int32_t G, int32_t part, int32_t parts, float* dw_gate_up,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_wgrad_shape("gate_up_wgrad", dtype, d, F);
+  if (rc) return rc;
+  return wgrad_common("foremoe_ffn_gate_up_wgrad", steps, n_steps, 2 * F, d, 2 * F, d, dtype, G, part, parts,
+                      dw_gate_up, ws, ws_bytes, stream);
+}
+
+int foremoe_ffn_down_wgrad_steps(const foremoe_wgrad_step* steps, int32_t n_steps, foremoe_dtype dtype, int32_t d,
+                                 int32_t F, int32_t G, int32_t part, int32_t parts, float* dw_down, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  int rc = check_wgrad_shape("down_wgrad", dtype, d, F);
+  if (rc) return rc;
+  return wgrad_common("foremoe_ffn_down_wgrad", steps, n_steps, d, F, d, F, dtype, G, part, parts, dw_down, ws,
+                      ws_bytes, stream);
+}
+
 int foremoe_ffn_gate_up_wgrad(const void* d_au, const void* x_perm, foremoe_dtype dtype, int32_t d, int32_t F,
                               int32_t S, const int32_t* slot_offset, const int32_t* slot_gidx, int32_t G,
                               int64_t n_cap, float* dw_gate_up, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_ffn("gate_up_wgrad", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
-  return wgrad_common("foremoe_ffn_gate_up_wgrad", d_au, 2 * F, x_perm, d, 2 * F, d, dtype, S, slot_offset, slot_gidx,
-                      G, n_cap, dw_gate_up, ws, ws_bytes, stream);
+  const foremoe_wgrad_step one = {d_au, x_perm, slot_offset, slot_gidx, S, n_cap};
+  return foremoe_ffn_gate_up_wgrad_steps(&one, 1, dtype, d, F, G, 0, 1, dw_gate_up, ws, ws_bytes, stream);
 }
 
 int foremoe_ffn_down_wgrad(const void* dy_perm, const void* h, foremoe_dtype dtype, int32_t d, int32_t F, int32_t S,
@@ -1865,8 +2107,8 @@ int foremoe_ffn_down_wgrad(const void* dy_perm, const void* h, foremoe_dtype dty
                            float* dw_down, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_ffn("down_wgrad", dtype, d, F, S, n_cap, slot_offset);
   if (rc) return rc;
-  return wgrad_common("foremoe_ffn_down_wgrad", dy_perm, d, h, F, d, F, dtype, S, slot_offset, slot_gidx, G, n_cap,
-                      dw_down, ws, ws_bytes, stream);
+  const foremoe_wgrad_step one = {dy_perm, h, slot_offset, slot_gidx, S, n_cap};
+  return foremoe_ffn_down_wgrad_steps(&one, 1, dtype, d, F, G, 0, 1, dw_down, ws, ws_bytes, stream);
 }
 
 int foremoe_grouped_ffn_wgrad(const void* x_perm, const void* h, const void* dy_perm, const void* d_au,

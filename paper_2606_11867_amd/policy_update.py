@@ -27,6 +27,18 @@ Schedules:
     feed nothing later in the micro-step, so the main stream goes on to the
     next micro-step right after the gate/up dgrad. A caller reading dx (or
     y) waits for the second stream first.
+
+Weight gradients grouped over micro-steps (wgrad_group M > 1): the two
+weight-gradient GEMMs of a group of M consecutive micro-steps run as one
+launch pair over all M micro-steps' rows (App. A.4: the fp32 expert
+gradients accumulate over the micro-steps of an update step; one
+read-modify-write of dW then serves M micro-steps), after the gate/up dgrad
+of the group's last micro-step, on a third stream, while the next group's
+micro-steps run. The operands they read (x_perm, h, dy_perm, d_au and the
+slot offsets) live in a ring of 2M + 1 buffer sets; micro-step i rewrites
+the set of micro-step i - 2M - 1 only after the launch that read it is done.
+finish() launches the weight gradients of an incomplete last group.
+Micro-step indices between start() and finish() must be consecutive.
 """
 from __future__ import annotations
 
@@ -65,13 +77,22 @@ class PolicyUpdate:
 
     split: give the row GEMMs their workspace (a partial last round of tiles
     is cut along K). n_cap: rows of the permuted buffers (default T * K, every
-    pair local; a rank share needs only its largest local pair count)."""
+    pair local; a rank share needs only its largest local pair count).
+    wgrad_group: micro-steps per weight-gradient launch pair (1: every
+    micro-step its own, beside its data-gradient GEMMs; the benchmark uses
+    8: ring of 17 sets of x_perm, h, dy_perm, d_au)."""
 
     def __init__(self, T: int, K: int, d: int, F: int, E: int, G: int, S_max: int, w_gate_up: torch.Tensor,
                  w_down: torch.Tensor, device, split: bool = True, y_dtype=torch.bfloat16,
-                 dx_dtype=torch.bfloat16, n_cap: Optional[int] = None):
+                 dx_dtype=torch.bfloat16, n_cap: Optional[int] = None, wgrad_group: int = 1):
         self.lib = _lib.load()
         self.T, self.K, self.d, self.F, self.E, self.G = T, K, d, F, E, G
+        M = int(wgrad_group)
+        if not 1 <= M <= _lib.MAX_WGRAD_STEPS or M * S_max > _lib.MAX_SLOTS:
+            raise ValueError(f"wgrad_group={M}: 1..{_lib.MAX_WGRAD_STEPS} micro-steps of at most "
+                             f"{_lib.MAX_SLOTS} slots in all")
+        self.M = M
+        self.R = 2 * M + 1 if M > 1 else 2  # weight-gradient operand sets
         self.dev = torch.device(device)
         self.n_cap = T * K if n_cap is None else int(n_cap)
         self.gu, self.dn = w_gate_up, w_down
@@ -85,42 +106,112 @@ class PolicyUpdate:
         def buffer_set():
             return dict(
                 counts=z(E, dt=torch.int32), rep_begin=z(E, 17, dt=torch.int32), slot_count=z(S_max, dt=torch.int32),
-                slot_offset=z(S_max + 1, dt=torch.int32), ws=workspace(T, K, E, dev),
-                x_perm=z(n_cap, d), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32), h=z(n_cap, F),
-                y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d, dt=y_dtype), dy_perm=z(n_cap, d),
-                dgates=z(T, K, dt=torch.float32), d_au=z(n_cap, 2 * F), dx_perm=z(n_cap, d),
-                dx=z(T, d, dt=dx_dtype))
+                ws=workspace(T, K, E, dev), r2p=z(n_cap, dt=torch.int32), p2r=z(T * K, dt=torch.int32),
+                y_perm=z(n_cap, d), au=z(n_cap, 2 * F), y=z(T, d, dt=y_dtype), dgates=z(T, K, dt=torch.float32),
+                dx_perm=z(n_cap, d), dx=z(T, d, dt=dx_dtype))
+
+        def wgrad_set():  # what the weight gradients read
+            return dict(slot_offset=z(S_max + 1, dt=torch.int32), x_perm=z(n_cap, d), h=z(n_cap, F),
+                        dy_perm=z(n_cap, d), d_au=z(n_cap, 2 * F))
 
         # two activation sets: the next micro-step's forward can start while
-        # this one's weight gradients still read its set
+        # this one's weight gradients (or second-stream gathers) still read
+        # its set; the weight-gradient operands in a ring of R sets
         self.sets: List[Dict[str, torch.Tensor]] = [buffer_set(), buffer_set()]
+        self.wsets: List[Dict[str, torch.Tensor]] = [wgrad_set() for _ in range(self.R)]
         self.dw_gate_up = z(G, 2 * F, d, dt=torch.float32)
         self.dw_down = z(G, d, F, dt=torch.float32)
         self.wws = wgrad_workspace(d, F, dev)
         self.rws = ffn_workspace(dev) if split else None
         self.main = torch.cuda.current_stream(dev)
         self.side = torch.cuda.Stream(dev)  # default priority, like every stream here
+        # grouped weight gradients run on a third stream; gdone[k % 4]: group
+        # k's launch pair is done
+        self.wside = torch.cuda.Stream(dev) if M > 1 else None
+        self.gdone = [Event() for _ in range(4)]
         # stream ordering uses events without the system-scope fence (both
         # streams are on this GPU; the fence would cost the recording stream
         # a few microseconds per record)
         self.done = [Event(), Event()]  # side-stream work of the micro-step using set b
-        self._dep = [Event() for _ in range(5)]  # the cross-stream dependencies of one micro-step
+        self._dep = [Event() for _ in range(8)]  # the cross-stream dependencies of one micro-step
         self._join = Event()
         self._ptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.sets]
+        self._wptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.wsets]
+        self.wmeta: List[Optional[MicroStep]] = [None] * self.R  # the micro-step whose operands a set holds
+        self._first: Optional[int] = None  # first and last micro-step run since start() / finish()
+        self._last: Optional[int] = None
+        self._flush_stream = self.main
+
+    def _indices(self, i: int, pipelined: bool):
+        b = i % 2 if pipelined else 0
+        wb = i % self.R if (pipelined or self.M > 1) else 0
+        return b, wb
 
     def set_of(self, i: int, pipelined: bool) -> Dict[str, torch.Tensor]:
         """The activation buffers micro-step i uses under that schedule."""
-        return self.sets[i % 2 if pipelined else 0]
+        b, wb = self._indices(i, pipelined)
+        return {**self.sets[b], **self.wsets[wb]}
+
+    def wgrad_launches_at(self, i: int) -> bool:
+        """Whether micro-step i launches weight gradients (grouped: the last
+        of its group; indices consecutive from a multiple of M)."""
+        return i % self.M == self.M - 1
 
     def start(self) -> None:
         """Before the first pipelined micro-step: nothing to wait for yet."""
-        for e in self.done:
+        for e in self.done + self.gdone:
             e.record(self.side)
 
-    def finish(self) -> None:
-        """Join the side stream into the main stream."""
-        self._join.record(self.side)
-        self._join.wait(self.main)
+    def _group(self, k: int, upto: Optional[int] = None) -> list:
+        """(set, micro-step) of the micro-steps of group k run since start()
+        (up to micro-step `upto`)."""
+        M, R = self.M, self.R
+        if self._first is None:
+            return []
+        hi = k * M + M - 1 if upto is None else min(upto, k * M + M - 1)
+        return [(j % R, self.wmeta[j % R]) for j in range(max(k * M, self._first), hi + 1)]
+
+    def finish(self, ev: Optional[dict] = None) -> bool:
+        """Launch the weight gradients of an incomplete last group, then join
+        the other streams into the main stream. ev: optional timing events of
+        the two weight-gradient phases, around that launch. Returns whether
+        there was such a launch."""
+        flushed = False
+        if self.M > 1 and self._last is not None and not self.wgrad_launches_at(self._last):
+            flushed = True
+            last = self._last
+            members = self._group(last // self.M, last)
+            st = self._flush_stream
+            if st is not self.main:
+                self._join.record(self.main)
+                self._join.wait(st)
+            for phase in ("down_wgrad", "gate_up_wgrad"):
+                if ev is not None and phase in ev:
+                    ev[phase][0].record(st)
+                _lib.check(self._wgrad_call(phase, members, 0, 1)(st.cuda_stream), phase)
+                if ev is not None and phase in ev:
+                    ev[phase][1].record(st)
+        self._first = self._last = None
+        for st in (self.side, self.wside):
+            if st is not None:
+                self._join.record(st)
+                self._join.wait(self.main)
+        return flushed
+
+    def _wgrad_call(self, phase: str, members: list, part: int, parts: int):
+        """The weight-gradient call of one phase over the micro-steps in
+        members, output part `part` of `parts`, as a function of the stream."""
+        lib, d, F, G = self.lib, self.d, self.F, self.G
+        wws, wwsz = self.wws.data_ptr(), self.wws.numel()
+        n = len(members)
+        if phase == "gate_up_wgrad":
+            a, b, fn, dw = "d_au", "x_perm", lib.foremoe_ffn_gate_up_wgrad_steps, self.dw_gate_up.data_ptr()
+        else:
+            a, b, fn, dw = "dy_perm", "h", lib.foremoe_ffn_down_wgrad_steps, self.dw_down.data_ptr()
+        recs = (_lib.WgradStep * n)(*[_lib.WgradStep(self._wptrs[wb][a], self._wptrs[wb][b],
+                                                     self._wptrs[wb]["slot_offset"], ms.plan.slot_gidx.data_ptr(),
+                                                     ms.S, self.n_cap) for wb, ms in members])
+        return lambda q: fn(recs, n, _lib.BF16, d, F, G, part, parts, dw, wws, wwsz, q)
 
     def ops(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
             pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False) -> list:
@@ -133,8 +224,9 @@ class PolicyUpdate:
         later in the micro-step)."""
         lib, main, side = self.lib, self.main, self.side
         overlap = overlap or pipelined
-        bset = i % 2 if pipelined else 0
-        P = self._ptrs[bset]
+        bset, wset = self._indices(i, pipelined)
+        P = {**self._ptrs[bset], **self._wptrs[wset]}
+        M = self.M
         T, K, d, F, G, n_cap = self.T, self.K, self.d, self.F, self.G, self.n_cap
         S = ms.S
         so = P["slot_offset"]
@@ -181,8 +273,15 @@ class PolicyUpdate:
             call("down_wgrad", st, lambda q: lib.foremoe_ffn_down_wgrad(
                 P["dy_perm"], P["h"], BF16, d, F, S, so, gidx, G, n_cap, dwdn, wws, wwsz, q))
 
-        if pipelined:  # set bset was last used two micro-steps ago: its weight gradients must be done
+        if pipelined:
+            # set bset was last used two micro-steps ago: its second-stream
+            # work (M = 1: its weight gradients too) must be done
             ops.append((None, lambda: self.done[bset].wait(main)))
+        k = i // M
+        if pipelined and M > 1 and i - self.R >= (self._first if self._first is not None else i):
+            # set wset was last read by the launch pair of group (i - R) // M
+            gq = ((i - self.R) // M) % 4
+            ops.append((None, lambda: self.gdone[gq].wait(main)))
         call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
             ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
         call("permute", main, lambda q: lib.foremoe_permute(
@@ -202,17 +301,17 @@ class PolicyUpdate:
         call("combine_bwd", main, lambda q: lib.foremoe_combine_bwd(
             ms.dy.data_ptr(), P["y_perm"], BF16, P["p2r"], ms.gates.data_ptr(), T, K, d, n_cap,
             P["dy_perm"], P["dgates"], q))
-        if overlap:
+        if overlap and M == 1:
             dep(side, main)
             down_wgrad(side)
         call("down_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_down_dgrad_timed(
             P["dy_perm"], P["au"], BF16, d, F, S, so, widx, G, dn, n_cap, P["d_au"], rws, rwsz, q, e0, e1))
-        if overlap:
+        if overlap and M == 1:
             dep(side, main)
             gate_up_wgrad(side)
         call("gate_up_dgrad", main, lambda q, e0, e1: lib.foremoe_ffn_gate_up_dgrad_timed(
             P["d_au"], BF16, d, F, S, so, widx, G, gu, n_cap, P["dx_perm"], rws, rwsz, q, e0, e1))
-        if not overlap:  # same order as on the side stream: down, then gate/up
+        if not overlap and M == 1:  # same order as on the side stream: down, then gate/up
             down_wgrad(main)
             gate_up_wgrad(main)
         if overlap and side_gathers >= 1:
@@ -221,11 +320,30 @@ class PolicyUpdate:
             P["dx_perm"], BF16, P["p2r"], T, K, d, n_cap, P["dx"], self.dx_dt, q))
         if pipelined:
             ops.append((None, lambda: self.done[bset].record(side)))
-        elif overlap:
+        if M > 1 and self.wgrad_launches_at(i):
+            # the whole group in one launch pair, on a third stream when overlapped
+            grp = self._group(k, i - 1) + [(wset, ms)] if self._first is not None else [(wset, ms)]
+            wst = self.wside if overlap else main
+            if overlap:
+                dep(wst, main)
+            for phase in ("down_wgrad", "gate_up_wgrad"):
+                call(phase, wst, self._wgrad_call(phase, grp, 0, 1))
+            if pipelined:
+                ops.append((None, lambda: self.gdone[k % 4].record(wst)))
+            elif overlap:
+                dep(main, wst)
+        if overlap and not pipelined:
             dep(main, side)
         return ops
 
     def run(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
             pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False) -> None:
-        for _, op in self.ops(i, ms, ev, overlap, pipelined, side_gathers, fwd_after_side):
+        ops = self.ops(i, ms, ev, overlap, pipelined, side_gathers, fwd_after_side)
+        _, wset = self._indices(i, pipelined)
+        self.wmeta[wset] = ms
+        if self._first is None:
+            self._first = i
+        self._last = i
+        self._flush_stream = self.wside if (overlap or pipelined) and self.M > 1 else self.main
+        for _, op in ops:
             op()

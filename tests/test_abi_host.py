@@ -184,3 +184,36 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and not r.stdout.strip()
+
+
+def test_wgrad_steps_check_their_records(lib):
+    from paper_2606_11867_amd import _lib
+    S = _lib.WgradStep
+    ok = S(FAKE, FAKE, FAKE, FAKE, 4, 64)
+    one = (S * 1)(ok)
+    # bad dtype, shape, G, step count, missing record array: rejected before any launch
+    assert lib.foremoe_ffn_gate_up_wgrad_steps(one, 1, 7, 128, 128, 2, 0, 1, FAKE, None, 0, None) == -1
+    assert lib.foremoe_ffn_gate_up_wgrad_steps(one, 1, 1, 96, 128, 2, 0, 1, FAKE, None, 0, None) == -2
+    assert lib.foremoe_ffn_down_wgrad_steps(one, 1, 1, 128, 128, 0, 0, 1, FAKE, None, 0, None) == -1
+    assert lib.foremoe_ffn_down_wgrad_steps(one, _lib.MAX_WGRAD_STEPS + 1, 1, 128, 128, 2, 0, 1, FAKE, None, 0,
+                                            None) == -1
+    assert lib.foremoe_ffn_down_wgrad_steps(None, 1, 1, 128, 128, 2, 0, 1, FAKE, None, 0, None) == -1
+    # the output part must be one of 1..FOREMOE_MAX_WGRAD_STEPS parts
+    for part, parts in ((0, 0), (2, 2), (-1, 2), (0, _lib.MAX_WGRAD_STEPS + 1)):
+        assert lib.foremoe_ffn_down_wgrad_steps(one, 1, 1, 128, 128, 2, part, parts, FAKE, None, 0, None) == -1
+    # a step with a NULL operand, a bad S, a bad n_cap
+    for bad in (S(None, FAKE, FAKE, FAKE, 4, 64), S(FAKE, FAKE, FAKE, None, 4, 64), S(FAKE, FAKE, FAKE, FAKE, -1, 64),
+                S(FAKE, FAKE, FAKE, FAKE, 4, -5)):
+        assert lib.foremoe_ffn_gate_up_wgrad_steps((S * 2)(ok, bad), 2, 1, 128, 128, 2, 0, 1, FAKE, None, 0,
+                                                   None) == -1
+    # more slots over all steps than one launch can index
+    big = S(FAKE, FAKE, FAKE, FAKE, _lib.MAX_SLOTS // 2 + 1, 64)
+    assert lib.foremoe_ffn_gate_up_wgrad_steps((S * 2)(big, big), 2, 1, 128, 128, 2, 0, 1, FAKE, None, 0,
+                                               None) == -1
+    # 32-bit buffer offsets of one step's operands
+    assert lib.foremoe_ffn_gate_up_wgrad_steps((S * 1)(S(FAKE, FAKE, FAKE, FAKE, 4, 1 << 21)), 1, 1, 2048, 768, 2,
+                                               0, 1, FAKE, None, 0, None) == -2
+    # nothing to do (no steps, or only empty ones): returns before any launch, dW untouched
+    assert lib.foremoe_ffn_gate_up_wgrad_steps(None, 0, 1, 128, 128, 2, 0, 1, None, None, 0, None) == 0
+    empty = (S * 2)(S(None, None, None, None, 0, 64), S(None, None, None, None, 3, 0))
+    assert lib.foremoe_ffn_down_wgrad_steps(empty, 2, 1, 128, 128, 2, 0, 1, None, None, 0, None) == 0

@@ -1,13 +1,18 @@
 """The benchmark's workload end to end at full size: all 16 micro-steps of
 the Qwen3-30B-A3B EP=8 rank share in the policy-update stage (T=16384,
 d=2048, F=768, E=128, top-8, 16 hosted experts + 4 replica slots per
-micro-step), run through the C ABI in exactly the launch configuration the
-benchmark times (paper_2606_11867_amd.policy_update: both workspaces, the
-weight gradients on a second stream, micro-steps pipelined over two
-activation sets). Every micro-step's y, dgates and dx, and the fp32 weight
-gradients accumulated over the 16 micro-steps (Sec. 6.2 main-expert
-accumulation; App. A.4 fp32 gradients), are compared whole-tensor with the
-fp64 oracle: max|err| <= 1e-2 * max|ref| + 1e-3 per tensor."""
+micro-step), run through the C ABI in the launch configurations of
+paper_2606_11867_amd.policy_update (both workspaces, micro-steps pipelined):
+the weight gradients of every micro-step on a second stream beside its
+data-gradient GEMMs, and the benchmark's default: the weight gradients of
+every group of 8 micro-steps in one launch pair over the group's rows, on a
+third stream while the next group runs. Every micro-step's y, dgates and
+dx, and the fp32 weight gradients accumulated over the 16 micro-steps
+(Sec. 6.2 main-expert accumulation; App. A.4 fp32 gradients), are compared
+whole-tensor with the fp64 oracle: max|err| <= 1e-2 * max|ref| + 1e-3 per
+tensor."""
+import functools
+
 import numpy as np
 import pytest
 import torch
@@ -17,11 +22,32 @@ from tests.gpu_helpers import check_close, config_workload, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
+NAME = "qwen3-30b-a3b-ep8-policy-update"
 
-def test_policy_update_full_shape_matches_oracle(gpu):
+
+@functools.lru_cache(maxsize=None)
+def oracle_results():
+    """Per micro-step y, dgates, dx, N and the 16-step accumulated gradients."""
+    w = config_workload(NAME)
+    spec = w.spec
+    T, K, F, d = spec.T, spec.K, spec.F, spec.d
+    gu, dn = w.weights(w.micro[0].plan)
+    G = int(len(w.micro[0].plan.local_experts))
+    rgu = np.zeros((G, 2 * F, d))
+    rdn = np.zeros((G, d, F))
+    per = []
+    for i, m in enumerate(w.micro):
+        fwd = O.layer_forward(w.x(i), m.ids, m.gates, m.plan, gu, dn, n_cap=T * K)
+        bwd = O.layer_backward(fwd, w.dy(i), m.gates, m.plan, gu, dn, T, K, rgu, rdn)
+        per.append(dict(y=fwd["y"], dgates=bwd["dgates"], dx=bwd["dx"], N=int(fwd["slot_offset"][-1])))
+    return per, rgu, rdn
+
+
+@pytest.mark.parametrize("wgrad_group", [1, 8])
+def test_policy_update_full_shape_matches_oracle(gpu, wgrad_group):
     from paper_2606_11867_amd import api
     from paper_2606_11867_amd.policy_update import MicroStep, PolicyUpdate
-    w = config_workload("qwen3-30b-a3b-ep8-policy-update")
+    w = config_workload(NAME)
     spec = w.spec
     T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
     bf = torch.bfloat16
@@ -35,9 +61,9 @@ def test_policy_update_full_shape_matches_oracle(gpu):
                              x=to_dev(w.x(i), bf, gpu), dy=to_dev(w.dy(i), bf, gpu),
                              plan=api.DevicePlan.from_host(m.plan, gpu)))
     pu = PolicyUpdate(T, K, d, F, E, G, max(ms.S for ms in mss), to_dev(gu, bf, gpu), to_dev(dn, bf, gpu), gpu,
-                      split=True)
-    print(f"\n[case] policy update, {len(mss)} micro-steps, pipelined two-stream schedule, both workspaces",
-          flush=True)
+                      split=True, wgrad_group=wgrad_group)
+    print(f"\n[case] policy update, {len(mss)} micro-steps, pipelined two-stream schedule, both workspaces, "
+          f"weight gradients every {wgrad_group} micro-step(s)", flush=True)
     outs = []
     pu.start()
     for i, ms in enumerate(mss):
@@ -45,8 +71,8 @@ def test_policy_update_full_shape_matches_oracle(gpu):
         st = pu.set_of(i, pipelined=True)
         # copies on the second stream, after permute_bwd (which waited for
         # every main-stream kernel of this micro-step); the set's event is
-        # recorded again after them, so micro-step i + 2 reuses the set
-        # only once they are done
+        # recorded again after them, so micro-step i + 2 reuses the set only
+        # once they are done
         with torch.cuda.stream(pu.side):
             outs.append(dict(y=st["y"].clone(), dgates=st["dgates"].clone(), dx=st["dx"].clone(),
                              N=st["slot_offset"][ms.S].clone()))
@@ -55,21 +81,53 @@ def test_policy_update_full_shape_matches_oracle(gpu):
     torch.cuda.synchronize()
     assert not pu.wws[:256].any().item() and not pu.rws[:4096].any().item(), "workspace counters not reset"
 
-    rgu = np.zeros((G, 2 * F, d))
-    rdn = np.zeros((G, d, F))
+    per, rgu, rdn = oracle_results()
     Ns = []
-    for i, m in enumerate(w.micro):
-        fwd = O.layer_forward(w.x(i), m.ids, m.gates, m.plan, gu, dn, n_cap=T * K)
-        bwd = O.layer_backward(fwd, w.dy(i), m.gates, m.plan, gu, dn, T, K, rgu, rdn)
-        N = int(fwd["slot_offset"][-1])
+    for i in range(len(w.micro)):
+        N = per[i]["N"]
         Ns.append(N)
         assert int(outs[i]["N"].item()) == N
         print(f"micro-step {i}: N={N}", flush=True)
-        check_close(f"y[{i}]", to_np(outs[i]["y"]), fwd["y"])
-        check_close(f"dgates[{i}]", to_np(outs[i]["dgates"]), bwd["dgates"])
-        check_close(f"dx[{i}]", to_np(outs[i]["dx"]), bwd["dx"])
+        check_close(f"y[{i}]", to_np(outs[i]["y"]), per[i]["y"])
+        check_close(f"dgates[{i}]", to_np(outs[i]["dgates"]), per[i]["dgates"])
+        check_close(f"dx[{i}]", to_np(outs[i]["dx"]), per[i]["dx"])
     # the heaviest micro-steps (about 42k pairs: several full rounds of tiles
     # plus a split tail) are among those checked
     assert max(Ns) > 40000 and min(Ns) < 4000
     check_close("dW_gate_up (16 micro-steps)", to_np(pu.dw_gate_up), rgu)
     check_close("dW_down (16 micro-steps)", to_np(pu.dw_down), rdn)
+
+
+@pytest.mark.parametrize("n_run", [5, 11])
+def test_grouped_weight_gradients_flush_an_incomplete_group(gpu, n_run):
+    """Micro-steps run in groups of 4 with the two-stream pipelined schedule,
+    a number of them that leaves the last group incomplete (finish() then
+    launches it): the accumulated gradients equal the oracle's over the
+    micro-steps run. Small shapes, several tiles and ragged slots."""
+    from paper_2606_11867_amd import api
+    from paper_2606_11867_amd.policy_update import MicroStep, PolicyUpdate
+    from workload import make_custom
+    w = make_custom(T=1024, d=256, F=128, E=32, K=4, P=4, n_rep=2, seed=57, micro_steps=n_run)
+    spec = w.spec
+    T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
+    bf = torch.bfloat16
+    gu, dn = w.weights(w.micro[0].plan)
+    G = int(w.micro[0].plan.G)
+    mss = [MicroStep(ids=torch.from_numpy(m.ids).to(gpu), gates=torch.from_numpy(m.gates).to(gpu),
+                     x=to_dev(w.x(i), bf, gpu), dy=to_dev(w.dy(i), bf, gpu),
+                     plan=api.DevicePlan.from_host(m.plan, gpu)) for i, m in enumerate(w.micro)]
+    pu = PolicyUpdate(T, K, d, F, E, G, max(ms.S for ms in mss), to_dev(gu, bf, gpu), to_dev(dn, bf, gpu), gpu,
+                      wgrad_group=4)
+    print(f"\n[case] {n_run} micro-steps in groups of 4, pipelined", flush=True)
+    pu.start()
+    for i, ms in enumerate(mss):
+        pu.run(i, ms, pipelined=True, side_gathers=1)
+    pu.finish()
+    torch.cuda.synchronize()
+    rgu = np.zeros((G, 2 * F, d))
+    rdn = np.zeros((G, d, F))
+    for i, m in enumerate(w.micro):
+        fwd = O.layer_forward(w.x(i), m.ids, m.gates, m.plan, gu, dn)
+        O.layer_backward(fwd, w.dy(i), m.gates, m.plan, gu, dn, T, K, rgu, rdn)
+    check_close(f"dW_gate_up ({n_run} micro-steps)", to_np(pu.dw_gate_up), rgu)
+    check_close(f"dW_down ({n_run} micro-steps)", to_np(pu.dw_down), rdn)

@@ -62,10 +62,13 @@ def wgrad_rmw_bytes(G: int, d: int, F: int, acc_elem: int = 4) -> float:
     return 2.0 * G * 3 * d * F * acc_elem
 
 
-def phase_bytes(N: int, g: int, T: int, K: int, d: int, F: int, b: int = 2) -> dict:
+def phase_bytes(N: int, g: int, T: int, K: int, d: int, F: int, b: int = 2, wgrad_group: int = 1) -> dict:
     """Algorithmic HBM bytes of every phase of one policy-update micro-step
     with N local pairs and g non-empty gradient groups (bf16 activations and
-    weights of b bytes, fp32 weight gradients read and written once)."""
+    weights of b bytes, fp32 weight gradients read and written once per
+    weight-gradient launch; a launch over wgrad_group micro-steps that touch
+    the same g groups shares that read-modify-write among them)."""
+    r = 1.0 / wgrad_group
     return {
         "histogram_assign": 4.0 * T * K,
         "permute": permute_bytes(N, T, K, d, b),
@@ -75,8 +78,8 @@ def phase_bytes(N: int, g: int, T: int, K: int, d: int, F: int, b: int = 2) -> d
         "combine_bwd": combine_bwd_bytes(N, T, K, d, b),
         "down_dgrad": b * (N * d + g * d * F + N * 2 * F + N * 2 * F),
         "gate_up_dgrad": b * (N * 2 * F + g * 2 * F * d + N * d),
-        "gate_up_wgrad": b * (N * 2 * F + N * d) + 2.0 * g * 2 * F * d * 4,
-        "down_wgrad": b * (N * d + N * F) + 2.0 * g * d * F * 4,
+        "gate_up_wgrad": b * (N * 2 * F + N * d) + r * 2.0 * g * 2 * F * d * 4,
+        "down_wgrad": b * (N * d + N * F) + r * 2.0 * g * d * F * 4,
         "permute_bwd": permute_bwd_bytes(N, T, K, d, b, b),
     }
 
