@@ -196,7 +196,8 @@ def main() -> int:
         pu.finish()
         torch.cuda.synchronize()
         print(json.dumps({"counters_pass": {"micro_steps": n_micro, "dispatches_per_micro_step": 3, "N": Ns,
-                                            "G": Gs, "T": T, "K": K, "d": d, "F": F}}), flush=True)
+                                            "G": Gs, "T": T, "K": K, "d": d, "F": F, "wgrad_group": M}}),
+              flush=True)
         return 0
 
     overlap = not args.no_overlap
@@ -300,8 +301,8 @@ def main() -> int:
                       "achieved": round(ach, 2), "unit": unit, "frac": round(ach / peak, 4),
                       "tflops": round(fl / t_s / 1e12, 2) if fl else None,
                       "gbs": round(by / t_s / 1e9, 1),
-                      "algorithmic_bytes_per_launch": round(by / args.steps, 0),
-                      "traffic_bytes_per_launch": tr,
+                      "algorithmic_bytes_per_micro_step": round(by / args.steps, 0),
+                      "traffic_bytes_per_micro_step": tr,
                       "traffic_over_algorithmic": round(tr / (by / args.steps), 3) if tr else None}
     # the dominant single-launch kernel, timed live in the timed region on
     # the stream it runs on
@@ -792,8 +793,7 @@ TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic_qwen3_share.json")
 PHASE_KERNELS = [
     ("hist_count_kernel", ["histogram_assign"], "paper_2606_11867_amd/csrc/dispatch.hip"),
     ("hist_scan_assign_kernel", ["histogram_assign"], "paper_2606_11867_amd/csrc/dispatch.hip"),
-    ("permute_rank_kernel", ["permute"], "paper_2606_11867_amd/csrc/dispatch.hip"),
-    ("gather_rows_kernel", ["permute"], "paper_2606_11867_amd/csrc/dispatch.hip"),
+    ("permute_gather_kernel", ["permute"], "paper_2606_11867_amd/csrc/dispatch.hip"),
     ("gemm_rows_kernel<true, 1>", ["gate_up_fwd"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
     ("gemm_rows_kernel<true, 0>", ["down_fwd"], "paper_2606_11867_amd/csrc/grouped_gemm.hip"),
     ("combine_kernel", ["combine", "permute_bwd"], "paper_2606_11867_amd/csrc/dispatch.hip"),
@@ -869,6 +869,7 @@ def summarize_counters(folder: str) -> int:
             rec["kernels"].add(key)
             rec["sources"].add(src)
     T, K, d, F = cp["T"], cp["K"], cp["d"], cp["F"]
+    M = cp.get("wgrad_group", 1)
     alg = collections.defaultdict(float)
     for N, g in zip(cp["N"], cp["G"]):
         for p, by in acc.phase_bytes(N, g, T, K, d, F, wgrad_group=M).items():
@@ -876,14 +877,16 @@ def summarize_counters(folder: str) -> int:
     kernels = {}
     for phase, rec in per_phase.items():
         n_k = len(rec["kernels"])
-        # launches of the phase: dispatches of its kernels / kernels per phase
+        # launches of the phase: dispatches of its kernels / kernels per phase;
+        # a weight-gradient launch serves M micro-steps
         launches = len(rec["fetch"]) // n_k
-        fetch = sum(rec["fetch"]) / launches
-        write = sum(rec["write"]) / launches
-        kernels[phase] = {"kernels": sorted(rec["kernels"]), "launches": launches,
-                          "read_bytes_per_launch": round(fetch), "write_bytes_per_launch": round(write),
-                          "hbm_bytes_per_launch": round(fetch + write),
-                          "algorithmic_bytes_per_launch": round(alg[phase]),
+        per = M if phase in ("gate_up_wgrad", "down_wgrad") else 1
+        fetch = sum(rec["fetch"]) / launches / per
+        write = sum(rec["write"]) / launches / per
+        kernels[phase] = {"kernels": sorted(rec["kernels"]), "launches": launches, "micro_steps_per_launch": per,
+                          "read_bytes_per_micro_step": round(fetch), "write_bytes_per_micro_step": round(write),
+                          "hbm_bytes_per_micro_step": round(fetch + write),
+                          "algorithmic_bytes_per_micro_step": round(alg[phase]),
                           "ratio": round((fetch + write) / alg[phase], 3),
                           "sources": {s: _file_sha(s) for s in sorted(rec["sources"])}}
     out = {"workload": "qwen3-30b-a3b EP=8 rank share, policy-update micro-steps (bench.py --counters-pass: "
@@ -895,13 +898,14 @@ def summarize_counters(folder: str) -> int:
     with open(TRAFFIC_RECORD, "w") as f:
         json.dump(out, f, indent=1)
         f.write("\n")
-    print("| phase | kernels | launches | read MB | written MB | HBM MB | algorithmic MB | ratio |")
-    print("|---|---|---|---|---|---|---|---|")
+    print("| phase | kernels | launches | micro-steps per launch | read MB | written MB | HBM MB | "
+          "algorithmic MB | ratio |")
+    print("|---|---|---|---|---|---|---|---|---|")
     for p, k in out["kernels"].items():
         print(f"| {p} | {', '.join('`' + x + '`' for x in k['kernels'])} | {k['launches']} | "
-              f"{k['read_bytes_per_launch'] / 1e6:.1f} | {k['write_bytes_per_launch'] / 1e6:.1f} | "
-              f"{k['hbm_bytes_per_launch'] / 1e6:.1f} | {k['algorithmic_bytes_per_launch'] / 1e6:.1f} | "
-              f"{k['ratio']:.2f} |")
+              f"{k['micro_steps_per_launch']} | {k['read_bytes_per_micro_step'] / 1e6:.1f} | "
+              f"{k['write_bytes_per_micro_step'] / 1e6:.1f} | {k['hbm_bytes_per_micro_step'] / 1e6:.1f} | "
+              f"{k['algorithmic_bytes_per_micro_step'] / 1e6:.1f} | {k['ratio']:.2f} |")
     return 0
 
 
@@ -910,9 +914,10 @@ PHASES_ORDER = ["histogram_assign", "permute", "gate_up_fwd", "down_fwd", "combi
 
 
 def measured_traffic(phase: str):
-    """HBM bytes per launch of a phase (FETCH_SIZE + WRITE_SIZE, each scaled
-    by a calibration copy) from the committed counter record, or None when
-    there is none or a source of the phase's kernels changed since."""
+    """HBM bytes per micro-step of a phase (FETCH_SIZE + WRITE_SIZE, each
+    scaled by a calibration copy; one launch per micro-step except the
+    grouped weight gradients) from the committed counter record, or None
+    when there is none or a source of the phase's kernels changed since."""
     if not os.path.exists(TRAFFIC_RECORD):
         return None
     with open(TRAFFIC_RECORD) as f:
@@ -922,7 +927,7 @@ def measured_traffic(phase: str):
         return None
     if any(_file_sha(src) != sha for src, sha in k["sources"].items()):
         return None
-    return float(k["hbm_bytes_per_launch"])
+    return float(k["hbm_bytes_per_micro_step"])
 
 
 def cpu_baseline(w, budget_s: float = 10.0) -> dict:
