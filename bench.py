@@ -69,6 +69,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--micro-steps", type=int, default=16, help="distinct micro-steps cycled through")
     ap.add_argument("--no-planner", action="store_true", help="skip the planner report")
+    ap.add_argument("--no-cache-report", action="store_true",
+                    help="skip the warm- vs cold-cache report (one micro-step at a time, one stream)")
     ap.add_argument("--no-transfer", action="store_true", help="skip the transfer-engine report")
     ap.add_argument("--no-other-configs", action="store_true",
                     help="skip the per-phase report of the Mixtral-8x7B and DeepSeek-V3 rank shares")
@@ -360,6 +362,8 @@ def main() -> int:
         ref["permute_frac"] = round(out["permute_gbs"] / ref["copy_gbs"], 4)
         ref["combine_frac"] = round(out["combine_gbs"] / ref["copy_gbs"], 4)
         out["measured_peaks"] = ref
+    if not args.no_cache_report:
+        out["cache"] = cache_report(pu, mss, n_micro, dom, dev)
     if not args.no_planner:
         out["planner"] = planner_report(w, api, dev, n_micro)
     if not args.no_transfer:
@@ -373,6 +377,51 @@ def main() -> int:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def cache_report(pu, mss, n_micro: int, dom: str, dev, flush_mib: int = 512) -> dict:
+    """Each micro-step alone, one stream, with its own weight gradients,
+    every phase between HIP events: once right after a warm-up run of the
+    same micro-step (warm: its inputs, weights and buffers partly in the L2s
+    and the 256 MB Infinity Cache) and once after a flush_mib scratch write
+    (cold: caches hold the scratch buffer). Medians over the micro-steps."""
+    import numpy as np
+    import torch
+
+    from paper_2606_11867_amd.hip_events import Event
+    from paper_2606_11867_amd.policy_update import PHASES
+
+    scratch = torch.empty(flush_mib << 20, dtype=torch.uint8, device=dev)
+    main = pu.main
+
+    def one(i):
+        ev = {p: (Event(timing=True), Event(timing=True)) for p in PHASES}
+        wev = {p: (Event(timing=True), Event(timing=True)) for p in ("gate_up_wgrad", "down_wgrad")}
+        a, b = Event(timing=True), Event(timing=True)
+        a.record(main)
+        pu.run(i, mss[i % n_micro], ev)
+        flushed = pu.finish(ev=wev)
+        b.record(main)
+        torch.cuda.synchronize()
+        ph = {p: ev[p][0].elapsed_time(ev[p][1]) * 1e3 for p in PHASES if p not in wev or not flushed}
+        if flushed:
+            ph.update({p: wev[p][0].elapsed_time(wev[p][1]) * 1e3 for p in wev})
+        return a.elapsed_time(b), ph
+
+    warm, cold = [], []
+    for i in range(n_micro):
+        one(i)
+        warm.append(one(i))
+        scratch.fill_(i & 0xFF)
+        cold.append(one(i))
+    med = lambda xs: float(np.median(xs))  # noqa: E731
+    phases = {p: {"warm_us": round(med([x[1][p] for x in warm]), 2), "cold_us": round(med([x[1][p] for x in cold]), 2)}
+              for p in PHASES}
+    return {"micro_step_ms": {"warm": round(med([x[0] for x in warm]), 4), "cold": round(med([x[0] for x in cold]), 4)},
+            "dominant_kernel": dom, "phases": phases,
+            "method": f"each of the {n_micro} micro-steps alone on one stream with its own weight gradients, "
+                      f"after a warm-up run of itself (warm) or after a {flush_mib} MiB scratch write (cold); "
+                      "medians over the micro-steps"}
 
 
 def reference_peaks(dev) -> dict:
