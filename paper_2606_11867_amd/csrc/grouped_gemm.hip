@@ -58,6 +58,12 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 #ifndef FM_LOAD_SPREAD
 #define FM_LOAD_SPREAD 2
 #endif
+// Wave priority while a k-step's MFMAs issue (0: leave it): the wave that
+// is multiplying wins the SIMD's issue arbitration over the other wave on
+// that SIMD, whose reads and loads then fill the gaps.
+#ifndef FM_SETPRIO
+#define FM_SETPRIO 1
+#endif
 
 enum Epi { kEpiStore = 0, kEpiSwigluFwd = 1, kEpiSwigluBwd = 2 };
 
@@ -333,10 +339,12 @@ struct Core {
     constexpr int NM = MB * NB;
     static_assert(NX >= 0 && NX <= NM, "loads per k-step");
     static_assert(CUR != NXT, "the fragments being read go to another set");
+    if constexpr (FM_SETPRIO > 0) __builtin_amdgcn_s_setprio(FM_SETPRIO);
 #pragma unroll
     for (int s = 0; s < NM; ++s) {
       const int i = s / NB, j = s % NB;
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[CUR][j], f.a[CUR][i], acc[i][j], 0, 0, 0);
+      if (FM_SETPRIO > 0 && s == NM - 1) __builtin_amdgcn_s_setprio(0);
       if (s < MB + NB) {
         if (s < MB) f.a[NXT][s] = AT::frag(nAs, o.a[s], o.ka, nkk);
         else f.b[NXT][s - MB] = BT::frag(nBs, o.b[s - MB], o.kb, nkk);
