@@ -265,14 +265,16 @@ int foremoe_dispatch_static(const int32_t* ids, int64_t T, int32_t K, const fore
  * workspace (optional, these and the input-gradient calls below): NULL, or
  * caller-owned device memory of at least foremoe_ffn_workspace_size()
  * bytes, 256-byte aligned, zero-filled before its first use (the library
- * leaves its counters at zero after every call). With it, a last round of
- * output tiles that would occupy at most 7/16 of the GPU's CUs is cut
- * along K (in GEMMs whose K is at least 2048) into up to 4 pieces (as many
- * as keep at most 7/8 of the CUs busy), each computed by its own
- * workgroup; the last piece to
- * finish adds the pieces' fp32 partial sums in piece order and writes the
- * tile. Results are deterministic either way and equal with and without the
- * workspace up to the fp32 summation order. Calls that share a workspace
+ * leaves its counters at zero after every call). A last round of output
+ * tiles that would occupy at most 7/16 of the GPU's CUs is cut along N into
+ * half-width tiles when the tiles are 256 wide (with or without a
+ * workspace). With the workspace, the (half) tiles of such a round are also
+ * cut along K (in GEMMs whose K is at least 2048) into up to 4 pieces (as
+ * many as keep at most 7/8 of the CUs busy), each computed by its own
+ * workgroup; the last piece to finish adds the pieces' fp32 partial sums in
+ * piece order and writes the tile. Results are deterministic either way and
+ * equal with and without the workspace up to the fp32 summation order.
+ * Calls that share a workspace
  * must not overlap in time (same stream, or ordered by events); after a
  * call that did not complete, zero the workspace again. Too small or
  * misaligned: FOREMOE_EINVAL, nothing launched. Ignored for f32.

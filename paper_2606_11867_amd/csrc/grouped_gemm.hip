@@ -1,8 +1,9 @@
 // Step 4: grouped SwiGLU expert FFN over the local slots (App. A), forward,
 // input gradient and weight gradient.
 //
-// bf16 path: persistent workgroups of 4 wavefronts walk a tile list built on
-// the device from the slot offsets (no host sync). Operand tiles stream from
+// bf16 path: persistent workgroups of 8 wavefronts (4 for 128-wide output
+// tiles) walk a tile list built on the device from the slot offsets (no
+// host sync). Operand tiles stream from
 // HBM straight into LDS with range-checked buffer loads (buffer_load ... lds:
 // no staging registers; rows outside the current slot read as zero and no
 // load can leave its operand) through a ring of LDS stages, and are
@@ -524,7 +525,8 @@ __device__ __forceinline__ void pipelined_k_loop_deep(CoreT& core, char* lds, in
     constexpr int k = decltype(kc)::value;
     CoreT::template load_frags<AT, BT, BK>(f, k, lds, lds + AT::BYTES, o, k);
   });
-  for (int kt = 0; kt < KT;) {
+  int kt = 0;
+  while (kt < KT) {  // kt advances inside the unrolled stage loop
     static_for<0, U>([&](auto phc) {
       constexpr int ph = decltype(phc)::value;
       if (kt >= KT) return;
@@ -833,6 +835,10 @@ __device__ __forceinline__ void rows_epilogue(const RowsArgs& a, const CoreT& co
 #ifndef FM_SPLIT_MIN_K
 #define FM_SPLIT_MIN_K 32
 #endif
+// Cut a small partial last round of 256-wide tiles along N (0: never).
+#ifndef FM_NSPLIT
+#define FM_NSPLIT 1
+#endif
 constexpr int kSplitMax = FM_SPLIT_MAX;    // pieces per tile at most (2..4)
 constexpr int kSplitMinK = FM_SPLIT_MIN_K;  // k-steps a tile needs before it is split
 #ifndef FM_SPLIT_REGION_KIB
@@ -945,18 +951,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   const typename CoreT::template Offsets<AT, BT, BK> offs(wm, wn);
 
   // Whole rounds of G tiles, one tile per workgroup per round. When the last
-  // round is partial (r < G tiles) and a workspace is given, its tiles are
-  // cut along K into `split` pieces each, so that r * split workgroups share
-  // it instead of r. The pieces of one tile run on workgroups of one XCD.
+  // round is partial (r < G tiles), its tiles may be cut into `halves`
+  // along N and, with a workspace, each (half) tile into `split` pieces
+  // along K, so that r * halves * split workgroups share it instead of r.
+  // The halves and pieces of one tile run on workgroups of one XCD.
   const int G = gridDim.x;
   const int v = xcd_virtual_id();
   const int r = total % G;
   int split = 1;
+  // With 256-wide tiles, a partial last round of at most 7/16 G tiles is
+  // first cut along N: each tile becomes two half-width tiles on two
+  // workgroups, with no partial sums (measured faster than cutting the same
+  // round along K). The K split then applies to the (half) tiles.
+  int halves = 1;
+  if constexpr (BN == 256 && FM_NSPLIT) halves = (r > 0 && 16 * r <= 7 * G) ? 2 : 1;
   if (a.sk_part && r > 0 && KT >= kSplitMinK) {
     // as many pieces as keep at most 7/8 of the workgroups busy, so that
     // the round is also spread over the XCDs (below); a split that fills
     // the GPU measured slower than the unsplit round spread out
-    split = (7 * G / 8) / r;
+    split = (7 * G / 8) / (r * halves);
     split = split < kSplitMax ? split : kSplitMax;
     if (split < 2) split = 1;
   }
@@ -964,7 +977,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   // One output tile, k-steps [kb, kb + nk). With split > 1 this is piece q
   // of a tile cut along K: the partial sums go to the workspace and the last
   // piece to arrive adds all pieces in piece order and writes the tile.
-  auto run_tile = [&](int t, int kb, int nk, int q, int pieces, int slot) {
+  // half_c = std::true_type: only columns [h BN / 2, (h + 1) BN / 2) of the
+  // tile, with each wave owning WM x WN / 2 (a tile of the split round cut
+  // along N, below; all of K, no partial sums).
+  auto run_tile = [&](auto half_c, int t, int h, int kb, int nk, int q, int pieces, int slot) {
+    constexpr bool HALF = decltype(half_c)::value;
+    constexpr int BNX = HALF ? BN / 2 : BN;
+    using CoreX = typename std::conditional<HALF, Core<BM, BNX, WGM, WGN, SW>, CoreT>::type;
+    using BTX = typename std::conditional<B_KMAJ, KTile<BNX, BK, NW>, MTile<BNX, BK, NW>>::type;
+    constexpr int STAGEX = AT::BYTES + BTX::BYTES;
     const int mtg = t / n_tiles, nt = t % n_tiles;
     int lo = 0, hi = a.S - 1;
     while (lo < hi) {
@@ -980,8 +1001,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     const int64_t m0 = rbeg + mrel;
     const int w = a.slot_widx[j];
     if (w < 0 || w >= a.W) return;  // invalid weight index: rows left unwritten (every piece skips)
-    const int n0 = nt * BN;           // first output column of the tile grid
-    const int f0 = nt * (BN / 2);     // SwiGLU: first H column
+    const int n0 = nt * BN + h * BNX;          // first output column of the tile grid
+    const int f0 = nt * (BN / 2) + h * (BNX / 2);  // SwiGLU: first H column
 
     // operand A: the slot's rows only (rows past the slot read as zero);
     // operand B: weight matrix w. Lane offsets are fixed for the tile; each
@@ -996,7 +1017,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     auto brow = [&](int r) -> uint32_t {
       if constexpr (B_KMAJ) {
         int wr;
-        if constexpr (SW) wr = r < BN / 2 ? f0 + r : a.F + f0 + (r - BN / 2);
+        if constexpr (SW) wr = r < BNX / 2 ? f0 + r : a.F + f0 + (r - BNX / 2);
         else wr = n0 + r;
         return (uint32_t)wr * ldb2;
       } else {
@@ -1004,58 +1025,76 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
         return (uint32_t)r * ldb2 + (uint32_t)n0 * 2u;
       }
     };
-    const uint32_t va0 = AT::voff(arow, 0), vb0 = BT::voff(brow, 0);
-    uint32_t sa_[AT::PER_WAVE], sb_[BT::PER_WAVE];
+    const uint32_t va0 = AT::voff(arow, 0), vb0 = BTX::voff(brow, 0);
+    uint32_t sa_[AT::PER_WAVE], sb_[BTX::PER_WAVE];
 #pragma unroll
     for (int i = 0; i < AT::PER_WAVE; ++i) sa_[i] = __builtin_amdgcn_readfirstlane(AT::voff(arow, i) - va0);
 #pragma unroll
-    for (int i = 0; i < BT::PER_WAVE; ++i) sb_[i] = __builtin_amdgcn_readfirstlane(BT::voff(brow, i) - vb0);
+    for (int i = 0; i < BTX::PER_WAVE; ++i) sb_[i] = __builtin_amdgcn_readfirstlane(BTX::voff(brow, i) - vb0);
     auto issue = [&](int kt, int p) {
       // stages past the last load nothing (zero-size resources)
       const bool live = kt < nk;
-      const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
+      const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGEX);
       const uint32_t k0 = live ? (uint32_t)((kb + kt) * BK) : 0u;
       if (p < AT::PER_WAVE) {
         AT::issue_s(buf_rsrc(abase + k0, live ? abytes - 2u * k0 : 0u), sa, va0, sa_[p], p);
       } else if constexpr (B_KMAJ) {
-        BT::issue_s(buf_rsrc(bbase + k0, live ? bbytes - 2u * k0 : 0u), sa + AT::BYTES, vb0, sb_[p - AT::PER_WAVE],
-                    p - AT::PER_WAVE);
+        BTX::issue_s(buf_rsrc(bbase + k0, live ? bbytes - 2u * k0 : 0u), sa + AT::BYTES, vb0, sb_[p - AT::PER_WAVE],
+                     p - AT::PER_WAVE);
       } else {
-        BT::issue_s(buf_rsrc(bbase + (int64_t)k0 * a.ldb, live ? bbytes - k0 * ldb2 : 0u), sa + AT::BYTES, vb0,
-                    sb_[p - AT::PER_WAVE], p - AT::PER_WAVE);
+        BTX::issue_s(buf_rsrc(bbase + (int64_t)k0 * a.ldb, live ? bbytes - k0 * ldb2 : 0u), sa + AT::BYTES, vb0,
+                     sb_[p - AT::PER_WAVE], p - AT::PER_WAVE);
       }
     };
 
-    core.zero();
-    pipelined_k_loop<CoreT, AT, BT, BK, NS, SW ? FM_FRAG_DIST_FWD : FM_FRAG_DIST>(core, lds, nk, offs, issue);
-    if (pieces > 1) {
-      // piece q' of tail tile t - full is computed by the workgroup with
-      // slot slot - q + q'; each keeps its partial sums in its own
-      // workspace slot
-      const __amdgpu_buffer_rsrc_t rs = split_rsrc(a.sk_part, (uint32_t)G * (BM * BN * 4));
-      split_store<CoreT, NW>(rs, slot, wave, core);
-      wait_vm<0>();  // this wave's partial sums have reached memory
-      __syncthreads();
-      if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[t - full], 1u) == (unsigned)(pieces - 1);
-      __syncthreads();
-      if (!s_last) return;
-      // the tile's pieces: slots slot - q .. slot - q + pieces - 1
-      {
-        static_assert(NW * kSplitRegionKiB * 1024 <= NS * STAGE, "split pieces must fit in the ring");
-        const __amdgpu_buffer_rsrc_t ts =
-            split_rsrc(a.sk_part + (size_t)(slot - q) * (BM * BN), (uint32_t)pieces * (BM * BN * 4));
-        char* wl = lds + wave * (kSplitRegionKiB * 1024);
-        if (pieces == 2) split_sum<NW, 2>(ts, wave, wl, core);
-        else if (pieces == 3) split_sum<NW, 3>(ts, wave, wl, core);
-        else split_sum<NW, 4>(ts, wave, wl, core);
+    // After the k-loop: a K piece stores its partial sums and the last piece
+    // of its tile to arrive adds all pieces in piece order; then the
+    // epilogue. cr is the full or the half-width core.
+    auto finish_tile = [&](auto& cr) {
+      using C = typename std::remove_reference<decltype(cr)>::type;
+      constexpr int BNC = C::WN * WGN;  // output columns this core covers
+      if (pieces > 1) {
+        // piece q' of this (half) tile is computed by the workgroup with
+        // slot slot - q + q'; each keeps its partial sums in its own
+        // workspace slot
+        const __amdgpu_buffer_rsrc_t rs = split_rsrc(a.sk_part, (uint32_t)G * (BM * BN * 4));
+        split_store<C, NW>(rs, slot, wave, cr);
+        wait_vm<0>();  // this wave's partial sums have reached memory
+        __syncthreads();
+        const int cidx = (t - full) * (BN / BNC) + h;  // arrival counter of this (half) tile
+        if (threadIdx.x == 0) s_last = atomicAdd(&a.sk_count[cidx], 1u) == (unsigned)(pieces - 1);
+        __syncthreads();
+        if (!s_last) return;
+        // the tile's pieces: slots slot - q .. slot - q + pieces - 1
+        {
+          static_assert(NW * kSplitRegionKiB * 1024 <= NS * STAGE, "split pieces must fit in the ring");
+          const __amdgpu_buffer_rsrc_t ts =
+              split_rsrc(a.sk_part + (size_t)(slot - q) * (BM * BNC), (uint32_t)pieces * (BM * BNC * 4));
+          char* wl = lds + wave * (kSplitRegionKiB * 1024);
+          if (pieces == 2) split_sum<NW, 2>(ts, wave, wl, cr);
+          else if (pieces == 3) split_sum<NW, 3>(ts, wave, wl, cr);
+          else split_sum<NW, 4>(ts, wave, wl, cr);
+        }
+        if (threadIdx.x == 0) atomicExch(&a.sk_count[cidx], 0u);  // ready for the next call
       }
-      if (threadIdx.x == 0) atomicExch(&a.sk_count[t - full], 0u);  // ready for the next call
+      static_assert(NW * EpiBytes<C, EPI>::PER_WAVE <= NS * STAGE, "epilogue staging must fit in the ring");
+      __syncthreads();  // every wave is done reading the ring: it now stages the epilogue
+      rows_epilogue<C, EPI>(a, cr, lds + wave * EpiBytes<C, EPI>::PER_WAVE, m0 + wm * C::WM, rend, n0, f0, wn);
+      __syncthreads();  // staging reads done before the next tile's loads overwrite the ring
+    };
+
+    if constexpr (HALF) {
+      static_assert(STAGEX <= STAGE, "the half-width ring fits in the ring");
+      CoreX hc;
+      const typename CoreX::template Offsets<AT, BTX, BK> ox(wm, wn);
+      hc.zero();
+      pipelined_k_loop<CoreX, AT, BTX, BK, NS, SW ? FM_FRAG_DIST_FWD : FM_FRAG_DIST>(hc, lds, nk, ox, issue);
+      finish_tile(hc);
+    } else {
+      core.zero();
+      pipelined_k_loop<CoreT, AT, BT, BK, NS, SW ? FM_FRAG_DIST_FWD : FM_FRAG_DIST>(core, lds, nk, offs, issue);
+      finish_tile(core);
     }
-    static_assert(NW * EpiBytes<CoreT, EPI>::PER_WAVE <= NS * STAGE, "epilogue staging must fit in the ring");
-    __syncthreads();  // every wave is done reading the ring: it now stages the epilogue
-    rows_epilogue<CoreT, EPI>(a, core, lds + wave * EpiBytes<CoreT, EPI>::PER_WAVE, m0 + wm * CoreT::WM, rend, n0,
-                              f0, wn);
-    __syncthreads();  // staging reads done before the next tile's loads overwrite the ring
   };
 
   // Whole rounds take the XCD-grouped ids. A partial last round that keeps
@@ -1065,20 +1104,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   // L2, with the pieces of a split tile on consecutive workgroups of that
   // XCD. The XCDs share only memory, so such a round runs faster on eight
   // partly busy XCDs than on fewer full ones.
-  for (int t = v; t < full; t += G) run_tile(t, 0, KT, 0, 1, v);
-  const int busy = r * split;
+  for (int t = v; t < full; t += G) run_tile(std::false_type{}, t, 0, 0, KT, 0, 1, v);
+  const int per = halves * split;  // workgroups per tile of the last round
+  const int busy = r * per;
   int u = v;
   if (FM_TAIL_SPREAD && G % 8 == 0 && 8 * busy <= 7 * G) {
     const int b = blockIdx.x, tpx = (r + 7) / 8;  // tiles per XCD
-    if (tpx * split <= G / 8) {
-      const int x = b % 8, c = b / 8, j = c / split, i = x * tpx + j;
-      u = (j < tpx && i < r) ? i * split + c % split : busy;  // busy: idle workgroup
+    if (tpx * per <= G / 8) {
+      const int x = b % 8, c = b / 8, j = c / per, i = x * tpx + j;
+      u = (j < tpx && i < r) ? i * per + c % per : busy;  // busy: idle workgroup
     }
   }
   if (u < busy) {
+    // unit u: tile full + u / per, half (u % per) / split, K piece u % split
     const int q = u % split;
     const int kb = q * KT / split, ke = (q + 1) * KT / split;
-    run_tile(full + u / split, kb, ke - kb, q, split, u);
+    if constexpr (BN == 256 && FM_NSPLIT) {
+      if (halves == 2) {
+        run_tile(std::true_type{}, full + u / per, (u % per) / split, kb, ke - kb, q, split, u);
+        return;
+      }
+    }
+    run_tile(std::false_type{}, full + u / split, 0, kb, ke - kb, q, split, u);
   }
 }
 
@@ -1315,7 +1362,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_wgrad_kernel(WgradArgs a)
   using AT = MTile<BM, BK, NW>;
   using BT = MTile<BN, BK, NW>;
   constexpr int STAGE = AT::BYTES + BT::BYTES;
-  constexpr int PER = AT::PER_WAVE + BT::PER_WAVE;
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
   __shared__ WgradPlan P;
 
