@@ -17,13 +17,16 @@ are read and written once per group instead of once per micro-step (the
 fp32 accumulation over micro-steps of App. A.4; the operands stay resident
 in a ring of 17 buffer sets). The streams are not joined at the end of a
 micro-step: the next micro-step's dispatch and forward start on the other
-activation set. permute_bwd (whose output feeds nothing later in the
-micro-step) runs on a second stream, so that the next micro-step's dispatch
-starts right after the gate/up dgrad. --wgrad-group 1 gives every
-micro-step its own weight gradients on the second stream, each beside the
-data-gradient GEMM that does not feed it; --no-pipeline joins the streams
-after every micro-step; --no-overlap runs all phases on one stream;
---side-gathers 0 keeps permute_bwd on the main stream.
+activation set. The combine and permute_bwd (whose outputs feed nothing
+later in the micro-step) run on a second stream, and so does the next
+micro-step's histogram + replica split, beside this micro-step's combine,
+so that the next micro-step starts with its permute right after the gate/up
+dgrad. --wgrad-group 1 gives every micro-step its own weight gradients on
+the second stream, each beside the data-gradient GEMM that does not feed
+it; --no-pipeline joins the streams after every micro-step; --no-overlap
+runs all phases on one stream; --side-gathers 1 keeps the combine, 0 also
+permute_bwd, on the main stream; --no-early-hist runs each histogram at
+the start of its micro-step on the main stream.
 
 All inputs are resident in HBM before timing. A first pass brackets every
 ABI call with HIP events on the stream it runs on, one kernel after
@@ -83,9 +86,12 @@ def parse():
                          "micro-step's forward start while this one's weight gradients run")
     ap.add_argument("--fwd-after-side", action="store_true",
                     help="pipelined: the gate/up forward waits for the previous micro-step's second-stream work")
-    ap.add_argument("--side-gathers", type=int, default=1, choices=(0, 1, 2),
-                    help="with overlap: run permute_bwd (1, the default), and also the combine (2), on the second "
+    ap.add_argument("--side-gathers", type=int, default=2, choices=(0, 1, 2),
+                    help="with overlap: run permute_bwd (1), and also the combine (2, the default), on the second "
                          "stream; 0 keeps both on the main stream")
+    ap.add_argument("--no-early-hist", action="store_true",
+                    help="pipelined: run each micro-step's histogram + replica split at its start on the main "
+                         "stream instead of on the second stream beside the previous micro-step's combine")
     ap.add_argument("--wgrad-group", type=int, default=8,
                     help="micro-steps per weight-gradient launch pair (their fp32 read-modify-write of dW "
                          "is shared; 1: every micro-step its own, beside its data-gradient GEMMs)")
@@ -171,8 +177,12 @@ def main() -> int:
     stream = pu.main
     setup_s = time.time() - t0
 
-    def run_step(i, ev=None, overlap=False, pipelined=False):
-        pu.run(i, mss[i % n_micro], ev, overlap, pipelined, args.side_gathers, args.fwd_after_side)
+    def run_step(i, ev=None, overlap=False, pipelined=False, last=None):
+        # last: the index of the last micro-step of this run (early_hist
+        # launches the next micro-step's histogram only if there is one)
+        nxt = mss[(i + 1) % n_micro] if last is not None and i < last else None
+        pu.run(i, mss[i % n_micro], ev, overlap, pipelined, args.side_gathers, args.fwd_after_side,
+               next_ms=nxt, early_hist=not args.no_early_hist)
 
     # ---- realised per-micro-step sizes (read back once, outside the timed region)
     Ns, Gs = [], []
@@ -194,7 +204,8 @@ def main() -> int:
         pu.start()
         for r in range(2):
             for i in range(n_micro):
-                run_step(r * n_micro + i, overlap=not args.no_overlap, pipelined=not args.no_pipeline)
+                run_step(r * n_micro + i, overlap=not args.no_overlap, pipelined=not args.no_pipeline,
+                         last=2 * n_micro - 1)
         pu.finish()
         torch.cuda.synchronize()
         print(json.dumps({"counters_pass": {"micro_steps": n_micro, "dispatches_per_micro_step": 3, "N": Ns,
@@ -254,18 +265,18 @@ def main() -> int:
 
     pipelined = overlap and not args.no_pipeline
 
-    def timed_step(i, ev):
-        run_step(i, ev, overlap=overlap, pipelined=pipelined)
+    def timed_step(i, ev, last):
+        run_step(i, ev, overlap=overlap, pipelined=pipelined, last=last)
 
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     pu.start()
     for i in range(2):
-        timed_step(i, None)
+        timed_step(i, None, 1)
     pu.finish()
     torch.cuda.synchronize()
     start.record(stream)
     for s in range(args.steps):
-        timed_step(s, evs[s])
+        timed_step(s, evs[s], args.steps - 1)
     pu.finish()
     end.record(stream)
     torch.cuda.synchronize()
@@ -342,7 +353,8 @@ def main() -> int:
                    "n_pairs_min": int(min(Ns)), "n_pairs_max": int(max(Ns)),
                    "backward_overlap": overlap, "tail_split": not args.no_split,
                    "pipelined_micro_steps": pipelined,
-                   "side_gathers": args.side_gathers if overlap else 0, "wgrad_group": M},
+                   "side_gathers": args.side_gathers if overlap else 0, "wgrad_group": M,
+                   "early_hist": bool(pipelined and not args.no_early_hist)},
         "ms_per_step_sequential": round(seq_ms_per_step, 4),
         "roofline": roofline,
         "grouped_ffn_tflops": round(ffn_flop / ffn_s / 1e12, 2),

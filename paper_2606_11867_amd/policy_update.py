@@ -133,6 +133,10 @@ class PolicyUpdate:
         # streams are on this GPU; the fence would cost the recording stream
         # a few microseconds per record)
         self.done = [Event(), Event()]  # side-stream work of the micro-step using set b
+        # early_hist: the histogram + replica split of the micro-step using
+        # set b, run on the second stream during the micro-step before it
+        self.hdone = [Event(), Event()]
+        self._early: set = set()
         self._dep = [Event() for _ in range(8)]  # the cross-stream dependencies of one micro-step
         self._join = Event()
         self._ptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.sets]
@@ -192,6 +196,7 @@ class PolicyUpdate:
                 if ev is not None and phase in ev:
                     ev[phase][1].record(st)
         self._first = self._last = None
+        self._early.clear()
         for st in (self.side, self.wside):
             if st is not None:
                 self._join.record(st)
@@ -214,14 +219,19 @@ class PolicyUpdate:
         return lambda q: fn(recs, n, _lib.BF16, d, F, G, part, parts, dw, wws, wwsz, q)
 
     def ops(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
-            pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False) -> list:
+            pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False,
+            next_ms: Optional[MicroStep] = None, early_hist: bool = False) -> list:
         """The operations of micro-step i on inputs ms, in order, as (phase,
         thunk) pairs (phase None: a stream dependency). ev maps phases to
         (begin, end) timing events (hip_events.Event or torch's): row GEMMs
         carry theirs on the kernel launch, the other phases are bracketed by event records on the stream
         the phase runs on. side_gathers (with overlap): 1 runs permute_bwd,
         2 also the combine, on the second stream (their outputs feed nothing
-        later in the micro-step)."""
+        later in the micro-step). early_hist (pipelined, with next_ms, the
+        inputs of micro-step i + 1): micro-step i + 1's histogram + replica
+        split runs on the second stream after this micro-step's down forward
+        (beside its combine), and micro-step i + 1 starts with the permute;
+        except after the last micro-step of a weight-gradient group."""
         lib, main, side = self.lib, self.main, self.side
         overlap = overlap or pipelined
         bset, wset = self._indices(i, pipelined)
@@ -282,8 +292,12 @@ class PolicyUpdate:
             # set wset was last read by the launch pair of group (i - R) // M
             gq = ((i - self.R) // M) % 4
             ops.append((None, lambda: self.gdone[gq].wait(main)))
-        call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
-            ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
+        early = pipelined and early_hist
+        if early and i in self._early:  # run during micro-step i - 1
+            ops.append((None, lambda: self.hdone[bset].wait(main)))
+        else:
+            call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
+                ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
         call("permute", main, lambda q: lib.foremoe_permute(
             ms.x.data_ptr(), BF16, T, d, ms.ids.data_ptr(), K, cp, P["rep_begin"], so, n_cap, P["x_perm"],
             P["r2p"], P["p2r"], P["ws"], wsz, q))
@@ -294,6 +308,28 @@ class PolicyUpdate:
             P["x_perm"], BF16, d, F, S, so, widx, G, gu, n_cap, P["h"], P["au"], rws, rwsz, q, e0, e1))
         call("down_fwd", main, lambda q, e0, e1: lib.foremoe_ffn_down_fwd_timed(
             P["h"], BF16, d, F, S, so, widx, G, dn, n_cap, P["y_perm"], rws, rwsz, q, e0, e1))
+        if early and next_ms is not None and not (M > 1 and self.wgrad_launches_at(i)):
+            # (not after the last micro-step of a group: the group's weight-
+            # gradient kernels, launched at its end, hold every CU for a while,
+            # and the next micro-step's own histogram, on the main stream,
+            # then takes that wait instead of its gate/up forward)
+            # micro-step i + 1's sets: the activation set of micro-step i - 1,
+            # whose main-stream kernels are done once this micro-step's have
+            # started, and a weight-gradient set last read by the grouped
+            # launch of micro-step i + 1 - R (M > 1)
+            j = i + 1
+            nb, nwb = self._indices(j, pipelined)
+            NP = {**self._ptrs[nb], **self._wptrs[nwb]}
+            dep(side, main)
+            if M > 1 and j - self.R >= (self._first if self._first is not None else i):
+                hq = ((j - self.R) // M) % 4
+                ops.append((None, lambda: self.gdone[hq].wait(side)))
+            ncp = ctypes.byref(next_ms.cplan)
+            ops.append(("histogram_assign", lambda: _lib.check(lib.foremoe_histogram_assign(
+                next_ms.ids.data_ptr(), T, K, ncp, NP["counts"], NP["rep_begin"], NP["slot_count"],
+                NP["slot_offset"], NP["ws"], self.sets[nb]["ws"].numel(), side.cuda_stream), "histogram_assign")))
+            ops.append((None, lambda: self.hdone[nb].record(side)))
+            ops.append((None, lambda: self._early.add(j)))
         if overlap and side_gathers >= 2:
             dep(side, main)
         call("combine", side if overlap and side_gathers >= 2 else main, lambda q: lib.foremoe_combine(
@@ -337,8 +373,9 @@ class PolicyUpdate:
         return ops
 
     def run(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
-            pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False) -> None:
-        ops = self.ops(i, ms, ev, overlap, pipelined, side_gathers, fwd_after_side)
+            pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False,
+            next_ms: Optional[MicroStep] = None, early_hist: bool = False) -> None:
+        ops = self.ops(i, ms, ev, overlap, pipelined, side_gathers, fwd_after_side, next_ms, early_hist)
         _, wset = self._indices(i, pipelined)
         self.wmeta[wset] = ms
         if self._first is None:

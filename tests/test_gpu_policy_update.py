@@ -4,10 +4,12 @@ d=2048, F=768, E=128, top-8, 16 hosted experts + 4 replica slots per
 micro-step), run through the C ABI in the launch configurations of
 paper_2606_11867_amd.policy_update (both workspaces, micro-steps pipelined):
 the weight gradients of every micro-step on a second stream beside its
-data-gradient GEMMs, and the benchmark's default: the weight gradients of
-every group of 8 micro-steps in one launch pair over the group's rows, on a
-third stream while the next group runs. Every micro-step's y, dgates and
-dx, and the fp32 weight gradients accumulated over the 16 micro-steps
+data-gradient GEMMs; the weight gradients of every group of 8 micro-steps
+in one launch pair over the group's rows, on a third stream while the next
+group runs; and the benchmark's default: that grouped schedule with each
+micro-step's histogram + replica split run on the second stream during the
+micro-step before it, and the combine on the second stream. Every
+micro-step's y, dgates and dx, and the fp32 weight gradients accumulated over the 16 micro-steps
 (Sec. 6.2 main-expert accumulation; App. A.4 fp32 gradients), are compared
 whole-tensor with the fp64 oracle: max|err| <= 1e-2 * max|ref| + 1e-3 per
 tensor."""
@@ -43,8 +45,9 @@ def oracle_results():
     return per, rgu, rdn
 
 
-@pytest.mark.parametrize("wgrad_group", [1, 8])
-def test_policy_update_full_shape_matches_oracle(gpu, wgrad_group):
+@pytest.mark.parametrize("wgrad_group,early_hist,side_gathers", [(1, False, 1), (8, False, 1), (8, True, 2)],
+                         ids=["wgrad-each", "wgrad-group8", "wgrad-group8-early-hist-combine-side"])
+def test_policy_update_full_shape_matches_oracle(gpu, wgrad_group, early_hist, side_gathers):
     from paper_2606_11867_amd import api
     from paper_2606_11867_amd.policy_update import MicroStep, PolicyUpdate
     w = config_workload(NAME)
@@ -63,14 +66,16 @@ def test_policy_update_full_shape_matches_oracle(gpu, wgrad_group):
     pu = PolicyUpdate(T, K, d, F, E, G, max(ms.S for ms in mss), to_dev(gu, bf, gpu), to_dev(dn, bf, gpu), gpu,
                       split=True, wgrad_group=wgrad_group)
     print(f"\n[case] policy update, {len(mss)} micro-steps, pipelined two-stream schedule, both workspaces, "
-          f"weight gradients every {wgrad_group} micro-step(s)", flush=True)
+          f"weight gradients every {wgrad_group} micro-step(s), early histogram {early_hist}, "
+          f"second-stream gathers {side_gathers}", flush=True)
     outs = []
     pu.start()
     for i, ms in enumerate(mss):
-        pu.run(i, ms, pipelined=True, side_gathers=1)
+        nxt = mss[i + 1] if i + 1 < len(mss) else None
+        pu.run(i, ms, pipelined=True, side_gathers=side_gathers, next_ms=nxt, early_hist=early_hist)
         st = pu.set_of(i, pipelined=True)
         # copies on the second stream, after permute_bwd (which waited for
-        # every main-stream kernel of this micro-step); the set's event is
+        # every main-stream kernel of this micro-step) and the combine; the set's event is
         # recorded again after them, so micro-step i + 2 reuses the set only
         # once they are done
         with torch.cuda.stream(pu.side):
