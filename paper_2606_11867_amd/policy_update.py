@@ -136,7 +136,7 @@ class PolicyUpdate:
         # early_hist: the histogram + replica split of the micro-step using
         # set b, run on the second stream during the micro-step before it
         self.hdone = [Event(), Event()]
-        self._early: set = set()
+        self._early: Dict[int, MicroStep] = {}  # micro-step index -> the inputs its early launch used
         self._dep = [Event() for _ in range(8)]  # the cross-stream dependencies of one micro-step
         self._join = Event()
         self._ptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.sets]
@@ -293,9 +293,11 @@ class PolicyUpdate:
             gq = ((i - self.R) // M) % 4
             ops.append((None, lambda: self.gdone[gq].wait(main)))
         early = pipelined and early_hist
-        if early and i in self._early:  # run during micro-step i - 1
+        run_hist = True
+        if i in self._early:  # launched during micro-step i - 1: its writes land first
             ops.append((None, lambda: self.hdone[bset].wait(main)))
-        else:
+            run_hist = self._early.pop(i) is not ms  # other inputs than announced: run it again
+        if run_hist:
             call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
                 ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
         call("permute", main, lambda q: lib.foremoe_permute(
@@ -329,7 +331,7 @@ class PolicyUpdate:
                 next_ms.ids.data_ptr(), T, K, ncp, NP["counts"], NP["rep_begin"], NP["slot_count"],
                 NP["slot_offset"], NP["ws"], self.sets[nb]["ws"].numel(), side.cuda_stream), "histogram_assign")))
             ops.append((None, lambda: self.hdone[nb].record(side)))
-            ops.append((None, lambda: self._early.add(j)))
+            ops.append((None, lambda: self._early.__setitem__(j, next_ms)))
         if overlap and side_gathers >= 2:
             dep(side, main)
         call("combine", side if overlap and side_gathers >= 2 else main, lambda q: lib.foremoe_combine(

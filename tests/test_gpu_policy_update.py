@@ -136,3 +136,54 @@ def test_grouped_weight_gradients_flush_an_incomplete_group(gpu, n_run):
         O.layer_backward(fwd, w.dy(i), m.gates, m.plan, gu, dn, T, K, rgu, rdn)
     check_close(f"dW_gate_up ({n_run} micro-steps)", to_np(pu.dw_gate_up), rgu)
     check_close(f"dW_down ({n_run} micro-steps)", to_np(pu.dw_down), rdn)
+
+
+def test_early_histogram_falls_back_when_inputs_differ(gpu):
+    """The benchmark's schedule (pipelined, combine and the next micro-step's
+    histogram + replica split on the second stream, weight gradients in
+    groups, here of 3) where micro-steps 0 and 3 announce other inputs for
+    their successor than the ones that then run: that successor waits for
+    the early launch and runs its own on the main stream. Micro-steps 1 and
+    4 announce the right ones (early launch used); 2 and 5 end a group (no
+    early launch). Every micro-step's y, dgates and dx and the accumulated
+    gradients match the oracle. Small shapes, several tiles and ragged
+    slots."""
+    from paper_2606_11867_amd import api
+    from paper_2606_11867_amd.policy_update import MicroStep, PolicyUpdate
+    from workload import make_custom
+    w = make_custom(T=1024, d=256, F=128, E=32, K=4, P=4, n_rep=2, seed=61, micro_steps=6)
+    spec = w.spec
+    T, K, d, F, E = spec.T, spec.K, spec.d, spec.F, spec.E
+    bf = torch.bfloat16
+    gu, dn = w.weights(w.micro[0].plan)
+    G = int(w.micro[0].plan.G)
+    mss = [MicroStep(ids=torch.from_numpy(m.ids).to(gpu), gates=torch.from_numpy(m.gates).to(gpu),
+                     x=to_dev(w.x(i), bf, gpu), dy=to_dev(w.dy(i), bf, gpu),
+                     plan=api.DevicePlan.from_host(m.plan, gpu)) for i, m in enumerate(w.micro)]
+    n = len(mss)
+    pu = PolicyUpdate(T, K, d, F, E, G, max(ms.S for ms in mss), to_dev(gu, bf, gpu), to_dev(dn, bf, gpu), gpu,
+                      wgrad_group=3)
+    print(f"\n[case] {n} micro-steps, early histogram, wrong successor announced by micro-steps 0 and 3", flush=True)
+    outs = []
+    pu.start()
+    for i, ms in enumerate(mss):
+        nxt = None if i + 1 == n else (mss[(i + 3) % n] if i % 3 == 0 else mss[i + 1])
+        if nxt is not None and i % 3 != 2:  # an early launch happens after every micro-step but a group's last
+            assert pu.wgrad_launches_at(i) is False
+        pu.run(i, ms, pipelined=True, side_gathers=2, next_ms=nxt, early_hist=True)
+        st = pu.set_of(i, pipelined=True)
+        with torch.cuda.stream(pu.side):
+            outs.append(dict(y=st["y"].clone(), dgates=st["dgates"].clone(), dx=st["dx"].clone()))
+        pu.done[i % 2].record(pu.side)
+    pu.finish()
+    torch.cuda.synchronize()
+    rgu = np.zeros((G, 2 * F, d))
+    rdn = np.zeros((G, d, F))
+    for i, m in enumerate(w.micro):
+        fwd = O.layer_forward(w.x(i), m.ids, m.gates, m.plan, gu, dn)
+        bwd = O.layer_backward(fwd, w.dy(i), m.gates, m.plan, gu, dn, T, K, rgu, rdn)
+        check_close(f"y[{i}]", to_np(outs[i]["y"]), fwd["y"])
+        check_close(f"dgates[{i}]", to_np(outs[i]["dgates"]), bwd["dgates"])
+        check_close(f"dx[{i}]", to_np(outs[i]["dx"]), bwd["dx"])
+    check_close("dW_gate_up", to_np(pu.dw_gate_up), rgu)
+    check_close("dW_down", to_np(pu.dw_down), rdn)
