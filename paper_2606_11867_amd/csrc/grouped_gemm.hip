@@ -974,12 +974,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
     if (split < 2) split = 1;
   }
   const int full = total - r;  // tiles of the whole rounds
-  // One output tile, k-steps [kb, kb + nk). With split > 1 this is piece q
-  // of a tile cut along K: the partial sums go to the workspace and the last
-  // piece to arrive adds all pieces in piece order and writes the tile.
-  // half_c = std::true_type: only columns [h BN / 2, (h + 1) BN / 2) of the
-  // tile, with each wave owning WM x WN / 2 (a tile of the split round cut
-  // along N, below; all of K, no partial sums).
+  // One output tile, k-steps [kb, kb + nk). With pieces > 1 this is piece q
+  // of a (half) tile cut along K: the partial sums go to the workspace and
+  // the last piece to arrive adds all pieces in piece order and writes the
+  // (half) tile. half_c = std::true_type: only columns
+  // [h BN / 2, (h + 1) BN / 2) of tile t, each wave owning WM x WN / 2 (a
+  // tile of the last round cut along N, below).
   auto run_tile = [&](auto half_c, int t, int h, int kb, int nk, int q, int pieces, int slot) {
     constexpr bool HALF = decltype(half_c)::value;
     constexpr int BNX = HALF ? BN / 2 : BN;
@@ -1101,8 +1101,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_rows_kernel(RowsArgs a) {
   // at most 7/8 of the workgroups busy is spread over all eight XCDs
   // instead, in blocks: XCD x takes tiles [x * tpx, (x + 1) * tpx), so that
   // neighbouring tiles (which share operand rows or weights) still share an
-  // L2, with the pieces of a split tile on consecutive workgroups of that
-  // XCD. The XCDs share only memory, so such a round runs faster on eight
+  // L2, with the halves and pieces of a tile on consecutive workgroups of
+  // that XCD. The XCDs share only memory, so such a round runs faster on eight
   // partly busy XCDs than on fewer full ones.
   for (int t = v; t < full; t += G) run_tile(std::false_type{}, t, 0, 0, KT, 0, 1, v);
   const int per = halves * split;  // workgroups per tile of the last round
