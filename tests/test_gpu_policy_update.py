@@ -138,16 +138,19 @@ def test_grouped_weight_gradients_flush_an_incomplete_group(gpu, n_run):
     check_close(f"dW_down ({n_run} micro-steps)", to_np(pu.dw_down), rdn)
 
 
-def test_early_histogram_falls_back_when_inputs_differ(gpu):
+@pytest.mark.parametrize("wgrad_group", [1, 3])
+def test_early_histogram_falls_back_when_inputs_differ(gpu, wgrad_group):
     """The benchmark's schedule (pipelined, combine and the next micro-step's
-    histogram + replica split on the second stream, weight gradients in
-    groups, here of 3) where micro-steps 0 and 3 announce other inputs for
-    their successor than the ones that then run: that successor waits for
-    the early launch and runs its own on the main stream. Micro-steps 1 and
-    4 announce the right ones (early launch used); 2 and 5 end a group (no
-    early launch). Every micro-step's y, dgates and dx and the accumulated
-    gradients match the oracle. Small shapes, several tiles and ragged
-    slots."""
+    histogram + replica split on the second stream) where micro-steps 0 and
+    3 announce other inputs for their successor than the ones that then
+    run: that successor waits for the early launch and runs its own on the
+    main stream; the others announce the right ones. Weight gradients in
+    groups of 3 (micro-steps 2 and 5 end a group and launch nothing early)
+    or of 1 (each micro-step's own on the second stream, operand sets in a
+    ring of 2, every micro-step but the last launches its successor's
+    histogram early). Every micro-step's y, dgates and dx and the
+    accumulated gradients match the oracle. Small shapes, several tiles and
+    ragged slots."""
     from paper_2606_11867_amd import api
     from paper_2606_11867_amd.policy_update import MicroStep, PolicyUpdate
     from workload import make_custom
@@ -162,14 +165,15 @@ def test_early_histogram_falls_back_when_inputs_differ(gpu):
                      plan=api.DevicePlan.from_host(m.plan, gpu)) for i, m in enumerate(w.micro)]
     n = len(mss)
     pu = PolicyUpdate(T, K, d, F, E, G, max(ms.S for ms in mss), to_dev(gu, bf, gpu), to_dev(dn, bf, gpu), gpu,
-                      wgrad_group=3)
-    print(f"\n[case] {n} micro-steps, early histogram, wrong successor announced by micro-steps 0 and 3", flush=True)
+                      wgrad_group=wgrad_group)
+    print(f"\n[case] {n} micro-steps, weight gradients in groups of {wgrad_group}, early histogram, wrong "
+          "successor announced by micro-steps 0 and 3", flush=True)
     outs = []
     pu.start()
     for i, ms in enumerate(mss):
         nxt = None if i + 1 == n else (mss[(i + 3) % n] if i % 3 == 0 else mss[i + 1])
-        if nxt is not None and i % 3 != 2:  # an early launch happens after every micro-step but a group's last
-            assert pu.wgrad_launches_at(i) is False
+        if wgrad_group == 3:  # micro-steps 0, 1, 3 and 4 launch their successor's histogram early
+            assert pu.wgrad_launches_at(i) == (i % 3 == 2)
         pu.run(i, ms, pipelined=True, side_gathers=2, next_ms=nxt, early_hist=True)
         st = pu.set_of(i, pipelined=True)
         with torch.cuda.stream(pu.side):
