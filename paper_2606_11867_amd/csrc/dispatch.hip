@@ -403,7 +403,11 @@ __global__ __launch_bounds__(kHistThreads) void hist_scan_assign_kernel(
 // key's list is its block's base (the scanned partial counts) plus its rank
 // within the block (written by the count kernel). The wavefront then copies
 // the rows of its local pairs, kRowsPerWave at a time: every 16-byte load of
-// a group is issued before its stores.
+// a group is issued before its stores. With few pairs (fewer groups of 64
+// than 16 wavefronts per CU) nsub wavefronts share a group:
+// each finds the group's rows, the first writes the index maps, and
+// wavefront s of the group copies the local pairs whose index among the
+// group's local pairs is s modulo nsub.
 // ---------------------------------------------------------------------------
 constexpr int kRowsPerWave = 4;
 constexpr int kVecPerLane = 4;  // 16-byte vectors per lane per row and pass
@@ -426,7 +430,7 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
     int nkeys, int R_max, const int32_t* __restrict__ block_base, const uint16_t* __restrict__ rank,
     const int32_t* __restrict__ rep_begin, const int32_t* __restrict__ rep_slot, const int32_t* __restrict__ row_off,
     int S, const int32_t* __restrict__ n_rows_dev, int64_t n_cap, int32_t* __restrict__ pair_to_row,
-    int32_t* __restrict__ row_to_pair, uint4* __restrict__ x_perm, int32_t* __restrict__ status) {
+    int32_t* __restrict__ row_to_pair, uint4* __restrict__ x_perm, int32_t* __restrict__ status, int nsub) {
   __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
   load_sources(km, s_tb);
   __syncthreads();
@@ -435,7 +439,10 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   const int RS = R_max + 1;
   const uint32_t row_bytes = (uint32_t)(vec_per_row * 16);
-  for (int64_t g = wave; g * 64 < npairs; g += nwaves) {
+  const int64_t ngroups = (npairs + 63) / 64;
+  for (int64_t W = wave; W < ngroups * nsub; W += nwaves) {
+    const int64_t g = W / nsub;
+    const int sub = (int)(W % nsub);
     const int64_t p = g * 64 + lane;
     int row = -1, tok = -1;
     if (p < npairs) {
@@ -451,13 +458,15 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
           if (rr >= 0 && rr < n_cap) {
             row = (int)rr;
             tok = (int)(p / km.K);
-            row_to_pair[row] = (int32_t)p;
+            if (sub == 0) row_to_pair[row] = (int32_t)p;
           }
         }
       }
-      pair_to_row[p] = row;
+      if (sub == 0) pair_to_row[p] = row;
     }
-    uint64_t local = __ballot(row >= 0);
+    // this wavefront's share of the group's local pairs
+    const uint64_t all = __ballot(row >= 0);
+    uint64_t local = __ballot(row >= 0 && lanes_below(all) % nsub == sub);
     while (local) {
       int rows[kRowsPerWave], toks[kRowsPerWave];
 #pragma unroll
@@ -943,9 +952,18 @@ static int permute_impl(const void* x, foremoe_dtype dtype, int64_t T, int32_t d
   const KeyMap km{plan->E, n_src, K, n_src >= 2 ? plan->src_token_begin : nullptr};
   const int64_t vpr = (int64_t)d * esz / 16;
   const int64_t groups = (npairs + 63) / 64;
-  hipLaunchKernelGGL(permute_gather_kernel, dim3(gather_grid(groups)), dim3(256), 0, st, (const uint4*)x, vpr, ids,
-                     npairs, km, nkeys, plan->R_max, base, rank, rep_begin, rep_slot, row_off, n_src * plan->S,
-                     slot_offset + plan->S, n_cap, pair_to_row, row_to_pair, (uint4*)x_perm, status);
+  // wavefronts per group of 64 pairs: enough to give the chip 16 per CU
+  // when there are fewer groups, at most 16 (measured on the benchmark's
+  // shares, 8 / 16 / 32 per CU: Qwen3 EP=8 permute 28.0 / 26.6 / 27.9 us,
+  // Mixtral-8x7B 28.2 / 28.1 / 28.1 us, from 89 us with one wavefront per
+  // group, DeepSeek-V3 EP=32 87 / 87 / 85 us)
+  const int64_t want = (int64_t)num_cus() * 16;
+  int nsub = 1;
+  if (groups > 0 && groups < want) nsub = (int)((want + groups - 1) / groups);  // no pairs: one, idle
+  nsub = nsub > 16 ? 16 : nsub;
+  hipLaunchKernelGGL(permute_gather_kernel, dim3(gather_grid(groups * nsub)), dim3(256), 0, st, (const uint4*)x, vpr,
+                     ids, npairs, km, nkeys, plan->R_max, base, rank, rep_begin, rep_slot, row_off, n_src * plan->S,
+                     slot_offset + plan->S, n_cap, pair_to_row, row_to_pair, (uint4*)x_perm, status, nsub);
   return check_launch("foremoe_permute");
 }
 
