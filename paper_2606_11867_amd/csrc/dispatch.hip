@@ -403,11 +403,15 @@ __global__ __launch_bounds__(kHistThreads) void hist_scan_assign_kernel(
 // key's list is its block's base (the scanned partial counts) plus its rank
 // within the block (written by the count kernel). The wavefront then copies
 // the rows of its local pairs, kRowsPerWave at a time: every 16-byte load of
-// a group is issued before its stores. With few pairs (fewer groups of 64
-// than 16 wavefronts per CU) nsub wavefronts share a group:
-// each finds the group's rows, the first writes the index maps, and
-// wavefront s of the group copies the local pairs whose index among the
-// group's local pairs is s modulo nsub.
+// a group is issued before its stores. A group is shared by nsub * ncol
+// wavefronts, each of which finds the group's rows (the first writes the
+// index maps): with few pairs (fewer groups of 64 than 16 wavefronts per
+// CU) wavefront s of nsub copies the local pairs whose index among the
+// group's local pairs is s modulo nsub; with rows wider than one copy pass
+// (64 * kVecPerLane vectors), wavefront c of ncol copies passes c, c +
+// ncol, ... of each of its rows, so that no wavefront waits for the loads
+// of one pass before issuing the next (with every wavefront in step, all
+// of them would read, then all write, and the two would not overlap).
 // ---------------------------------------------------------------------------
 constexpr int kRowsPerWave = 4;
 constexpr int kVecPerLane = 4;  // 16-byte vectors per lane per row and pass
@@ -430,7 +434,8 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
     int nkeys, int R_max, const int32_t* __restrict__ block_base, const uint16_t* __restrict__ rank,
     const int32_t* __restrict__ rep_begin, const int32_t* __restrict__ rep_slot, const int32_t* __restrict__ row_off,
     int S, const int32_t* __restrict__ n_rows_dev, int64_t n_cap, int32_t* __restrict__ pair_to_row,
-    int32_t* __restrict__ row_to_pair, uint4* __restrict__ x_perm, int32_t* __restrict__ status, int nsub) {
+    int32_t* __restrict__ row_to_pair, uint4* __restrict__ x_perm, int32_t* __restrict__ status, int nsub,
+    int ncol) {
   __shared__ int s_tb[FOREMOE_MAX_SOURCES + 1];
   load_sources(km, s_tb);
   __syncthreads();
@@ -440,9 +445,10 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
   const int RS = R_max + 1;
   const uint32_t row_bytes = (uint32_t)(vec_per_row * 16);
   const int64_t ngroups = (npairs + 63) / 64;
-  for (int64_t W = wave; W < ngroups * nsub; W += nwaves) {
-    const int64_t g = W / nsub;
-    const int sub = (int)(W % nsub);
+  const int per = nsub * ncol;  // wavefronts per group
+  for (int64_t W = wave; W < ngroups * per; W += nwaves) {
+    const int64_t g = W / per;
+    const int sub = (int)(W % per) / ncol, col = (int)(W % per) % ncol;
     const int64_t p = g * 64 + lane;
     int row = -1, tok = -1;
     if (p < npairs) {
@@ -458,11 +464,11 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
           if (rr >= 0 && rr < n_cap) {
             row = (int)rr;
             tok = (int)(p / km.K);
-            if (sub == 0) row_to_pair[row] = (int32_t)p;
+            if (sub == 0 && col == 0) row_to_pair[row] = (int32_t)p;
           }
         }
       }
-      if (sub == 0) pair_to_row[p] = row;
+      if (sub == 0 && col == 0) pair_to_row[p] = row;
     }
     // this wavefront's share of the group's local pairs
     const uint64_t all = __ballot(row >= 0);
@@ -485,7 +491,7 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(
       bool dup[kRowsPerWave];
 #pragma unroll
       for (int r = 0; r < kRowsPerWave; ++r) dup[r] = r > 0 && toks[r] >= 0 && toks[r] == toks[r - 1];
-      for (int64_t v0 = 0; v0 < vec_per_row; v0 += 64 * kVecPerLane) {
+      for (int64_t v0 = (int64_t)col * 64 * kVecPerLane; v0 < vec_per_row; v0 += (int64_t)ncol * 64 * kVecPerLane) {
         uint4 a[kRowsPerWave][kVecPerLane];
 #pragma unroll
         for (int r = 0; r < kRowsPerWave; ++r) {
@@ -961,9 +967,13 @@ static int permute_impl(const void* x, foremoe_dtype dtype, int64_t T, int32_t d
   int nsub = 1;
   if (groups > 0 && groups < want) nsub = (int)((want + groups - 1) / groups);  // no pairs: one, idle
   nsub = nsub > 16 ? 16 : nsub;
-  hipLaunchKernelGGL(permute_gather_kernel, dim3(gather_grid(groups * nsub)), dim3(256), 0, st, (const uint4*)x, vpr,
-                     ids, npairs, km, nkeys, plan->R_max, base, rank, rep_begin, rep_slot, row_off, n_src * plan->S,
-                     slot_offset + plan->S, n_cap, pair_to_row, row_to_pair, (uint4*)x_perm, status, nsub);
+  // copy passes per row: one wavefront each (at most 8)
+  int ncol = (int)((vpr + 64 * kVecPerLane - 1) / (64 * kVecPerLane));
+  ncol = ncol < 1 ? 1 : (ncol > 8 ? 8 : ncol);
+  hipLaunchKernelGGL(permute_gather_kernel, dim3(gather_grid(groups * nsub * ncol)), dim3(256), 0, st,
+                     (const uint4*)x, vpr, ids, npairs, km, nkeys, plan->R_max, base, rank, rep_begin, rep_slot,
+                     row_off, n_src * plan->S, slot_offset + plan->S, n_cap, pair_to_row, row_to_pair,
+                     (uint4*)x_perm, status, nsub, ncol);
   return check_launch("foremoe_permute");
 }
 
