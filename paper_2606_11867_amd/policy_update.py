@@ -38,7 +38,8 @@ micro-steps run. The operands they read (x_perm, h, dy_perm, d_au and the
 slot offsets) live in a ring of 2M + 1 buffer sets; micro-step i rewrites
 the set of micro-step i - 2M - 1 only after the launch that read it is done.
 finish() launches the weight gradients of an incomplete last group.
-Micro-step indices between start() and finish() must be consecutive.
+Micro-step indices between start() and finish() must be consecutive, and
+the schedule (pipelined or not) the same.
 """
 from __future__ import annotations
 
@@ -136,12 +137,15 @@ class PolicyUpdate:
         # early_hist: the histogram + replica split of the micro-step using
         # set b, run on the second stream during the micro-step before it
         self.hdone = [Event(), Event()]
-        self._early: Dict[int, MicroStep] = {}  # micro-step index -> the inputs its early launch used
+        # micro-step index -> (inputs, activation set, weight-gradient set)
+        # its early launch used
+        self._early: Dict[int, tuple] = {}
         self._dep = [Event() for _ in range(8)]  # the cross-stream dependencies of one micro-step
         self._join = Event()
         self._ptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.sets]
         self._wptrs = [{k: v.data_ptr() for k, v in st.items()} for st in self.wsets]
         self.wmeta: List[Optional[MicroStep]] = [None] * self.R  # the micro-step whose operands a set holds
+        self._pipelined = False  # the schedule of the micro-steps run since start() / finish()
         self._first: Optional[int] = None  # first and last micro-step run since start() / finish()
         self._last: Optional[int] = None
         self._flush_stream = self.main
@@ -231,7 +235,9 @@ class PolicyUpdate:
         inputs of micro-step i + 1): micro-step i + 1's histogram + replica
         split runs on the second stream after this micro-step's down forward
         (beside its combine), and micro-step i + 1 starts with the permute;
-        except after the last micro-step of a weight-gradient group."""
+        except after the last micro-step of a weight-gradient group. The
+        returned operations must be run, in order (run() does): building
+        them consumes the record of such an early launch."""
         lib, main, side = self.lib, self.main, self.side
         overlap = overlap or pipelined
         bset, wset = self._indices(i, pipelined)
@@ -295,8 +301,10 @@ class PolicyUpdate:
         early = pipelined and early_hist
         run_hist = True
         if i in self._early:  # launched during micro-step i - 1: its writes land first
-            ops.append((None, lambda: self.hdone[bset].wait(main)))
-            run_hist = self._early.pop(i) is not ms  # other inputs than announced: run it again
+            ems, eb, ewb = self._early.pop(i)
+            ops.append((None, lambda: self.hdone[eb].wait(main)))
+            # other inputs than announced, or other sets (another schedule): run it again
+            run_hist = not (ems is ms and eb == bset and ewb == wset)
         if run_hist:
             call("histogram_assign", main, lambda q: lib.foremoe_histogram_assign(
                 ms.ids.data_ptr(), T, K, cp, P["counts"], P["rep_begin"], P["slot_count"], so, P["ws"], wsz, q))
@@ -331,7 +339,7 @@ class PolicyUpdate:
                 next_ms.ids.data_ptr(), T, K, ncp, NP["counts"], NP["rep_begin"], NP["slot_count"],
                 NP["slot_offset"], NP["ws"], self.sets[nb]["ws"].numel(), side.cuda_stream), "histogram_assign")))
             ops.append((None, lambda: self.hdone[nb].record(side)))
-            ops.append((None, lambda: self._early.__setitem__(j, next_ms)))
+            ops.append((None, lambda: self._early.__setitem__(j, (next_ms, nb, nwb))))
         if overlap and side_gathers >= 2:
             dep(side, main)
         call("combine", side if overlap and side_gathers >= 2 else main, lambda q: lib.foremoe_combine(
@@ -377,6 +385,10 @@ class PolicyUpdate:
     def run(self, i: int, ms: MicroStep, ev: Optional[dict] = None, overlap: bool = False,
             pipelined: bool = False, side_gathers: int = 0, fwd_after_side: bool = False,
             next_ms: Optional[MicroStep] = None, early_hist: bool = False) -> None:
+        if self._first is not None and pipelined != self._pipelined:
+            # the buffer sets and the waits that guard them depend on it
+            raise ValueError("pipelined cannot change between start() and finish()")
+        self._pipelined = pipelined
         ops = self.ops(i, ms, ev, overlap, pipelined, side_gathers, fwd_after_side, next_ms, early_hist)
         _, wset = self._indices(i, pipelined)
         self.wmeta[wset] = ms
