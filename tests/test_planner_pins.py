@@ -268,12 +268,12 @@ def test_stage4_two_replicated_experts_worked_example():
 def test_stage3_machine_confinement():
     # Two machines of two ranks, one base and one redundant slot per rank
     # (App. D: replicas stay inside their machine). Machine 0 holds e0 (500)
-    # and e1 (10): round 1 puts a replica of e0 on r1; round 2 picks e0
-    # again (250 per copy > 10) but r0 holds it and r1's slot is used, so
-    # the machine stops, although machine 1's ranks carry no load at all.
-    # Machine 1 holds e2, e3 with no load: round 1 takes e2 (equal loads per
-    # copy, lower id) onto r3; round 2 takes e2 again (0/2 = 0/1, lower id),
-    # which no rank can take.
+    # and e1 (10): the first pick puts a replica of e0 on r1; the second
+    # picks e0 again (250 per copy > 10) but r0 holds it and r1's slot is
+    # used, so the machine stops, although machine 1's ranks carry no load.
+    # Machine 1 holds e2, e3 with no load: the first pick takes e2 (equal
+    # loads per copy, lower id) onto r3; the second takes e2 again (0/2 =
+    # 0/1, lower id), which no rank can take.
     w = np.array([[500, 10, 0, 0], [0, 0, 0, 0], [0, 0, 0, 0], [0, 0, 0, 0]])
     mp = PL.policy_update_plan(w, np.array([0, 1, 2, 3]), M=2, R=2, N_b=1, N_r=1)
     assert mp.copies == [[0, 1], [1], [2, 3], [3]]
