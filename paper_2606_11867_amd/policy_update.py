@@ -166,7 +166,10 @@ class PolicyUpdate:
         return i % self.M == self.M - 1
 
     def start(self) -> None:
-        """Before the first pipelined micro-step: nothing to wait for yet."""
+        """Before the first pipelined micro-step: nothing to wait for yet, and
+        no early launch of an earlier sequence is used (its sets may have
+        been rewritten since)."""
+        self._early.clear()
         for e in self.done + self.gdone:
             e.record(self.side)
 
