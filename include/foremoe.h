@@ -244,7 +244,9 @@ int foremoe_dispatch_static(const int32_t* ids, int64_t T, int32_t K, const fore
 /*
  * Step 4, forward (App. A: SwiGLU expert with gate, up and down matrices).
  * For each slot j, rows [slot_offset[j], slot_offset[j+1]) (clamped to
- * n_cap), with w = slot_widx[j]:
+ * n_cap), with w = slot_widx[j] (a slot with w outside [0, W) is skipped by
+ * this and the input-gradient calls: its rows of every output keep what
+ * they held):
  *   A = X Wg[w]^T, U = X Wu[w]^T      (fp32 accumulate)
  *   H = silu(A) * U,  silu(a) = a / (1 + exp(-a))
  *   Y = H Wd[w]^T

@@ -184,3 +184,55 @@ def test_n_split_last_round(gpu, F, rows):
         check_close(f"dX (run {i})", to_np(run["dx"][rt]), g["dX"])
         check_close(f"H (run {i})", to_np(run["h"][rt]), f["H"])
         check_close(f"dA (run {i})", to_np(run["d_au"][rt][:, :F]), g["dA"])
+
+
+def test_invalid_weight_index_slot_is_skipped(gpu):
+    """A slot whose weight index is outside [0, W) is skipped by every row
+    GEMM: its rows of every output keep what they held, and no arrival
+    counter is left set, also when the last round is cut into halves and K
+    pieces (here halves in 2 pieces for the gate/up forward, in 4 for the
+    down dgrad); the other slots' rows match the oracle."""
+    from paper_2606_11867_amd import _lib, api
+    F, rows, widx = 256, [3000, 2000, 700], [0, -1, W]
+    grid = torch.cuda.get_device_properties(gpu).multi_processor_count
+    if grid == 256:
+        assert expected_layout(rows, 2 * F, D, grid) == (2, 2) and expected_layout(rows, F, D, grid) == (2, 4)
+    rng = np.random.default_rng(23)
+    off = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    N = int(off[-1])
+    x = bf16_round(rng.standard_normal((N, D)).astype(np.float32))
+    dy = bf16_round(rng.standard_normal((N, D)).astype(np.float32))
+    gu = bf16_round((rng.standard_normal((W, 2 * F, D)) / np.sqrt(D)).astype(np.float32))
+    dn = bf16_round((rng.standard_normal((W, D, F)) / np.sqrt(F)).astype(np.float32))
+    au_in = bf16_round((2.0 * rng.standard_normal((N, 2 * F))).astype(np.float32))
+    bf = torch.bfloat16
+    dev = lambda a: torch.from_numpy(a).to(gpu).to(bf)  # noqa: E731
+    xd, dyd, gud, dnd, aud = dev(x), dev(dy), dev(gu), dev(dn), dev(au_in)
+    so = torch.from_numpy(off).to(gpu)
+    wi = torch.from_numpy(np.array(widx, dtype=np.int32)).to(gpu)
+    ws = api.ffn_workspace(gpu)
+    sentinel = 7.0
+    h, y, au = (torch.full((N, c), sentinel, dtype=bf, device=gpu) for c in (F, D, 2 * F))
+    d_au, dx = (torch.full((N, c), sentinel, dtype=bf, device=gpu) for c in (2 * F, D))
+    lib = _lib.load()
+    st = torch.cuda.current_stream(gpu).cuda_stream
+    print(f"\n[case] slots {rows} with weight indices {widx} (W={W}), F={F}", flush=True)
+    assert lib.foremoe_grouped_ffn_fwd(xd.data_ptr(), _lib.BF16, D, F, len(rows), so.data_ptr(), wi.data_ptr(), W,
+                                       gud.data_ptr(), dnd.data_ptr(), N, h.data_ptr(), y.data_ptr(), au.data_ptr(),
+                                       ws.data_ptr(), ws.numel(), st) == 0
+    assert lib.foremoe_grouped_ffn_dgrad(dyd.data_ptr(), aud.data_ptr(), _lib.BF16, D, F, len(rows), so.data_ptr(),
+                                         wi.data_ptr(), W, gud.data_ptr(), dnd.data_ptr(), N, d_au.data_ptr(),
+                                         dx.data_ptr(), ws.data_ptr(), ws.numel(), st) == 0
+    torch.cuda.synchronize()
+    assert not ws[:4096].any().item(), "split arrival counters not reset"
+    skipped = slice(int(off[1]), N)  # slots 1 and 2
+    for name, t in (("H", h), ("Y", y), ("A|U", au), ("dA|dU", d_au), ("dX", dx)):
+        assert bool((t[skipped] == sentinel).all()), f"{name}: rows of a skipped slot were written"
+    n0 = int(off[1])
+    sub, sw = np.array([0, n0]), np.array([0])
+    f = O.ffn_forward(x[:n0].astype(np.float64), sub, sw, gu, dn)
+    g = O.ffn_dgrad(dy[:n0].astype(np.float64), au_in[:n0, :F], au_in[:n0, F:], sub, sw, gu, dn)
+    check_close("H (slot 0)", to_np(h[:n0]), f["H"])
+    check_close("Y (slot 0)", to_np(y[:n0]), f["Y"])
+    check_close("dA (slot 0)", to_np(d_au[:n0, :F]), g["dA"])
+    check_close("dX (slot 0)", to_np(dx[:n0]), g["dX"])
