@@ -191,3 +191,42 @@ def test_early_histogram_falls_back_when_inputs_differ(gpu, wgrad_group):
         check_close(f"dx[{i}]", to_np(outs[i]["dx"]), bwd["dx"])
     check_close("dW_gate_up", to_np(pu.dw_gate_up), rgu)
     check_close("dW_down", to_np(pu.dw_down), rdn)
+
+
+def test_benchmark_dispatch_bit_exact_every_micro_step(gpu):
+    """Steps 1-3 of all 16 micro-steps of the benchmark's workload, called as
+    the benchmark calls them (foremoe_histogram_assign, then foremoe_permute;
+    n_cap = T * K; one workspace reused from micro-step to micro-step, so
+    each call starts on what the previous one left): counts, replica bounds,
+    slot counts and offsets, both index maps and the permuted rows are
+    bit-exact against the oracle (Sec. 5 counts, Sec. 7.2 contiguous replica
+    split, Sec. 9 dispatch)."""
+    from paper_2606_11867_amd import api
+    w = config_workload(NAME)
+    T, K = w.micro[0].ids.shape
+    n_cap = T * K
+    ws = api.workspace(T, K, w.spec.E, gpu)
+    for m in w.micro:
+        print(f"\n[case] dispatch of micro-step {m.index}", flush=True)
+        counts, invalid = O.histogram(m.ids, m.plan.E)
+        rb, sc, so = O.assign_replicas(counts, m.plan)
+        N = int(so[-1])
+        # no pair is dropped at either n_cap, so the maps agree
+        xr = w.x(m.index)
+        x_perm, r2p, p2r, dropped = O.permute(xr, m.ids, m.plan, rb, so, N + 37)
+        assert dropped == 0
+        ids = torch.from_numpy(m.ids).to(gpu)
+        plan = api.DevicePlan.from_host(m.plan, gpu)
+        g_counts, g_rb, g_sc, g_so = api.histogram_assign(ids, plan, ws)
+        xd = to_dev(xr, torch.bfloat16, gpu)
+        g_xp, g_r2p, g_p2r = api.permute(xd, ids, plan, g_rb, g_so, n_cap, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(g_counts.cpu().numpy(), counts)
+        assert np.array_equal(g_rb.cpu().numpy(), rb)
+        assert np.array_equal(g_sc.cpu().numpy(), sc)
+        assert np.array_equal(g_so.cpu().numpy(), so)
+        assert np.array_equal(g_p2r.cpu().numpy(), p2r)
+        assert np.array_equal(g_r2p.cpu().numpy()[:N], r2p[:N])
+        assert np.array_equal(to_np(g_xp[:N]), x_perm[:N])  # bf16 -> f64 is exact
+        status = ws[:256].view(torch.int32).cpu().numpy()
+        assert status[0] == invalid and status[1] == 0 and status[2] == 0
