@@ -63,6 +63,44 @@ def test_dispatch_bit_exact(gpu, name, fused):
     assert status[63] == 0, "histogram_assign ticket not reset"
 
 
+def test_dispatch_bit_exact_every_dsv3_micro_step(gpu):
+    """Steps 1-3 of all 16 micro-steps of the DeepSeek-V3 EP=32 share (T*K =
+    262144 pairs, E = 256: the largest key count the fused
+    histogram + replica split takes), through foremoe_histogram_assign as
+    the benchmark calls it, one workspace reused, bit-exact against the
+    oracle. The index maps do not depend on the row width, so the rows
+    copied here are 256 wide (seeded) instead of 7168."""
+    from paper_2606_11867_amd import api
+    w = _wl("dsv3")
+    T, K = w.micro[0].ids.shape
+    rng = np.random.default_rng(71)
+    x = rng.standard_normal((T, 256))
+    xd = to_dev(x, torch.bfloat16, gpu)
+    x = to_np(xd)  # the rows as stored (bf16)
+    ws = api.workspace(T, K, w.spec.E, gpu)
+    for m in w.micro:
+        print(f"\n[case] dsv3 dispatch, micro-step {m.index}", flush=True)
+        counts, invalid = O.histogram(m.ids, m.plan.E)
+        rb, sc, so = O.assign_replicas(counts, m.plan)
+        N = int(so[-1])
+        x_perm, r2p, p2r, dropped = O.permute(x, m.ids, m.plan, rb, so, N + 37)
+        ids = torch.from_numpy(m.ids).to(gpu)
+        plan = api.DevicePlan.from_host(m.plan, gpu)
+        g_counts, g_rb, g_sc, g_so = api.histogram_assign(ids, plan, ws)
+        g_xp, g_r2p, g_p2r = api.permute(xd, ids, plan, g_rb, g_so, N + 37, ws)
+        torch.cuda.synchronize()
+        assert dropped == 0
+        assert np.array_equal(g_counts.cpu().numpy(), counts)
+        assert np.array_equal(g_rb.cpu().numpy(), rb)
+        assert np.array_equal(g_sc.cpu().numpy(), sc)
+        assert np.array_equal(g_so.cpu().numpy(), so)
+        assert np.array_equal(g_p2r.cpu().numpy(), p2r)
+        assert np.array_equal(g_r2p.cpu().numpy()[:N], r2p[:N])
+        assert np.array_equal(to_np(g_xp[:N]), x_perm[:N])
+        status = ws[:256].view(torch.int32).cpu().numpy()
+        assert status[0] == invalid and status[1] == 0 and status[2] == 0
+
+
 def test_histogram_assign_stale_workspace(gpu):
     """A workspace full of garbage (a nonzero arrival ticket, as after a call
     that did not complete or a workspace never zero-filled) still gives the
